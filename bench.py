@@ -1,0 +1,181 @@
+"""Benchmark: prefix-cached paged extend attention on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload turn]
+
+One step = one pass of the hot path over one batch: cw_kv_write_pages (the
+new K/V into their pages) then cw_extend_attention (the new tokens over the
+cached prefix and themselves).  The default workload is the single agent turn
+(prefix 16384, suffix 1024, 32 query / 8 kv heads, head_dim 128, page 16,
+bf16, pages randomly permuted in a 4096-page pool).  Inputs are synthetic,
+seeded, and resident in HBM before timing starts.
+
+Prints one JSON line: value = algorithmic extend TFLOP/s of the whole step
+(4 * D * Hq * sum(Ls*Lp + Ls(Ls+1)/2) FLOPs per step), plus the roofline of
+the extend kernel timed alone with HIP events, and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 2.4 GHz x 4096 FLOP/clk (dense bf16 MFMA)
+PEAK_HBM_GBS = 8000.0
+
+WORKLOAD_DESC = {
+    "tiny": "tiny extend: prefix 256, suffix 64, 4q/1kv, D=64, P=16",
+    "turn": "single agent turn: prefix 16384, suffix 1024, 32q/8kv (GQA 4), D=128, P=16, bf16, 4096-page permuted pool",
+    "batch16": "16 agent turns sharing an 8192-token prefix, prefix lognormal(20k) 4k-64k, suffix U[200,4000], 32q/8kv, D=128, P=16, bf16",
+    "long": "long-session extend: prefix 131072, suffix 8192, 64q/8kv (GQA 8), D=128, P=64, bf16",
+    "mixed": "mixed step: 48 decodes + 16 extends, 32q/8kv, D=128, P=16, fp8-e4m3fn pool",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="turn", choices=list(WORKLOAD_DESC))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample (0 disables)")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, target_s: float):
+    """The oracle (float64, blocked) on the first suffix tokens of sequence 0."""
+    import oracle
+    from tests.conftest import paged_inputs
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    inp = paged_inputs(w)
+    s = w.spec
+    lp, ls = int(s.prefix_lens[0]), int(s.suffix_lens[0])
+
+    def run(n_tok):
+        sub = oracle.PagedInputs(inp.q[:n_tok], inp.k_new[:n_tok], inp.v_new[:n_tok], inp.k_pool,
+                                 inp.v_pool, inp.block_table[:1], np.array([lp]), np.array([n_tok]),
+                                 inp.gqa_group, inp.softmax_scale, inp.kv_dtype, inp.k_scale,
+                                 inp.v_scale)
+        t0 = time.perf_counter()
+        oracle.extend_attention_blocked(sub, block_tokens=64)
+        return time.perf_counter() - t0
+
+    n = min(16, ls)
+    dt = run(n)
+    if dt < target_s and n < ls:
+        n = int(min(ls, max(n + 1, n * target_s / max(dt, 1e-3))))
+        dt = run(n)
+    pairs = n * lp + n * (n + 1) // 2
+    flops = 4.0 * s.head_dim * s.num_q_heads * pairs
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} of {ls} suffix tokens of sequence 0, all {s.num_q_heads} query heads "
+                      f"(float64 blocked oracle), {dt:.1f} s",
+            "tok_s": n / dt}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    import cw_workloads as cw
+    import paper_2606_16824_amd as cwlib
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    w = cw.make(args.workload)
+    s = w.spec
+    print(f"[bench] workload {args.workload}: {s.num_seqs} seqs, {s.total_new_tokens} new tokens, "
+          f"{s.flops() / 1e12:.3f} TFLOP", file=sys.stderr, flush=True)
+    mv = lambda t: None if t is None else t.to(dev).contiguous()
+    q, kn, vn, kp, vp = mv(w.q), mv(w.k_new), mv(w.v_new), mv(w.k_pool), mv(w.v_pool)
+    ks, vs, bt = mv(w.k_scale), mv(w.v_scale), mv(w.block_table)
+    out = torch.empty_like(q)
+    lse = torch.empty(q.shape[0], q.shape[1], device=dev, dtype=torch.float32)
+    ws_ext = torch.empty(cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
+                                                      s.gqa_group, s.head_dim, s.page_size),
+                         dtype=torch.uint8, device=dev)
+    ws_wr = torch.empty(cwlib.write_pages_workspace_bytes(s.num_seqs), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        cwlib.kv_write_pages(kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, k_scale=ks,
+                             v_scale=vs, workspace=ws_wr)
+        cwlib.extend_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, s.gqa_group,
+                               s.softmax_scale, k_scale=ks, v_scale=vs, out=out, lse=lse,
+                               workspace=ws_ext)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps, kernel-only events recorded by the library
+    lib = cwlib.library()
+    k_starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    k_stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    for e in k_starts + k_stops:  # torch creates the HIP event on first record
+        e.record(stream)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        lib.cw_set_timing_events(k_starts[i].cuda_event, k_stops[i].cuda_event)
+        assert k_starts[i].cuda_event and k_stops[i].cuda_event
+        step()
+    t_stop.record(stream)
+    torch.cuda.synchronize()
+    lib.cw_set_timing_events(None, None)
+    total_ms = t_start.elapsed_time(t_stop)
+    ms = total_ms / args.steps
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)]))
+    flops = s.flops()
+    value = flops / (ms * 1e-3) / 1e12
+    achieved = flops / (kern_ms * 1e-3) / 1e12
+    print(f"[bench] step {ms:.4f} ms, extend kernel {kern_ms:.4f} ms, {achieved:.1f} TFLOP/s kernel",
+          file=sys.stderr, flush=True)
+
+    result = {
+        "metric": "extend-attn TFLOP/s (% bf16 MFMA peak) + new tok/s; decode HBM GB/s % peak",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if s.kv_dtype == "bf16" else "bf16+fp8kv",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_DESC[args.workload], "new_tokens": s.total_new_tokens,
+                   "tflop_per_step": round(flops / 1e12, 5), "seed": s.seed},
+        "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "kernel": "extend_kernel", "kernel_ms": round(kern_ms, 5)},
+    }
+    if args.cpu_seconds > 0:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

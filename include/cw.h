@@ -1,0 +1,172 @@
+/*
+ * cw.h -- prefix-cached paged extend attention on MI355X (gfx950).
+ *
+ * The computation behind the CacheWise KV-cache policy (CacheWise, Sec. 2:
+ * KV prefixes persist in fixed-size blocks and later requests that extend a
+ * prefix reuse them; Sec. 3: each agent turn reuses and extends a growing
+ * prefix; Sec. 6.1: GQA/MQA models served with chunked prefill).  A new turn's
+ * suffix tokens attend causally to themselves and to the cached prefix whose
+ * K/V sit in a paged pool reached through a per-sequence block table.
+ *
+ * Semantics (sequence b, prefix length Lp, suffix length Ls, GQA group G):
+ *   suffix row i of b is packed row cu_b + i, cu = exclusive prefix sum of
+ *   suffix_lens; it sits at absolute position Lp + i and attends to keys
+ *   0 .. Lp + i (bottom-right causal alignment).  Query head h uses kv head
+ *   h / G.  Key j < Lp is slot j % P of physical page block_table[b][j / P]
+ *   of the pool; key Lp + i is row cu_b + i of k_new / v_new.
+ *   out = softmax(scale * q K^T) V per row, lse = natural log of the softmax
+ *   denominator including the row maximum (m + ln sum exp(s - m)).
+ *
+ * Layouts (row-major, last dimension contiguous):
+ *   q, out          bf16 [T, Hq, D]         T = sum of suffix_lens, Hq = Hkv * G
+ *   k_new, v_new    bf16 [T, Hkv, D]
+ *   k_pool, v_pool  bf16 or fp8-e4m3fn [num_pages, Hkv, P, D]
+ *                   one (page, kv head) is P*D contiguous elements
+ *   k_scale,v_scale fp32 [num_pages, Hkv]   fp8 pools only (NULL for bf16):
+ *                   stored value = code * scale of its (page, kv head)
+ *   block_table     int32 [num_seqs, bt_stride]; entries at or past
+ *                   ceil((Lp+Ls)/P) are never read
+ *   lse             fp32 [T, Hq] or NULL
+ *   prefix_lens_h, suffix_lens_h   HOST int32 [num_seqs], read during the call
+ *
+ * Supported: head_dim 64 or 128; page_size 16 or 64; 1 <= gqa_group <= 16;
+ * softmax_scale finite and > 0.  In an fp8 pool only the cached prefix is fp8:
+ * the suffix keys/values come from the bf16 k_new / v_new.
+ *
+ * Ownership and ordering: the caller owns every buffer, including the
+ * workspace; the library keeps only a per-device cache of device properties
+ * and a small pinned host staging area it allocates on first use.  All work is
+ * enqueued on `stream`; returning CW_OK means enqueued, not finished; buffers
+ * must stay valid until the stream has passed the work.  Calls on one stream
+ * may share one workspace; calls that may run concurrently need separate ones.
+ *
+ * Errors: every argument is checked before anything is enqueued, so a call
+ * that returns an error has enqueued nothing.  A HIP failure while enqueuing
+ * returns CW_ERR_HIP; faults inside kernels surface, as usual with HIP, at a
+ * later synchronisation.  cw_last_error_message() returns a thread-local
+ * description of the last error.  No call throws or aborts.
+ *
+ * Preconditions the library does not check (checking would need device reads):
+ * page ids < num_pages; write slots of different sequences are disjoint;
+ * pages shared between sequences lie inside every sharer's prefix; out and
+ * lse alias no input.
+ */
+#ifndef CW_H_
+#define CW_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CW_OK = 0,
+  CW_ERR_NULL = 1,        /* a required pointer is NULL */
+  CW_ERR_UNSUPPORTED = 2, /* head_dim, page_size, gqa_group, dtype or scale not supported */
+  CW_ERR_BAD_LENS = 3,    /* negative length, Lp+Ls > bt_stride*P, or sizes overflow */
+  CW_ERR_ALIGN = 4,       /* a tensor or workspace pointer not 16-byte aligned */
+  CW_ERR_WORKSPACE = 5,   /* workspace_bytes smaller than the matching *_workspace_bytes() */
+  CW_ERR_HIP = 6          /* a HIP runtime call failed while enqueuing */
+} cw_status_t;
+
+typedef enum { CW_KV_BF16 = 0, CW_KV_FP8_E4M3FN = 1 } cw_kv_dtype_t;
+
+/* Scatter the new K/V rows into their pool slots (CacheWise Sec. 2: the KV of a
+ * request is kept in fixed-size blocks so a later turn can reuse it).
+ * For i < Ls_b: pos = Lp_b + i, page = block_table[b][pos / P], slot = pos % P;
+ * k_pool[page][h][slot][:] = k_new[cu_b + i][h][:] for every kv head h (and V).
+ * bf16 pool: a bit copy.  fp8 pool: code = nearest e4m3fn value (ties to even)
+ * of clamp(x / scale[page][h], -448, 448), x the bf16 value and the quotient an
+ * IEEE fp32 division; k_scale/v_scale are then required.  No other byte of the
+ * pools changes.  Workspace: cw_write_pages_workspace_bytes(num_seqs) bytes. */
+size_t cw_write_pages_workspace_bytes(int32_t num_seqs);
+cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                              const float* k_scale, const float* v_scale,
+                              const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                              const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                              int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
+                              int32_t page_size, cw_kv_dtype_t kv_dtype, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes cw_extend_attention needs for these lengths on the current
+ * device (work list plus split-K partials).  0 if the arguments are invalid. */
+size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                 int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                                 int32_t head_dim, int32_t page_size);
+
+/* Prefix-cached paged extend attention (CacheWise Sec. 2-3: a request that
+ * extends a cached prefix computes attention only for its new tokens, over the
+ * reused prefix blocks plus itself; Sec. 6.1: GQA).  See the file comment for
+ * the exact semantics and layouts.  Sequences with Ls = 0 own no rows; Lp = 0
+ * is plain causal self-attention.  Does not write the new K/V into the pool:
+ * cw_kv_write_pages does, and the two calls commute. */
+cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_new,
+                                const void* k_pool, const void* v_pool, const float* k_scale,
+                                const float* v_scale, const int32_t* block_table,
+                                int32_t bt_stride, int32_t num_pages,
+                                const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                                int32_t head_dim, int32_t page_size, float softmax_scale,
+                                cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream);
+
+/* Decode: every sequence has exactly one new token (CacheWise Sec. 2:
+ * continuous batching of decode steps).  Same as cw_extend_attention with all
+ * suffix lengths 1: q/out are [num_seqs, Hq, D], k_new/v_new [num_seqs, Hkv, D],
+ * and the new token sits at position prefix_lens_h[b]. */
+size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
+                                 int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                 int32_t page_size);
+cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_new,
+                                const void* k_pool, const void* v_pool, const float* k_scale,
+                                const float* v_scale, const int32_t* block_table,
+                                int32_t bt_stride, int32_t num_pages,
+                                const int32_t* prefix_lens_h, int32_t num_seqs,
+                                int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype,
+                                void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/* Tuning knobs for tests and benchmarks; every value gives the same results
+ * within floating-point tolerance.  Process-wide; set them before querying a
+ * workspace size, since they change the plan.
+ *   CW_TUNE_KV_CHUNK_TILES  0 = automatic split-K; n > 0 = split every key
+ *                           range into chunks of n 64-key tiles.
+ *   CW_TUNE_TARGET_WGS      0 = automatic; n > 0 = split-K until at least n
+ *                           workgroups are launched.
+ * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
+typedef enum { CW_TUNE_KV_CHUNK_TILES = 0, CW_TUNE_TARGET_WGS = 1 } cw_tune_key_t;
+cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value);
+
+/* Benchmark hook: when `start` and `stop` are non-NULL, every later
+ * cw_extend_attention / cw_decode_attention call records `start` on its stream
+ * right before the main attention kernel and `stop` right after it (before any
+ * split-K merge), so hipEventElapsedTime gives that kernel's duration alone.
+ * Pass NULL, NULL to stop.  Process-wide; the events stay owned by the caller. */
+cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop);
+
+/* Host-only view of the extend work plan, for tests of the planner: writes up
+ * to `capacity` work items of 8 int32 each, in launch order
+ * {seq, kv_head, first packed row, key begin, key end, partial slot or -1,
+ *  rows in tile, 0}; a seq of -1 marks an idle padding item.  Returns the
+ * number of items, or -1 if the arguments are invalid.  Makes no HIP call
+ * other than a cached device-property query, and works without a GPU. */
+int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                             int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                             int32_t head_dim, int32_t page_size, int32_t* items_out,
+                             int64_t capacity);
+
+const char* cw_status_string(cw_status_t status);
+const char* cw_last_error_message(void);
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t cw_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CW_H_ */

@@ -1,0 +1,163 @@
+"""Prefix-cached paged extend attention on MI355X: Python binding of libcw.so.
+
+Thin argument marshalling over the C ABI of include/cw.h: every function
+passes device pointers (``tensor.data_ptr()``), host length arrays and torch's
+current HIP stream to the library, which runs the HIP kernels.  There is no
+fallback: without the built library every call raises.
+
+    extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens,
+                     suffix_lens, gqa_group, softmax_scale, k_scale=None,
+                     v_scale=None, out=None, lse=None, workspace=None)
+    decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens,
+                     gqa_group, softmax_scale, ...)
+    kv_write_pages(k_new, v_new, k_pool, v_pool, block_table, prefix_lens,
+                   suffix_lens, k_scale=None, v_scale=None, workspace=None)
+
+Page size and head dim are read from the pool shape [num_pages, Hkv, P, D];
+an fp8 pool is a uint8 (or float8_e4m3fn) tensor of e4m3fn codes.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import _lib as L
+
+__all__ = ["CWError", "extend_attention", "decode_attention", "kv_write_pages",
+           "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
+           "set_tuning", "plan_items", "library"]
+
+
+class CWError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+def library():
+    return L.load()
+
+
+def _check(status: int):
+    if status != L.CW_OK:
+        lib = library()
+        raise CWError(status, lib.cw_last_error_message().decode(errors="replace"))
+
+
+def _lens(x) -> np.ndarray:
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+    return a
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None or a.size == 0 else a.ctypes.data
+
+
+def _dptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _kv_dtype(pool: torch.Tensor) -> int:
+    if pool.dtype == torch.bfloat16:
+        return L.CW_KV_BF16
+    if pool.dtype in (torch.uint8, torch.float8_e4m3fn):
+        return L.CW_KV_FP8_E4M3FN
+    raise ValueError(f"unsupported pool dtype {pool.dtype}")
+
+
+def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
+    if workspace is None:
+        return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    return workspace
+
+
+def write_pages_workspace_bytes(num_seqs: int) -> int:
+    return int(library().cw_write_pages_workspace_bytes(num_seqs))
+
+
+def extend_workspace_bytes(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim,
+                           page_size) -> int:
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    return int(library().cw_extend_workspace_bytes(_ptr(lp), _ptr(ls), len(lp), num_kv_heads,
+                                                   gqa_group, head_dim, page_size))
+
+
+def decode_workspace_bytes(prefix_lens, num_kv_heads, gqa_group, head_dim, page_size) -> int:
+    lp = _lens(prefix_lens)
+    return int(library().cw_decode_workspace_bytes(_ptr(lp), len(lp), num_kv_heads, gqa_group,
+                                                   head_dim, page_size))
+
+
+def set_tuning(key: int, value: int):
+    _check(library().cw_set_tuning(key, value))
+
+
+def plan_items(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page_size) -> np.ndarray:
+    """The extend work list in launch order, int32 [n, 8] (see cw_extend_plan_items)."""
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    lib = library()
+    n = lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
+                                 page_size, None, 0)
+    if n < 0:
+        raise CWError(L.CW_ERR_UNSUPPORTED, "invalid plan arguments")
+    out = np.zeros((max(n, 1), 8), dtype=np.int32)
+    lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
+                             page_size, out.ctypes.data, n)
+    return out[:n]
+
+
+def kv_write_pages(k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
+                   k_scale=None, v_scale=None, workspace=None):
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    num_pages, hkv, page, d = k_pool.shape
+    ws = _workspace(write_pages_workspace_bytes(len(lp)), k_pool.device, workspace)
+    _check(library().cw_kv_write_pages(
+        _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale), _dptr(v_scale),
+        _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls), len(lp), hkv, d,
+        page, _kv_dtype(k_pool), _dptr(ws), ws.numel(), _stream()))
+
+
+def extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
+                     gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None, lse=None,
+                     workspace=None):
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    num_pages, hkv, page, d = k_pool.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page), q.device, None)
+    _check(library().cw_extend_attention(
+        _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
+        _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
+        len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),
+        _dptr(lse), _dptr(workspace), workspace.numel(), _stream()))
+    return out
+
+
+def decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, gqa_group,
+                     softmax_scale, k_scale=None, v_scale=None, out=None, lse=None, workspace=None):
+    lp = _lens(prefix_lens)
+    num_pages, hkv, page, d = k_pool.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = _workspace(decode_workspace_bytes(lp, hkv, gqa_group, d, page), q.device, None)
+    _check(library().cw_decode_attention(
+        _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
+        _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), len(lp),
+        hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out), _dptr(lse),
+        _dptr(workspace), workspace.numel(), _stream()))
+    return out

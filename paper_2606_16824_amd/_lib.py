@@ -1,0 +1,58 @@
+"""ctypes declarations of libcw.so (the C ABI declared in include/cw.h)."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcw.so")
+
+CW_OK, CW_ERR_NULL, CW_ERR_UNSUPPORTED, CW_ERR_BAD_LENS, CW_ERR_ALIGN, CW_ERR_WORKSPACE, CW_ERR_HIP = range(7)
+CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1
+CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS = 0, 1
+
+_i32p = C.POINTER(C.c_int32)
+_fp = C.POINTER(C.c_float)
+_vp = C.c_void_p
+_i32 = C.c_int32
+_sz = C.c_size_t
+
+# name: (restype, argtypes)
+SIGNATURES = {
+    "cw_write_pages_workspace_bytes": (_sz, [_i32]),
+    "cw_kv_write_pages": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32,
+                                    _i32, _i32, _i32, C.c_int, _vp, _sz, _vp]),
+    "cw_extend_workspace_bytes": (_sz, [_vp, _vp, _i32, _i32, _i32, _i32, _i32]),
+    "cw_extend_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                      _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
+                                      _vp, _sz, _vp]),
+    "cw_decode_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32]),
+    "cw_decode_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
+                                      _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
+                                      _vp, _sz, _vp]),
+    "cw_set_tuning": (C.c_int, [C.c_int, _i32]),
+    "cw_set_timing_events": (C.c_int, [_vp, _vp]),
+    "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),
+    "cw_status_string": (C.c_char_p, [C.c_int]),
+    "cw_last_error_message": (C.c_char_p, []),
+    "cw_version": (_i32, []),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> C.CDLL:
+    """Loads libcw.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} not found: build the HIP library first "
+            "(python -m paper_2606_16824_amd.build)")
+    lib = C.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib

@@ -1,0 +1,88 @@
+"""Builds libcw.so (the C-ABI library) in-tree with hipcc for gfx950.
+
+Usage: python -m paper_2606_16824_amd.build [--jobs N]
+Every .hip / .cpp under csrc/ is compiled to an object in _build/ (in
+parallel), then linked into paper_2606_16824_amd/libcw.so.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "libcw.so")
+ARCH = "gfx950"
+
+HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
+
+COMMON = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
+    "-Wno-unused-function", "-Wno-unused-command-line-argument",
+    # no packed-FP32 VALU instructions in generated device code
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+]
+
+
+def sources():
+    out = []
+    for dirpath, _, files in os.walk(CSRC):
+        for f in sorted(files):
+            if f.endswith((".hip", ".cpp")):
+                out.append(os.path.join(dirpath, f))
+    return sorted(out)
+
+
+def _obj(src):
+    rel = os.path.relpath(src, CSRC).replace(os.sep, "__")
+    return os.path.join(BUILD, rel + ".o")
+
+
+def _compile(src):
+    obj = _obj(src)
+    lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
+    cmd = [HIPCC, *COMMON, *lang, "-c", src, "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    return src, r.returncode, r.stdout + r.stderr, cmd
+
+
+def build(jobs: int = 8, verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = sources()
+    errors = []
+    with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
+        for src, rc, log, cmd in ex.map(_compile, srcs):
+            if verbose or rc != 0:
+                print(" ".join(cmd), file=sys.stderr)
+            # the host pass does not know the packed-fp32 feature; drop that warning
+            log = "\n".join(l for l in log.splitlines() if "packed-fp32-ops" not in l)
+            if log.strip() and (verbose or rc != 0):
+                print(log, file=sys.stderr)
+            if rc != 0:
+                errors.append(src)
+    if errors:
+        raise RuntimeError("hipcc failed for: " + ", ".join(errors))
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp,
+           *[_obj(s) for s in srcs]]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        print(" ".join(cmd), "\n", r.stdout, r.stderr, file=sys.stderr)
+        raise RuntimeError("link of libcw.so failed")
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--jobs", type=int, default=8)
+    ap.add_argument("-v", "--verbose", action="store_true")
+    a = ap.parse_args()
+    print(build(a.jobs, a.verbose))

@@ -1,0 +1,458 @@
+// C ABI front end: argument validation, planning, plan upload, launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/cw.h"
+#include "cw_internal.h"
+#include "planner.h"
+
+namespace cw {
+namespace {
+
+thread_local std::string g_last_error;
+Tuning g_tuning;
+std::mutex g_tuning_mu;
+hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;  // guarded by g_tuning_mu
+
+cw_status_t fail(cw_status_t s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+cw_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(CW_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+Tuning current_tuning() {
+  std::lock_guard<std::mutex> g(g_tuning_mu);
+  return g_tuning;
+}
+
+// ---------------------------------------------------------------------------
+// per-device state
+
+constexpr int kMaxDevices = 64;
+constexpr int kStagingSlots = 8;
+
+struct StagingSlot {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+
+struct DeviceState {
+  std::once_flag props_once;
+  int32_t num_cus = 256;
+  int32_t num_xcds = 8;
+  std::mutex staging_mu;
+  StagingSlot slots[kStagingSlots];
+  int next_slot = 0;
+};
+
+DeviceState g_devices[kMaxDevices];
+
+// Current device, or -1 when no GPU runtime is usable (host-only queries).
+int current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return -1;
+  }
+  return (dev >= 0 && dev < kMaxDevices) ? dev : -1;
+}
+
+// Compute-unit and XCD count of the current device; MI355X defaults without one.
+void device_shape(int32_t* cus, int32_t* xcds) {
+  const int dev = current_device();
+  if (dev < 0) {
+    *cus = 256;
+    *xcds = 8;
+    return;
+  }
+  DeviceState& st = g_devices[dev];
+  std::call_once(st.props_once, [&]() {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) {
+      st.num_cus = n;
+      // gfx950 groups 32 CUs per XCD (256 CUs in 8 XCDs; a CPX partition is one XCD)
+      st.num_xcds = n >= 32 ? n / 32 : 1;
+    } else {
+      (void)hipGetLastError();
+    }
+  });
+  *cus = st.num_cus;
+  *xcds = st.num_xcds;
+}
+
+// Copies `bytes` of host data to `dst` on `stream` through a pinned staging
+// slot, so that the copy is asynchronous and the caller's host buffer can be
+// reused at once.  A slot is reused only after its previous copy completed.
+cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
+  if (bytes == 0) return CW_OK;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(CW_ERR_HIP, "device index %d out of range", dev);
+  DeviceState& st = g_devices[dev];
+  std::lock_guard<std::mutex> g(st.staging_mu);
+  StagingSlot& s = st.slots[st.next_slot];
+  st.next_slot = (st.next_slot + 1) % kStagingSlots;
+  if (s.ev == nullptr) {
+    e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+  }
+  if (s.pending) {
+    e = hipEventSynchronize(s.ev);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    s.pending = false;
+  }
+  if (s.cap < bytes) {
+    if (s.host) (void)hipHostFree(s.host);
+    s.host = nullptr;
+    s.cap = 0;
+    const size_t cap = std::max<size_t>(bytes, size_t(1) << 20);
+    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
+    s.cap = cap;
+  }
+  std::memcpy(s.host, src, bytes);
+  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  e = hipEventRecord(s.ev, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  s.pending = true;
+  return CW_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---------------------------------------------------------------------------
+// validation
+
+cw_status_t check_shape(int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                        int32_t page_size) {
+  if (num_seqs < 0) return fail(CW_ERR_BAD_LENS, "num_seqs = %d is negative", num_seqs);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CW_ERR_UNSUPPORTED, "head_dim = %d (supported: 64, 128)", head_dim);
+  if (page_size != 16 && page_size != 64)
+    return fail(CW_ERR_UNSUPPORTED, "page_size = %d (supported: 16, 64)", page_size);
+  if (num_kv_heads < 1 || num_kv_heads > 1024)
+    return fail(CW_ERR_UNSUPPORTED, "num_kv_heads = %d (supported: 1..1024)", num_kv_heads);
+  if (gqa_group < 1 || gqa_group > 16)
+    return fail(CW_ERR_UNSUPPORTED, "gqa_group = %d (supported: 1..16)", gqa_group);
+  return CW_OK;
+}
+
+// Lengths: non-negative, fit the block table, and the packed sizes fit int32.
+cw_status_t check_lens(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t bt_stride,
+                       int32_t page_size, int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                       bool check_table) {
+  if (num_seqs > 0 && (lp == nullptr || ls == nullptr))
+    return fail(CW_ERR_NULL, "prefix_lens_h / suffix_lens_h is NULL");
+  if (check_table && num_seqs > 0 && bt_stride < 1)
+    return fail(CW_ERR_BAD_LENS, "bt_stride = %d must be >= 1", bt_stride);
+  int64_t total = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    if (lp[b] < 0 || ls[b] < 0)
+      return fail(CW_ERR_BAD_LENS, "sequence %d: negative length (Lp=%d, Ls=%d)", b, lp[b], ls[b]);
+    const int64_t n = int64_t(lp[b]) + ls[b];
+    if (n > INT32_MAX / 2) return fail(CW_ERR_BAD_LENS, "sequence %d: Lp+Ls=%lld too long", b, (long long)n);
+    if (check_table && n > int64_t(bt_stride) * page_size)
+      return fail(CW_ERR_BAD_LENS, "sequence %d: Lp+Ls=%lld exceeds bt_stride*P=%lld", b,
+                  (long long)n, (long long)bt_stride * page_size);
+    total += ls[b];
+  }
+  const int64_t hq = int64_t(num_kv_heads) * gqa_group;
+  if (total * hq * head_dim > INT64_C(1) << 40 || total > INT32_MAX / 32)
+    return fail(CW_ERR_BAD_LENS, "total suffix tokens %lld too large", (long long)total);
+  (void)hq;
+  return CW_OK;
+}
+
+cw_status_t check_dtype(cw_kv_dtype_t kv_dtype, const float* k_scale, const float* v_scale) {
+  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN)
+    return fail(CW_ERR_UNSUPPORTED, "kv_dtype = %d", int(kv_dtype));
+  if (kv_dtype == CW_KV_FP8_E4M3FN && (k_scale == nullptr || v_scale == nullptr))
+    return fail(CW_ERR_NULL, "fp8 pool needs k_scale and v_scale");
+  return CW_OK;
+}
+
+int64_t sum_suffix(const int32_t* ls, int32_t num_seqs) {
+  int64_t t = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) t += ls[b];
+  return t;
+}
+
+ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t num_kv_heads,
+                     int32_t gqa_group, int32_t head_dim) {
+  int32_t cus = 256, xcds = 8;
+  device_shape(&cus, &xcds);
+  return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, cus, xcds,
+                           current_tuning());
+}
+
+cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, const void* k_pool,
+                        const void* v_pool, const float* k_scale, const float* v_scale,
+                        const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                        const int32_t* lp, const int32_t* ls, int32_t num_seqs,
+                        int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                        int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype, void* out,
+                        float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  cw_status_t s = check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size);
+  if (s != CW_OK) return s;
+  s = check_dtype(kv_dtype, k_scale, v_scale);
+  if (s != CW_OK) return s;
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(CW_ERR_UNSUPPORTED, "softmax_scale = %g (must be finite and > 0)", double(softmax_scale));
+  if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
+  s = check_lens(lp, ls, num_seqs, bt_stride, page_size, num_kv_heads, gqa_group, head_dim, true);
+  if (s != CW_OK) return s;
+  const int64_t total = sum_suffix(ls, num_seqs);
+  if (total == 0) return CW_OK;  // no rows: nothing to do
+  if (!q || !k_new || !v_new || !out || !block_table)
+    return fail(CW_ERR_NULL, "q, k_new, v_new, out and block_table are required");
+  bool any_prefix = false;
+  for (int32_t b = 0; b < num_seqs; ++b) any_prefix |= lp[b] > 0;
+  if (any_prefix && (!k_pool || !v_pool)) return fail(CW_ERR_NULL, "k_pool / v_pool is NULL");
+  if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out) ||
+      !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(workspace))
+    return fail(CW_ERR_ALIGN, "tensor and workspace pointers must be 16-byte aligned");
+  if (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)) return fail(CW_ERR_ALIGN, "lse not 4-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(block_table) & 3u)) return fail(CW_ERR_ALIGN, "block_table not 4-byte aligned");
+
+  ExtendPlan plan = make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim);
+  if (workspace == nullptr || workspace_bytes < plan.total_bytes)
+    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
+
+  std::vector<uint8_t> meta(plan.meta_bytes);
+  pack_plan_meta(plan, meta.data());
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  s = upload(meta.data(), meta.size(), ws, stream);
+  if (s != CW_OK) return s;
+
+  ExtendParams p{};
+  p.q = q;
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.k_pool = k_pool;
+  p.v_pool = v_pool;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.block_table = block_table;
+  p.out = out;
+  p.lse = lse;
+  p.seqs = reinterpret_cast<const SeqInfo*>(ws + plan.off_seqs);
+  p.items = reinterpret_cast<const WorkItem*>(ws + plan.off_items);
+  p.groups = reinterpret_cast<const CombineGroup*>(ws + plan.off_groups);
+  p.part_o = reinterpret_cast<float*>(ws + plan.off_part_o);
+  p.part_ml = reinterpret_cast<float*>(ws + plan.off_part_ml);
+  p.bt_stride = bt_stride;
+  p.num_kv_heads = num_kv_heads;
+  p.gqa_group = gqa_group;
+  p.num_seqs = num_seqs;
+  p.scale_log2 = softmax_scale * 1.4426950408889634f;
+  p.n_items = static_cast<int32_t>(plan.items.size());
+  p.n_groups = static_cast<int32_t>(plan.groups.size());
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  {
+    std::lock_guard<std::mutex> g(g_tuning_mu);
+    ev0 = g_ev_start;
+    ev1 = g_ev_stop;
+  }
+  hipError_t e = hipSuccess;
+  if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  e = launch_extend(p, head_dim, page_size, kv_dtype == CW_KV_FP8_E4M3FN, stream);
+  if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
+  if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if (p.n_groups > 0) {
+    e = launch_combine(p, head_dim, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
+  }
+  return CW_OK;
+}
+
+}  // namespace
+}  // namespace cw
+
+using namespace cw;
+
+extern "C" {
+
+size_t cw_write_pages_workspace_bytes(int32_t num_seqs) {
+  if (num_seqs < 0) return 0;
+  return std::max<size_t>(256, (size_t(num_seqs) * sizeof(SeqInfo) + 255) & ~size_t(255));
+}
+
+cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                              const float* k_scale, const float* v_scale,
+                              const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                              const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                              int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
+                              int32_t page_size, cw_kv_dtype_t kv_dtype, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  cw_status_t s = check_shape(num_seqs, num_kv_heads, 1, head_dim, page_size);
+  if (s != CW_OK) return s;
+  s = check_dtype(kv_dtype, k_scale, v_scale);
+  if (s != CW_OK) return s;
+  if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
+  s = check_lens(prefix_lens_h, suffix_lens_h, num_seqs, bt_stride, page_size, num_kv_heads, 1,
+                 head_dim, true);
+  if (s != CW_OK) return s;
+  const int64_t total = sum_suffix(suffix_lens_h, num_seqs);
+  if (total == 0) return CW_OK;
+  if (!k_new || !v_new || !k_pool || !v_pool || !block_table)
+    return fail(CW_ERR_NULL, "k_new, v_new, k_pool, v_pool and block_table are required");
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool) ||
+      !aligned16(workspace))
+    return fail(CW_ERR_ALIGN, "tensor and workspace pointers must be 16-byte aligned");
+  const size_t need = cw_write_pages_workspace_bytes(num_seqs);
+  if (workspace == nullptr || workspace_bytes < need)
+    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  std::vector<SeqInfo> seqs(num_seqs);
+  int64_t cu = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), 0};
+    cu += suffix_lens_h[b];
+  }
+  s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
+  if (s != CW_OK) return s;
+  WriteParams p{};
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.k_pool = k_pool;
+  p.v_pool = v_pool;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.block_table = block_table;
+  p.seqs = static_cast<const SeqInfo*>(workspace);
+  p.bt_stride = bt_stride;
+  p.num_seqs = num_seqs;
+  p.num_kv_heads = num_kv_heads;
+  p.total_tokens = static_cast<int32_t>(total);
+  hipError_t e = launch_write_pages(p, head_dim, page_size, kv_dtype == CW_KV_FP8_E4M3FN, stream);
+  if (e != hipSuccess) return hip_fail(e, "write_pages kernel launch");
+  return CW_OK;
+}
+
+size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                 int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                                 int32_t head_dim, int32_t page_size) {
+  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+  if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                 head_dim, false) != CW_OK)
+    return 0;
+  if (num_seqs == 0) return 256;
+  return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim).total_bytes;
+}
+
+cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_new,
+                                const void* k_pool, const void* v_pool, const float* k_scale,
+                                const float* v_scale, const int32_t* block_table,
+                                int32_t bt_stride, int32_t num_pages,
+                                const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                                int32_t head_dim, int32_t page_size, float softmax_scale,
+                                cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, hipStream_t stream) {
+  return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
+                     num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
+                     head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
+                     workspace_bytes, stream);
+}
+
+size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
+                                 int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                 int32_t page_size) {
+  if (num_seqs < 0) return 0;
+  std::vector<int32_t> ones(num_seqs, 1);
+  return cw_extend_workspace_bytes(prefix_lens_h, ones.data(), num_seqs, num_kv_heads, gqa_group,
+                                   head_dim, page_size);
+}
+
+cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_new,
+                                const void* k_pool, const void* v_pool, const float* k_scale,
+                                const float* v_scale, const int32_t* block_table,
+                                int32_t bt_stride, int32_t num_pages,
+                                const int32_t* prefix_lens_h, int32_t num_seqs,
+                                int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype,
+                                void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  if (num_seqs < 0) return fail(CW_ERR_BAD_LENS, "num_seqs = %d is negative", num_seqs);
+  std::vector<int32_t> ones(num_seqs, 1);
+  return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
+                     num_pages, prefix_lens_h, ones.data(), num_seqs, num_kv_heads, gqa_group,
+                     head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
+                     workspace_bytes, stream);
+}
+
+cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
+  if (value < 0) return fail(CW_ERR_UNSUPPORTED, "tuning value %d is negative", value);
+  std::lock_guard<std::mutex> g(g_tuning_mu);
+  switch (key) {
+    case CW_TUNE_KV_CHUNK_TILES: g_tuning.kv_chunk_tiles = value; return CW_OK;
+    case CW_TUNE_TARGET_WGS: g_tuning.target_wgs = value; return CW_OK;
+  }
+  return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));
+}
+
+cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop) {
+  std::lock_guard<std::mutex> g(g_tuning_mu);
+  g_ev_start = start;
+  g_ev_stop = stop;
+  return CW_OK;
+}
+
+int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                             int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                             int32_t head_dim, int32_t page_size, int32_t* items_out,
+                             int64_t capacity) {
+  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return -1;
+  if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                 head_dim, false) != CW_OK)
+    return -1;
+  ExtendPlan plan = make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim);
+  const int64_t n = static_cast<int64_t>(plan.items.size());
+  if (items_out) {
+    for (int64_t i = 0; i < std::min(n, capacity); ++i) {
+      const WorkItem& w = plan.items[i];
+      int32_t* o = items_out + 8 * i;
+      o[0] = w.seq; o[1] = w.kvh; o[2] = w.q_row0; o[3] = w.kv_begin;
+      o[4] = w.kv_end; o[5] = w.part; o[6] = w.rows; o[7] = 0;
+    }
+  }
+  return n;
+}
+
+const char* cw_status_string(cw_status_t status) {
+  switch (status) {
+    case CW_OK: return "CW_OK";
+    case CW_ERR_NULL: return "CW_ERR_NULL: a required pointer is NULL";
+    case CW_ERR_UNSUPPORTED: return "CW_ERR_UNSUPPORTED: unsupported shape, dtype or parameter";
+    case CW_ERR_BAD_LENS: return "CW_ERR_BAD_LENS: invalid sequence lengths";
+    case CW_ERR_ALIGN: return "CW_ERR_ALIGN: misaligned pointer";
+    case CW_ERR_WORKSPACE: return "CW_ERR_WORKSPACE: workspace too small";
+    case CW_ERR_HIP: return "CW_ERR_HIP: HIP runtime error";
+  }
+  return "unknown cw_status_t";
+}
+
+const char* cw_last_error_message(void) { return g_last_error.c_str(); }
+
+int32_t cw_version(void) { return 100; }
+
+}  // extern "C"

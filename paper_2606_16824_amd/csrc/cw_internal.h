@@ -1,0 +1,102 @@
+// Internal types shared by the host front end, the planner and the kernels.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace cw {
+
+// Tile shape of the extend kernel: a workgroup owns BLOCK_M packed query rows
+// (row = token * G + group member) of one (sequence, kv head) and walks keys
+// BLOCK_N at a time.
+constexpr int BLOCK_M = 128;
+constexpr int BLOCK_N = 64;
+constexpr int WAVES = 4;  // four wave64s, 32 query rows each
+constexpr int THREADS = WAVES * 64;
+
+// Per-sequence metadata on the device.
+struct SeqInfo {
+  int32_t lp;  // cached prefix length
+  int32_t ls;  // suffix length
+  int32_t cu;  // first packed token row of the sequence
+  int32_t pad;
+};
+
+// One workgroup's share of the extend: packed query rows
+// [q_row0, q_row0 + rows) of sequence `seq`, kv head `kvh`, keys
+// [kv_begin, kv_end).  part >= 0 writes an unnormalised split-K partial.
+struct WorkItem {
+  int32_t seq;  // -1: idle padding item
+  int32_t kvh;
+  int32_t q_row0;
+  int32_t kv_begin;
+  int32_t kv_end;
+  int32_t part;
+  int32_t rows;
+  int32_t pad;
+};
+
+// A query tile whose key range was split: `n_parts` partial slots starting at
+// `part0` are merged into the output.
+struct CombineGroup {
+  int32_t seq;
+  int32_t kvh;
+  int32_t q_row0;
+  int32_t rows;
+  int32_t part0;
+  int32_t n_parts;
+  int32_t pad0;
+  int32_t pad1;
+};
+
+struct ExtendParams {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  const void* k_pool;
+  const void* v_pool;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* block_table;
+  void* out;
+  float* lse;
+  const SeqInfo* seqs;
+  const WorkItem* items;
+  const CombineGroup* groups;
+  float* part_o;   // [n_parts, BLOCK_M, D]
+  float* part_ml;  // [n_parts, BLOCK_M, 2]  (running max in log2 units, sum)
+  int32_t bt_stride;
+  int32_t num_kv_heads;
+  int32_t gqa_group;
+  int32_t num_seqs;
+  float scale_log2;  // softmax_scale * log2(e)
+  int32_t n_items;
+  int32_t n_groups;
+  int32_t pad;
+};
+
+struct WriteParams {
+  const void* k_new;
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* block_table;
+  const SeqInfo* seqs;
+  int32_t bt_stride;
+  int32_t num_seqs;
+  int32_t num_kv_heads;
+  int32_t total_tokens;
+};
+
+// Kernel launchers (each defined in the translation unit of its kernel).
+hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
+                         hipStream_t stream);
+hipError_t launch_combine(const ExtendParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size, bool fp8,
+                              hipStream_t stream);
+
+}  // namespace cw

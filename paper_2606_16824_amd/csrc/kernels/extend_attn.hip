@@ -1,0 +1,407 @@
+// Prefix-cached paged extend attention, bf16 MFMA on gfx950.
+//
+// One workgroup = four wave64s = BLOCK_M (128) packed query rows of one
+// (sequence, kv head); packed row r is token r / G, query head kvh * G + r % G,
+// so one staged key/value tile serves the whole GQA group.  Keys are walked
+// BLOCK_N (64) at a time over [kv_begin, kv_end); key j < Lp comes from the page
+// pool through the block table, key j >= Lp from k_new / v_new.
+//
+// Per tile, each wave computes S^T = K Q^T (keys x its 32 rows) with
+// v_mfma_f32_32x32x16_bf16, so that a lane owns one query row: the row max is a
+// max over the lane's 32 values plus one exchange with the other half-wave, and
+// the softmax statistics and the O rescale stay in the lane.  Then
+// O^T += V^T P^T with P rounded to bf16; V is stored transposed in LDS so that
+// the contraction (key) dimension is contiguous for the MFMA operand.
+//
+// MFMA 32x32x16 operand layouts (wave64, lane l, half h = l / 32):
+//   A[m][k]: lane m + 32 * (k / 8), element k % 8
+//   B[k][n]: lane n + 32 * (k / 8), element k % 8
+//   C[m][n]: lane n + 32 * ((m / 4) % 2), element (m % 4) + 4 * (m / 8)
+// Row m of the S^T output held in element i of half h is m = 8(i/4) + 4h + i%4.
+// Reading A row m from key swap_bits_2_3(m) makes element i of half h hold key
+// 16(i/8) + 8h + i%8 (within a 32-key block), which is exactly the B-operand
+// order the P^T V product needs: P values feed the second MFMA without any
+// data movement across lanes.  K rows are stored in LDS at row swap(j) so the
+// A-operand reads stay linear.
+//
+// Softmax runs in base 2 with scale * log2(e) folded into one FMA; the running
+// max starts at a large negative finite value so that fully masked rows give
+// exp2(-inf) = 0 instead of NaN.  Masked keys are excluded by setting their
+// score to -inf; K/V rows past the sequence are staged as zeros, so stale or
+// NaN pool slots are never multiplied in.
+//
+// fp8-e4m3fn pools: codes are widened exactly to bf16 while staging (every
+// e4m3fn value is a bf16 value); the page's K scale multiplies the scores of
+// its keys and the V scale multiplies P before the bf16 rounding.
+#include <hip/hip_runtime.h>
+
+#include "../cw_internal.h"
+
+namespace cw {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kNegBig = -1.0e30f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+__device__ __forceinline__ int swap_bits_2_3(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+// Two e4m3fn codes (bytes 0,1 or 2,3 of `w`) -> two bf16 in one dword, exact.
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  f32x2 f = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w), HI);
+  const uint32_t a = __float_as_uint(f.x), b = __float_as_uint(f.y);
+  return (a >> 16) | (b & 0xFFFF0000u);  // the low 16 bits of an e4m3fn value are zero
+}
+
+__device__ __forceinline__ u32x4 fp8x8_to_bf16x8(u32x2 c) {
+  u32x4 r;
+  r.x = fp8x2_to_bf16x2<false>(c.x);
+  r.y = fp8x2_to_bf16x2<true>(c.x);
+  r.z = fp8x2_to_bf16x2<false>(c.y);
+  r.w = fp8x2_to_bf16x2<true>(c.y);
+  return r;
+}
+
+template <int D, int P, bool FP8>
+struct Tile {
+  static constexpr int KROW = D + 8;        // K tile row stride (elements): 16 B pad
+  static constexpr int VROW = BLOCK_N + 8;  // V^T tile row stride (elements)
+  static constexpr int K_CHUNKS = BLOCK_N * D / 8 / THREADS;  // 16-byte K chunks per thread
+  static constexpr int V_UNITS = 16 * (D / 8);                // (4 keys x 8 dims) V units
+  static constexpr int KT = D / 16;                            // k-steps of Q K^T
+  static constexpr int DB = D / 32;                            // 32-row blocks of O^T
+};
+
+// Global -> registers for one key/value tile (prefetched one tile ahead).
+template <int D, int P, bool FP8>
+struct TileRegs {
+  using T = Tile<D, P, FP8>;
+  u32x4 k[T::K_CHUNKS];  // bf16 K chunks (fp8 prefix rows already widened)
+  u32x4 v[4];            // 4 key rows x 8 dims of V (bf16)
+  float ks, vs;          // this thread's row scale (threads 0..63, fp8 only)
+};
+
+template <int D, int P, bool FP8>
+__device__ __forceinline__ u32x4 load_row8(const void* pool, const void* fresh, const int32_t* bt,
+                                           int j, int lp, int ls, int cu, int hkv, int kvh, int d0) {
+  u32x4 r = {0u, 0u, 0u, 0u};
+  if (j < lp) {
+    const int pg = bt[j / P];
+    const size_t off = ((size_t(pg) * hkv + kvh) * P + (j % P)) * D + d0;
+    if constexpr (FP8) {
+      r = fp8x8_to_bf16x8(*reinterpret_cast<const u32x2*>(static_cast<const uint8_t*>(pool) + off));
+    } else {
+      r = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(pool) + off);
+    }
+  } else if (j < lp + ls) {
+    const size_t off = (size_t(cu + j - lp) * hkv + kvh) * D + d0;
+    r = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(fresh) + off);
+  }
+  return r;
+}
+
+template <int D, int P, bool FP8>
+__global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
+  using T = Tile<D, P, FP8>;
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[BLOCK_N * T::KROW];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[D * T::VROW];
+  __shared__ __attribute__((aligned(16))) float ks_lds[BLOCK_N];
+  __shared__ __attribute__((aligned(16))) float vs_lds[BLOCK_N];
+
+  const WorkItem it = p.items[blockIdx.x];
+  if (it.seq < 0) return;  // idle padding item (uniform across the workgroup)
+  const SeqInfo sq = p.seqs[it.seq];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int G = p.gqa_group, hkv = p.num_kv_heads, hq = hkv * G;
+  const int kvh = it.kvh;
+  const int32_t* bt = p.block_table + size_t(it.seq) * p.bt_stride;
+
+  // this lane's query row and its causal limit (number of visible keys)
+  const int r_local = wave * 32 + col;
+  const bool row_ok = r_local < it.rows;
+  const int r = it.q_row0 + r_local;
+  const int t = r / G, g = r - t * G;
+  const int lim = row_ok ? sq.lp + t + 1 : 0x7FFFFFFF;
+  const bool wave_active = wave * 32 < it.rows;
+  const int wave_min_lim = sq.lp + (it.q_row0 + wave * 32) / G + 1;
+  const int wave_last_row = it.q_row0 + min(wave * 32 + 31, it.rows - 1);
+  const int wave_max_lim = sq.lp + wave_last_row / G + 1;
+
+  // Q^T as the B operand: k-step kk holds dims 16 kk + 8 h + [0, 8) of this row
+  bf16x8 qf[T::KT];
+  {
+    const uint16_t* qrow =
+        static_cast<const uint16_t*>(p.q) + (size_t(sq.cu + t) * hq + size_t(kvh) * G + g) * D;
+#pragma unroll
+    for (int kk = 0; kk < T::KT; ++kk) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (row_ok) v = *reinterpret_cast<const u32x4*>(qrow + 16 * kk + 8 * h);
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  f32x16 o[T::DB];
+#pragma unroll
+  for (int b = 0; b < T::DB; ++b) o[b] = f32x16{};
+  float m_run = kNegBig, l_run = 0.f;
+  const float c = p.scale_log2;
+
+  // staging assignment: K chunk i -> row (tid + 256 i) / (D/8), 16-byte column
+  // (tid + 256 i) % (D/8); V unit tid -> keys 4 (tid % 16) .. +3, dims 8 (tid / 16) .. +7
+  const int vkg = tid & 15, vdg = tid >> 4;
+  const bool v_unit = tid < T::V_UNITS;
+
+  TileRegs<D, P, FP8> regs;
+  auto load_tile = [&](int j0) {
+#pragma unroll
+    for (int i = 0; i < T::K_CHUNKS; ++i) {
+      const int cidx = tid + THREADS * i;
+      const int row = cidx / (D / 8), c8 = cidx % (D / 8);
+      regs.k[i] = load_row8<D, P, FP8>(p.k_pool, p.k_new, bt, j0 + row, sq.lp, sq.ls, sq.cu, hkv,
+                                       kvh, c8 * 8);
+    }
+    if (v_unit) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        regs.v[k] = load_row8<D, P, FP8>(p.v_pool, p.v_new, bt, j0 + 4 * vkg + k, sq.lp, sq.ls,
+                                         sq.cu, hkv, kvh, vdg * 8);
+    }
+    if constexpr (FP8) {
+      if (tid < BLOCK_N) {
+        const int j = j0 + tid;
+        regs.ks = 1.f;
+        regs.vs = 1.f;
+        if (j < sq.lp) {
+          const size_t si = size_t(bt[j / P]) * hkv + kvh;
+          regs.ks = p.k_scale[si];
+          regs.vs = p.v_scale[si];
+        }
+      }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < T::K_CHUNKS; ++i) {
+      const int cidx = tid + THREADS * i;
+      const int row = cidx / (D / 8), c8 = cidx % (D / 8);
+      *reinterpret_cast<u32x4*>(k_lds + swap_bits_2_3(row) * T::KROW + c8 * 8) = regs.k[i];
+    }
+    if (v_unit) {
+      // transpose 4 keys x 8 dims: dword w of row k holds dims 2w (low) and 2w+1 (high)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t a0 = regs.v[0][w], a1 = regs.v[1][w], a2 = regs.v[2][w], a3 = regs.v[3][w];
+        u32x2 lo, hi;
+        lo.x = (a0 & 0xFFFFu) | (a1 << 16);
+        lo.y = (a2 & 0xFFFFu) | (a3 << 16);
+        hi.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
+        hi.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
+        *reinterpret_cast<u32x2*>(v_lds + (vdg * 8 + 2 * w) * T::VROW + 4 * vkg) = lo;
+        *reinterpret_cast<u32x2*>(v_lds + (vdg * 8 + 2 * w + 1) * T::VROW + 4 * vkg) = hi;
+      }
+    }
+    if constexpr (FP8) {
+      if (tid < BLOCK_N) {
+        ks_lds[tid] = regs.ks;
+        vs_lds[tid] = regs.vs;
+      }
+    }
+  };
+
+  if (it.kv_begin < it.kv_end) load_tile(it.kv_begin);
+  for (int j0 = it.kv_begin; j0 < it.kv_end; j0 += BLOCK_N) {
+    __syncthreads();  // every wave is done reading the previous tile
+    store_tile();
+    __syncthreads();
+    if (j0 + BLOCK_N < it.kv_end) load_tile(j0 + BLOCK_N);  // in flight during the math
+
+    if (!wave_active || j0 >= wave_max_lim) continue;  // nothing visible for this wave
+
+    // S^T = K Q^T for two 32-key blocks
+    f32x16 s[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      s[blk] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < T::KT; ++kk) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+            k_lds + (32 * blk + col) * T::KROW + 16 * kk + 8 * h);
+        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[blk], 0, 0, 0);
+      }
+    }
+
+    // scores in log2 units, masked
+    const bool need_mask = j0 + BLOCK_N > wave_min_lim;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int kl = 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7);  // key within the tile
+        float x;
+        if constexpr (FP8) x = s[blk][i] * (c * ks_lds[kl]);
+        else x = s[blk][i];
+        if (need_mask && j0 + kl >= lim) x = -INFINITY;
+        s[blk][i] = x;
+        mx = fmaxf(mx, x);
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, FP8 ? mx : mx * c);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+
+    bf16x8 pf[4];
+    float psum = 0.f;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float pv;
+        if constexpr (FP8) pv = __builtin_amdgcn_exp2f(s[blk][i] - m_new);
+        else pv = __builtin_amdgcn_exp2f(fmaf(s[blk][i], c, -m_new));
+        psum += pv;
+        if constexpr (FP8) pv *= vs_lds[32 * blk + 16 * (i >> 3) + 8 * h + (i & 7)];
+        pf[2 * blk + (i >> 3)][i & 7] = static_cast<__bf16>(pv);
+      }
+    }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
+
+    // O^T += V^T P^T over four 16-key slices
+#pragma unroll
+    for (int b = 0; b < T::DB; ++b) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
+            v_lds + (32 * b + col) * T::VROW + 16 * u + 8 * h);
+        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], o[b], 0, 0, 0);
+      }
+    }
+  }
+
+  if (!wave_active) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (it.part < 0) {
+    if (!row_ok) return;
+    const float inv = 1.f / l_tot;
+    uint16_t* orow = static_cast<uint16_t*>(p.out) + (size_t(sq.cu + t) * hq + size_t(kvh) * G + g) * D;
+#pragma unroll
+    for (int b = 0; b < T::DB; ++b) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = 32 * b + 8 * q4 + 4 * h;
+        bf16x4 v4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = static_cast<__bf16>(o[b][4 * q4 + e] * inv);
+        *reinterpret_cast<u32x2*>(orow + d) = __builtin_bit_cast(u32x2, v4);
+      }
+    }
+    if (p.lse != nullptr && h == 0)
+      p.lse[size_t(sq.cu + t) * hq + size_t(kvh) * G + g] = (m_run + __log2f(l_tot)) * kLn2;
+  } else {
+    float* po = p.part_o + (size_t(it.part) * BLOCK_M + r_local) * D;
+#pragma unroll
+    for (int b = 0; b < T::DB; ++b) {
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = 32 * b + 8 * q4 + 4 * h;
+        float4 v = make_float4(o[b][4 * q4], o[b][4 * q4 + 1], o[b][4 * q4 + 2], o[b][4 * q4 + 3]);
+        *reinterpret_cast<float4*>(po + d) = v;
+      }
+    }
+    if (h == 0) {
+      float* ml = p.part_ml + (size_t(it.part) * BLOCK_M + r_local) * 2;
+      ml[0] = m_run;
+      ml[1] = l_tot;
+    }
+  }
+}
+
+// Merges the split-K partials of one query tile: weights 2^(m_c - max m),
+// O = sum w_c O_c / sum w_c l_c.  Fixed order, no atomics.
+template <int D>
+__global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
+  constexpr int ROWS_PER_WG = 8;
+  constexpr int PER = D / 32;  // dims per thread
+  const int grp = blockIdx.x / (BLOCK_M / ROWS_PER_WG);
+  const int lr = (blockIdx.x % (BLOCK_M / ROWS_PER_WG)) * ROWS_PER_WG + threadIdx.x / 32;
+  const int d0 = (threadIdx.x % 32) * PER;
+  const CombineGroup cg = p.groups[grp];
+  if (lr >= cg.rows) return;
+  const SeqInfo sq = p.seqs[cg.seq];
+  const int G = p.gqa_group, hq = p.num_kv_heads * G;
+  const int r = cg.q_row0 + lr;
+  const int t = r / G, g = r - t * G;
+
+  float mstar = -INFINITY;
+  for (int c = 0; c < cg.n_parts; ++c)
+    mstar = fmaxf(mstar, p.part_ml[(size_t(cg.part0 + c) * BLOCK_M + lr) * 2]);
+  float acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  float L = 0.f;
+  for (int c = 0; c < cg.n_parts; ++c) {
+    const size_t pr = size_t(cg.part0 + c) * BLOCK_M + lr;
+    const float w = exp2f(p.part_ml[pr * 2] - mstar);
+    L += w * p.part_ml[pr * 2 + 1];
+    const float* po = p.part_o + pr * D + d0;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] += w * po[e];
+  }
+  const float inv = 1.f / L;
+  uint16_t* orow = static_cast<uint16_t*>(p.out) + (size_t(sq.cu + t) * hq + size_t(cg.kvh) * G + g) * D + d0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const __bf16 v = static_cast<__bf16>(acc[e] * inv);
+    orow[e] = __builtin_bit_cast(uint16_t, v);
+  }
+  if (p.lse != nullptr && threadIdx.x % 32 == 0)
+    p.lse[size_t(sq.cu + t) * hq + size_t(cg.kvh) * G + g] = (mstar + log2f(L)) * kLn2;
+}
+
+template <int D, int P, bool FP8>
+hipError_t launch_extend_t(const ExtendParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL((extend_kernel<D, P, FP8>), dim3(p.n_items), dim3(THREADS), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
+                         hipStream_t stream) {
+  if (p.n_items <= 0) return hipSuccess;
+#define CW_CASE(D_, P_)                                                       \
+  if (head_dim == D_ && page_size == P_)                                      \
+    return fp8 ? launch_extend_t<D_, P_, true>(p, stream)                     \
+               : launch_extend_t<D_, P_, false>(p, stream);
+  CW_CASE(64, 16)
+  CW_CASE(64, 64)
+  CW_CASE(128, 16)
+  CW_CASE(128, 64)
+#undef CW_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_combine(const ExtendParams& p, int head_dim, hipStream_t stream) {
+  if (p.n_groups <= 0) return hipSuccess;
+  const dim3 grid(p.n_groups * (BLOCK_M / 8));
+  if (head_dim == 64) hipLaunchKernelGGL(combine_kernel<64>, grid, dim3(256), 0, stream, p);
+  else if (head_dim == 128) hipLaunchKernelGGL(combine_kernel<128>, grid, dim3(256), 0, stream, p);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace cw

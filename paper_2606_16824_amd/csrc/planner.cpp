@@ -1,0 +1,198 @@
+// Extend work planner (host).
+//
+// Work unit: one query tile (BLOCK_M packed rows of one sequence and kv head)
+// over a contiguous range of keys.  A tile whose rows end at token t_last needs
+// keys [0, Lp + t_last + 1) (bottom-right causal).  When there are too few
+// tiles to fill the GPU, each tile's key range is split into chunks of about
+// equal length ("split-K"); the chunks write unnormalised partials that a
+// second kernel merges with a log-sum-exp weighting.
+//
+// Launch order is XCD-aware: the dispatcher hands workgroup i to XCD i % X, and
+// each XCD has its own L2.  All tiles of one (sequence, kv head) read the same
+// keys, so they are kept on one XCD (split into several bundles only when there
+// are fewer bundles than XCDs), bundles are spread over XCDs
+// longest-processing-time first, and the per-XCD queues are interleaved.
+// Queues that run out early are padded with idle items so that later items
+// still land on their XCD.
+#include "planner.h"
+
+#include <algorithm>
+#include <climits>
+#include <numeric>
+
+namespace cw {
+namespace {
+
+constexpr int32_t MIN_CHUNK_TILES = 4;  // a chunk of fewer keys wastes the Q load
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Tile {
+  int32_t seq, kvh, q_row0, rows, kv_len, n_kt;
+};
+
+struct Bundle {
+  std::vector<WorkItem> items;
+  int64_t cost = 0;  // key tiles
+};
+
+}  // namespace
+
+ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
+                             int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                             int32_t head_dim, int32_t num_cus, int32_t num_xcds,
+                             const Tuning& tuning) {
+  ExtendPlan plan;
+  plan.seqs.resize(num_seqs);
+  int64_t cu = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    plan.seqs[b] = SeqInfo{prefix_lens[b], suffix_lens[b], static_cast<int32_t>(cu), 0};
+    cu += suffix_lens[b];
+  }
+
+  // 1. query tiles, per sequence and kv head
+  std::vector<Tile> tiles;
+  int64_t total_kt = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    const int64_t rows = int64_t(suffix_lens[b]) * gqa_group;
+    for (int64_t r0 = 0; r0 < rows; r0 += BLOCK_M) {
+      const int32_t nr = static_cast<int32_t>(std::min<int64_t>(BLOCK_M, rows - r0));
+      const int64_t t_last = (r0 + nr - 1) / gqa_group;
+      const int32_t kv_len = static_cast<int32_t>(prefix_lens[b] + t_last + 1);
+      const int32_t n_kt = (kv_len + BLOCK_N - 1) / BLOCK_N;
+      for (int32_t h = 0; h < num_kv_heads; ++h) {
+        tiles.push_back(Tile{b, h, static_cast<int32_t>(r0), nr, kv_len, n_kt});
+        total_kt += n_kt;
+      }
+    }
+  }
+
+  // 2. split-K: number of chunks per tile.  Automatic: when there are fewer
+  // tiles than `target` workgroups (two resident per CU), each tile gets about
+  // n_kt / (total_kt / target) chunks, so chunks are of about equal length and
+  // their count is close to the target.
+  const int64_t target = tuning.target_wgs > 0 ? tuning.target_wgs : 2LL * num_cus;
+  double chunk_len = 0.0;  // 0: no split
+  if (tuning.kv_chunk_tiles > 0) {
+    chunk_len = tuning.kv_chunk_tiles;
+  } else if (static_cast<int64_t>(tiles.size()) < target && !tiles.empty()) {
+    chunk_len = std::max<double>(MIN_CHUNK_TILES, double(total_kt) / double(target));
+  }
+  auto n_chunks = [&](int32_t n_kt) -> int64_t {
+    if (chunk_len <= 0.0) return 1;
+    if (tuning.kv_chunk_tiles > 0) return std::max<int64_t>(1, (n_kt + tuning.kv_chunk_tiles - 1) / tuning.kv_chunk_tiles);
+    const int64_t n = static_cast<int64_t>(double(n_kt) / chunk_len + 0.5);
+    return std::max<int64_t>(1, std::min<int64_t>(n, n_kt / MIN_CHUNK_TILES));
+  };
+
+  // 3. work items grouped into bundles by (sequence, kv head)
+  std::vector<Bundle> bundles;
+  {
+    int32_t cur_seq = -1, cur_kvh = -1;
+    std::vector<std::vector<WorkItem>> chunk_major;  // [chunk][tile] inside a bundle
+    auto flush = [&]() {
+      if (chunk_major.empty()) return;
+      Bundle bd;
+      for (auto& v : chunk_major)
+        for (auto& it : v) {
+          bd.items.push_back(it);
+          bd.cost += (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
+        }
+      bundles.push_back(std::move(bd));
+      chunk_major.clear();
+    };
+    // tiles are ordered (seq, q tile, kvh); regroup them per (seq, kvh)
+    std::vector<size_t> order(tiles.size());
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t c) {
+      if (tiles[a].seq != tiles[c].seq) return tiles[a].seq < tiles[c].seq;
+      return tiles[a].kvh < tiles[c].kvh;
+    });
+    for (size_t oi : order) {
+      const Tile& t = tiles[oi];
+      if (t.seq != cur_seq || t.kvh != cur_kvh) {
+        flush();
+        cur_seq = t.seq;
+        cur_kvh = t.kvh;
+      }
+      const int64_t n_c = n_chunks(t.n_kt);
+      int32_t part0 = -1;
+      if (n_c > 1) {
+        part0 = static_cast<int32_t>(plan.n_parts);
+        plan.groups.push_back(CombineGroup{t.seq, t.kvh, t.q_row0, t.rows, part0,
+                                           static_cast<int32_t>(n_c), 0, 0});
+        plan.n_parts += n_c;
+      }
+      for (int64_t c = 0; c < n_c; ++c) {
+        const int64_t kt0 = c * t.n_kt / n_c, kt1 = (c + 1) * t.n_kt / n_c;
+        WorkItem it{t.seq, t.kvh, t.q_row0, static_cast<int32_t>(kt0 * BLOCK_N),
+                    static_cast<int32_t>(std::min<int64_t>(kt1 * BLOCK_N, t.kv_len)),
+                    n_c > 1 ? static_cast<int32_t>(part0 + c) : -1, t.rows, 0};
+        if (static_cast<int64_t>(chunk_major.size()) <= c) chunk_major.resize(c + 1);
+        chunk_major[c].push_back(it);
+      }
+    }
+    flush();
+  }
+
+  // 4. enough bundles to occupy every XCD: halve the largest while possible
+  const int32_t X = std::max(1, num_xcds);
+  while (static_cast<int32_t>(bundles.size()) < 2 * X) {
+    auto it = std::max_element(bundles.begin(), bundles.end(),
+                               [](const Bundle& a, const Bundle& c) { return a.items.size() < c.items.size(); });
+    if (it == bundles.end() || it->items.size() < 2) break;
+    Bundle hi;
+    const size_t half = it->items.size() / 2;
+    hi.items.assign(it->items.begin() + half, it->items.end());
+    it->items.resize(half);
+    it->cost = hi.cost = 0;
+    for (auto& w : it->items) it->cost += (w.kv_end - w.kv_begin + BLOCK_N - 1) / BLOCK_N;
+    for (auto& w : hi.items) hi.cost += (w.kv_end - w.kv_begin + BLOCK_N - 1) / BLOCK_N;
+    bundles.push_back(std::move(hi));
+  }
+
+  // 5. LPT assignment of bundles to XCD queues, then interleave
+  std::stable_sort(bundles.begin(), bundles.end(),
+                   [](const Bundle& a, const Bundle& c) { return a.cost > c.cost; });
+  std::vector<std::vector<WorkItem>> queues(X);
+  std::vector<int64_t> load(X, 0);
+  for (auto& bd : bundles) {
+    const int32_t x = static_cast<int32_t>(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += bd.cost;
+    queues[x].insert(queues[x].end(), bd.items.begin(), bd.items.end());
+  }
+  size_t max_len = 0;
+  for (auto& qv : queues) max_len = std::max(max_len, qv.size());
+  const WorkItem idle{-1, 0, 0, 0, 0, -1, 0, 0};
+  int32_t used_queues = 0;
+  for (auto& qv : queues) used_queues += qv.empty() ? 0 : 1;
+  for (size_t i = 0; i < max_len; ++i)
+    for (int32_t x = 0; x < X; ++x) {
+      if (i < queues[x].size()) plan.items.push_back(queues[x][i]);
+      else if (used_queues > 1) plan.items.push_back(idle);
+    }
+  // trailing idle items launch nothing useful
+  while (!plan.items.empty() && plan.items.back().seq < 0) plan.items.pop_back();
+
+  // 6. workspace layout
+  plan.off_seqs = 0;
+  plan.off_items = align256(plan.off_seqs + plan.seqs.size() * sizeof(SeqInfo));
+  plan.off_groups = align256(plan.off_items + plan.items.size() * sizeof(WorkItem));
+  plan.meta_bytes = align256(plan.off_groups + plan.groups.size() * sizeof(CombineGroup));
+  plan.off_part_o = plan.meta_bytes;
+  plan.off_part_ml = align256(plan.off_part_o + size_t(plan.n_parts) * BLOCK_M * head_dim * sizeof(float));
+  plan.total_bytes = align256(plan.off_part_ml + size_t(plan.n_parts) * BLOCK_M * 2 * sizeof(float));
+  return plan;
+}
+
+void pack_plan_meta(const ExtendPlan& plan, uint8_t* dst) {
+  std::fill(dst, dst + plan.meta_bytes, uint8_t(0));
+  std::copy(reinterpret_cast<const uint8_t*>(plan.seqs.data()),
+            reinterpret_cast<const uint8_t*>(plan.seqs.data() + plan.seqs.size()), dst + plan.off_seqs);
+  std::copy(reinterpret_cast<const uint8_t*>(plan.items.data()),
+            reinterpret_cast<const uint8_t*>(plan.items.data() + plan.items.size()), dst + plan.off_items);
+  std::copy(reinterpret_cast<const uint8_t*>(plan.groups.data()),
+            reinterpret_cast<const uint8_t*>(plan.groups.data() + plan.groups.size()), dst + plan.off_groups);
+}
+
+}  // namespace cw

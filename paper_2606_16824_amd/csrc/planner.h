@@ -1,0 +1,39 @@
+// Host planner: turns host-side lengths into the extend work list.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "cw_internal.h"
+
+namespace cw {
+
+struct Tuning {
+  int32_t kv_chunk_tiles = 0;  // 0 = automatic
+  int32_t target_wgs = 0;      // 0 = automatic
+};
+
+struct ExtendPlan {
+  std::vector<SeqInfo> seqs;
+  std::vector<WorkItem> items;  // launch order
+  std::vector<CombineGroup> groups;
+  int64_t n_parts = 0;
+  // Workspace layout (byte offsets, 256-byte aligned).
+  size_t off_seqs = 0, off_items = 0, off_groups = 0, off_part_o = 0, off_part_ml = 0;
+  size_t meta_bytes = 0;  // seqs + items + groups: the part uploaded per call
+  size_t total_bytes = 0;
+};
+
+// Builds the plan.  `num_cus` and `num_xcds` describe the device.
+// Lengths must already be validated.
+ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
+                             int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                             int32_t head_dim, int32_t num_cus, int32_t num_xcds,
+                             const Tuning& tuning);
+
+// Serialises seqs, items and groups into `dst` (meta_bytes long) at their offsets.
+void pack_plan_meta(const ExtendPlan& plan, uint8_t* dst);
+
+}  // namespace cw

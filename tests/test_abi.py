@@ -1,0 +1,124 @@
+"""The C ABI on the CPU: symbols, argument validation, status strings, the planner.
+
+No call here reaches the GPU: invalid arguments are rejected before any HIP
+call, and the planner is host code.
+"""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_16824_amd as cwlib
+from paper_2606_16824_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "cw.h")
+
+
+def lib():
+    return cwlib.library()
+
+
+def test_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    names = set(re.findall(r"\b(cw_[a-z0-9_]+)\s*\(", text))
+    assert {"cw_kv_write_pages", "cw_extend_attention", "cw_decode_attention"} <= names
+    for n in sorted(names):
+        assert hasattr(lib(), n), n
+    assert names == set(L.SIGNATURES), "binding and header disagree"
+    assert lib().cw_version() >= 100
+
+
+def test_status_strings():
+    for s in range(7):
+        assert lib().cw_status_string(s).decode().startswith("CW_")
+
+
+FAKE = 0x100000  # a 16-byte-aligned address that is never dereferenced
+
+
+def _extend(**over):
+    lp = np.array(over.pop("lp", [10, 20]), dtype=np.int32)
+    ls = np.array(over.pop("ls", [5, 6]), dtype=np.int32)
+    a = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k_pool=FAKE, v_pool=FAKE, k_scale=None, v_scale=None,
+             block_table=FAKE, bt_stride=4, num_pages=100, num_kv_heads=2, gqa_group=4,
+             head_dim=128, page_size=16, scale=0.088, kv_dtype=0, out=FAKE, lse=None,
+             workspace=FAKE, workspace_bytes=1 << 40)
+    a.update(over)
+    return lib().cw_extend_attention(
+        a["q"], a["k_new"], a["v_new"], a["k_pool"], a["v_pool"], a["k_scale"], a["v_scale"],
+        a["block_table"], a["bt_stride"], a["num_pages"], lp.ctypes.data, ls.ctypes.data, len(lp),
+        a["num_kv_heads"], a["gqa_group"], a["head_dim"], a["page_size"], a["scale"],
+        a["kv_dtype"], a["out"], a["lse"], a["workspace"], a["workspace_bytes"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(q=None), L.CW_ERR_NULL),
+    (dict(out=None), L.CW_ERR_NULL),
+    (dict(block_table=None), L.CW_ERR_NULL),
+    (dict(kv_dtype=1), L.CW_ERR_NULL),  # fp8 without scales
+    (dict(head_dim=96), L.CW_ERR_UNSUPPORTED),
+    (dict(page_size=32), L.CW_ERR_UNSUPPORTED),
+    (dict(gqa_group=0), L.CW_ERR_UNSUPPORTED),
+    (dict(gqa_group=17), L.CW_ERR_UNSUPPORTED),
+    (dict(num_kv_heads=0), L.CW_ERR_UNSUPPORTED),
+    (dict(scale=0.0), L.CW_ERR_UNSUPPORTED),
+    (dict(scale=float("inf")), L.CW_ERR_UNSUPPORTED),
+    (dict(kv_dtype=7), L.CW_ERR_UNSUPPORTED),
+    (dict(lp=[-1, 3]), L.CW_ERR_BAD_LENS),
+    (dict(ls=[2, -3]), L.CW_ERR_BAD_LENS),
+    (dict(lp=[60, 0], ls=[5, 1]), L.CW_ERR_BAD_LENS),  # 65 > bt_stride * P = 64
+    (dict(bt_stride=0), L.CW_ERR_BAD_LENS),
+    (dict(q=FAKE + 8), L.CW_ERR_ALIGN),
+    (dict(k_pool=FAKE + 2), L.CW_ERR_ALIGN),
+    (dict(workspace=FAKE + 4), L.CW_ERR_ALIGN),
+    (dict(workspace_bytes=16), L.CW_ERR_WORKSPACE),
+    (dict(workspace=None), L.CW_ERR_WORKSPACE),
+])
+def test_extend_rejects_before_any_gpu_work(over, status):
+    assert _extend(**over) == status
+    assert lib().cw_last_error_message().decode()
+
+
+def test_all_empty_suffixes_is_a_no_op():
+    assert _extend(ls=[0, 0], q=None, out=None) == L.CW_OK
+
+
+def test_lp_plus_ls_exactly_fills_table_is_valid_until_workspace():
+    assert _extend(lp=[48, 0], ls=[16, 1], workspace_bytes=1) == L.CW_ERR_WORKSPACE
+
+
+def test_write_pages_validation():
+    lp = np.array([3, 0], dtype=np.int32)
+    ls = np.array([2, 4], dtype=np.int32)
+    ws = lib().cw_write_pages_workspace_bytes(2)
+    assert ws >= 32 and ws % 256 == 0
+
+    def call(**o):
+        a = dict(k_new=FAKE, v_new=FAKE, k_pool=FAKE, v_pool=FAKE, k_scale=None, v_scale=None,
+                 bt=FAKE, stride=1, d=128, p=16, dt=0, ws=FAKE, wsb=ws)
+        a.update(o)
+        return lib().cw_kv_write_pages(a["k_new"], a["v_new"], a["k_pool"], a["v_pool"],
+                                       a["k_scale"], a["v_scale"], a["bt"], a["stride"], 10,
+                                       lp.ctypes.data, ls.ctypes.data, 2, 2, a["d"], a["p"],
+                                       a["dt"], a["ws"], a["wsb"], None)
+    assert call(k_pool=None) == L.CW_ERR_NULL
+    assert call(dt=1) == L.CW_ERR_NULL
+    assert call(d=80) == L.CW_ERR_UNSUPPORTED
+    assert call(v_new=FAKE + 1) == L.CW_ERR_ALIGN
+    assert call(wsb=8) == L.CW_ERR_WORKSPACE
+
+
+def test_workspace_query_rejects_bad_args():
+    lp = np.array([5], dtype=np.int32)
+    ls = np.array([-1], dtype=np.int32)
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, ls.ctypes.data, 1, 1, 1, 64, 16) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 72, 16) == 0
+
+
+def test_tuning_keys():
+    assert lib().cw_set_tuning(0, -1) == L.CW_ERR_UNSUPPORTED
+    assert lib().cw_set_tuning(9, 1) == L.CW_ERR_UNSUPPORTED
+    assert lib().cw_set_tuning(0, 0) == L.CW_OK
+    assert lib().cw_set_tuning(1, 0) == L.CW_OK

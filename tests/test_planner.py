@@ -1,0 +1,73 @@
+"""Properties of the host work planner (runs on the CPU)."""
+import numpy as np
+import pytest
+
+import paper_2606_16824_amd as cwlib
+
+BM, BN = 128, 64
+
+
+def check_plan(lp, ls, hkv, g, d=128, p=16):
+    items = cwlib.plan_items(lp, ls, hkv, g, d, p)
+    real = items[items[:, 0] >= 0]
+    # every (seq, kv head, query tile) key range [0, kv_len) is covered exactly once
+    cover = {}
+    for seq, kvh, r0, kb, ke, part, rows, _ in real:
+        assert 0 <= kb < ke and kb % BN == 0
+        cover.setdefault((seq, kvh, r0), []).append((kb, ke, part, rows))
+    for b in range(len(lp)):
+        nrows = ls[b] * g
+        for r0 in range(0, nrows, BM):
+            rows = min(BM, nrows - r0)
+            kv_len = lp[b] + (r0 + rows - 1) // g + 1
+            for h in range(hkv):
+                ch = sorted(cover.pop((b, h, r0)))
+                assert ch[0][0] == 0 and ch[-1][1] == kv_len
+                for (a0, a1, _, _), (b0, _, _, _) in zip(ch, ch[1:]):
+                    assert a1 == b0
+                assert all(c[3] == rows for c in ch)
+                parts = [c[2] for c in ch]
+                if len(ch) == 1:
+                    assert parts == [-1]
+                else:
+                    assert parts == list(range(parts[0], parts[0] + len(ch)))
+    assert not cover
+    allp = real[:, 5][real[:, 5] >= 0]
+    assert len(np.unique(allp)) == len(allp)
+    return items
+
+
+def test_turn_plan_fills_two_workgroups_per_cu():
+    items = check_plan([16384], [1024], 8, 4)
+    assert len(items) == 512
+    # XCD-aware: workgroup i runs on XCD i % 8; all work of a kv head on one XCD
+    for x in range(8):
+        assert len(set(items[x::8, 1].tolist())) == 1
+
+
+def test_long_plan_is_unsplit_and_head_aligned():
+    items = check_plan([131072], [8192], 8, 8, p=64)
+    assert len(items) == 4096 and np.all(items[:, 5] == -1)
+    for x in range(8):
+        assert len(set(items[x::8, 1].tolist())) == 1
+
+
+@pytest.mark.parametrize("lp,ls,hkv,g", [
+    ([256], [64], 1, 4),
+    ([0, 37, 200, 64], [70, 1, 129, 33], 2, 1),
+    ([40, 10, 0], [0, 20, 0], 1, 4),
+    ([5000, 30000, 12000], [1, 1, 1], 8, 4),
+    ([100] * 40, [300] * 40, 4, 2),
+])
+def test_plan_coverage(lp, ls, hkv, g):
+    check_plan(np.array(lp), np.array(ls), hkv, g)
+
+
+def test_forced_chunking():
+    cwlib.set_tuning(0, 3)
+    try:
+        items = check_plan(np.array([700]), np.array([150]), 2, 4)
+        real = items[items[:, 0] >= 0]
+        assert np.all(real[:, 4] - real[:, 3] <= 3 * BN)
+    finally:
+        cwlib.set_tuning(0, 0)
