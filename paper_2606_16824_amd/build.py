@@ -27,6 +27,7 @@ COMMON = [
     "-Wno-unused-function", "-Wno-unused-command-line-argument",
     # no packed-FP32 VALU instructions in generated device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
 

@@ -45,6 +45,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kNegBig = -1.0e30f;
 constexpr float kLn2 = 0.69314718055994531f;
@@ -72,50 +73,37 @@ __device__ __forceinline__ u32x4 fp8x8_to_bf16x8(u32x2 c) {
 }
 
 template <int D, int P, bool FP8>
-struct Tile {
+struct Geo {
   static constexpr int KROW = D + 8;        // K tile row stride (elements): 16 B pad
   static constexpr int VROW = BLOCK_N + 8;  // V^T tile row stride (elements)
-  static constexpr int K_CHUNKS = BLOCK_N * D / 8 / THREADS;  // 16-byte K chunks per thread
-  static constexpr int V_UNITS = 16 * (D / 8);                // (4 keys x 8 dims) V units
-  static constexpr int KT = D / 16;                            // k-steps of Q K^T
-  static constexpr int DB = D / 32;                            // 32-row blocks of O^T
+  static constexpr int CPR = D / 8;         // 16-byte chunks per K/V row
+  static constexpr int KCH = BLOCK_N * CPR / THREADS;  // K chunks per thread
+  static constexpr int RSTEP = THREADS / CPR;          // rows between a thread's K chunks
+  static constexpr int VUNITS = 16 * CPR;              // (4 keys x 8 dims) V units per tile
+  static constexpr int NPG = BLOCK_N / P;              // pages per tile
+  static constexpr int KT = D / 16;                    // k-steps of K Q^T
+  static constexpr int DB = D / 32;                    // 32-row blocks of O^T
 };
 
-// Global -> registers for one key/value tile (prefetched one tile ahead).
-template <int D, int P, bool FP8>
-struct TileRegs {
-  using T = Tile<D, P, FP8>;
-  u32x4 k[T::K_CHUNKS];  // bf16 K chunks (fp8 prefix rows already widened)
-  u32x4 v[4];            // 4 key rows x 8 dims of V (bf16)
-  float ks, vs;          // this thread's row scale (threads 0..63, fp8 only)
+template <int N>
+struct Pages {
+  int id[N];
+};
+template <int N>
+struct Scales {
+  float k[N], v[N];
 };
 
-template <int D, int P, bool FP8>
-__device__ __forceinline__ u32x4 load_row8(const void* pool, const void* fresh, const int32_t* bt,
-                                           int j, int lp, int ls, int cu, int hkv, int kvh, int d0) {
-  u32x4 r = {0u, 0u, 0u, 0u};
-  if (j < lp) {
-    const int pg = bt[j / P];
-    const size_t off = ((size_t(pg) * hkv + kvh) * P + (j % P)) * D + d0;
-    if constexpr (FP8) {
-      r = fp8x8_to_bf16x8(*reinterpret_cast<const u32x2*>(static_cast<const uint8_t*>(pool) + off));
-    } else {
-      r = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(pool) + off);
-    }
-  } else if (j < lp + ls) {
-    const size_t off = (size_t(cu + j - lp) * hkv + kvh) * D + d0;
-    r = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(fresh) + off);
-  }
-  return r;
-}
+// Tile modes (uniform across the workgroup): every key in the cached prefix,
+// every key in the new suffix, or anything else (prefix/suffix boundary or the
+// end of the sequence inside the tile).
+enum : int { MODE_PREFIX = 0, MODE_SUFFIX = 1, MODE_MIXED = 2 };
 
 template <int D, int P, bool FP8>
 __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
-  using T = Tile<D, P, FP8>;
+  using T = Geo<D, P, FP8>;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[BLOCK_N * T::KROW];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[D * T::VROW];
-  __shared__ __attribute__((aligned(16))) float ks_lds[BLOCK_N];
-  __shared__ __attribute__((aligned(16))) float vs_lds[BLOCK_N];
 
   const WorkItem it = p.items[blockIdx.x];
   if (it.seq < 0) return;  // idle padding item (uniform across the workgroup)
@@ -125,18 +113,21 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
   const int h = lane >> 5, col = lane & 31;
   const int G = p.gqa_group, hkv = p.num_kv_heads, hq = hkv * G;
   const int kvh = it.kvh;
+  const int lp = sq.lp, total_len = sq.lp + sq.ls;
   const int32_t* bt = p.block_table + size_t(it.seq) * p.bt_stride;
+  const uint16_t* k_new = static_cast<const uint16_t*>(p.k_new);
+  const uint16_t* v_new = static_cast<const uint16_t*>(p.v_new);
 
   // this lane's query row and its causal limit (number of visible keys)
   const int r_local = wave * 32 + col;
   const bool row_ok = r_local < it.rows;
   const int r = it.q_row0 + r_local;
   const int t = r / G, g = r - t * G;
-  const int lim = row_ok ? sq.lp + t + 1 : 0x7FFFFFFF;
+  const int lim = row_ok ? lp + t + 1 : 0x7FFFFFFF;
   const bool wave_active = wave * 32 < it.rows;
-  const int wave_min_lim = sq.lp + (it.q_row0 + wave * 32) / G + 1;
+  const int wave_min_lim = lp + (it.q_row0 + wave * 32) / G + 1;
   const int wave_last_row = it.q_row0 + min(wave * 32 + 31, it.rows - 1);
-  const int wave_max_lim = sq.lp + wave_last_row / G + 1;
+  const int wave_max_lim = lp + wave_last_row / G + 1;
 
   // Q^T as the B operand: k-step kk holds dims 16 kk + 8 h + [0, 8) of this row
   bf16x8 qf[T::KT];
@@ -157,51 +148,111 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
   float m_run = kNegBig, l_run = 0.f;
   const float c = p.scale_log2;
 
-  // staging assignment: K chunk i -> row (tid + 256 i) / (D/8), 16-byte column
-  // (tid + 256 i) % (D/8); V unit tid -> keys 4 (tid % 16) .. +3, dims 8 (tid / 16) .. +7
-  const int vkg = tid & 15, vdg = tid >> 4;
-  const bool v_unit = tid < T::V_UNITS;
+  // staging geometry: K chunk i = row kr0 + RSTEP i, dims 8 kc .. +7;
+  // V unit = keys 4 vkg .. +3, dims 8 vdg .. +7 (threads below VUNITS)
+  const int kr0 = tid / T::CPR, kc = tid % T::CPR;
+  const int vkg = tid / T::CPR, vdg = tid % T::CPR;
+  const bool v_unit = tid < T::VUNITS;
 
-  TileRegs<D, P, FP8> regs;
-  auto load_tile = [&](int j0) {
+  auto mode_of = [&](int j0) {
+    if (j0 + BLOCK_N <= lp) return int(MODE_PREFIX);
+    if (j0 >= lp && j0 + BLOCK_N <= total_len) return int(MODE_SUFFIX);
+    return int(MODE_MIXED);
+  };
+  // physical pages of the prefix part of the tile at j0 (same address in every lane)
+  auto load_pages = [&](int j0) {
+    Pages<T::NPG> pg;
 #pragma unroll
-    for (int i = 0; i < T::K_CHUNKS; ++i) {
-      const int cidx = tid + THREADS * i;
-      const int row = cidx / (D / 8), c8 = cidx % (D / 8);
-      regs.k[i] = load_row8<D, P, FP8>(p.k_pool, p.k_new, bt, j0 + row, sq.lp, sq.ls, sq.cu, hkv,
-                                       kvh, c8 * 8);
+    for (int q = 0; q < T::NPG; ++q) pg.id[q] = (j0 + q * P < lp) ? bt[j0 / P + q] : 0;
+    return pg;
+  };
+  auto load_scales = [&](int j0, Pages<T::NPG> pg) {
+    Scales<T::NPG> sc;
+#pragma unroll
+    for (int q = 0; q < T::NPG; ++q) {
+      sc.k[q] = 1.f;
+      sc.v[q] = 1.f;
+      if (j0 + q * P < lp) {
+        const size_t si = size_t(pg.id[q]) * hkv + kvh;
+        sc.k[q] = p.k_scale[si];
+        sc.v[q] = p.v_scale[si];
+      }
     }
+    return sc;
+  };
+  // element offset of tile row `row` (j0 page aligned) in the pool
+  auto pool_off = [&](Pages<T::NPG> pg, int row) -> size_t {
+    int pgid = pg.id[0];
+#pragma unroll
+    for (int q = 1; q < T::NPG; ++q) pgid = (row / P == q) ? pg.id[q] : pgid;
+    return ((size_t(pgid) * hkv + kvh) * P + (row % P)) * D;
+  };
+  // element offset of key j >= lp in k_new / v_new
+  auto fresh_off = [&](int j) -> size_t { return (size_t(sq.cu + j - lp) * hkv + kvh) * D; };
+  auto load_pool = [&](const void* pool, size_t off) -> u32x4 {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if constexpr (FP8) {
+      const u32x2 w = *reinterpret_cast<const u32x2*>(static_cast<const uint8_t*>(pool) + off);
+      v.x = w.x;
+      v.y = w.y;
+    } else {
+      v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(pool) + off);
+    }
+    return v;
+  };
+  // One 8-element piece of tile row `row`: pool (prefix), k_new/v_new (suffix)
+  // or zero past the sequence.  Branches depend only on the tile mode (uniform);
+  // a mixed tile loads both candidates from valid addresses and selects.
+  auto load_piece = [&](int mode, int j0, int row, int d0, Pages<T::NPG> pg, const void* pool,
+                        const uint16_t* fresh) -> u32x4 {
+    const int j = j0 + row;
+    if (mode == MODE_PREFIX) return load_pool(pool, pool_off(pg, row) + d0);
+    if (mode == MODE_SUFFIX) return *reinterpret_cast<const u32x4*>(fresh + fresh_off(j) + d0);
+    const bool pre = j < lp, fr = !pre && j < total_len;
+    u32x4 a = {0u, 0u, 0u, 0u};
+    if (j0 < lp) a = load_pool(pool, pool_off(pg, pre ? row : 0) + d0);
+    const u32x4 b = *reinterpret_cast<const u32x4*>(fresh + fresh_off(fr ? j : lp) + d0);
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    return pre ? a : (fr ? b : z);
+  };
+
+  // raw tile registers: bf16 rows, or fp8 prefix rows in .xy (widened when stored)
+  u32x4 kraw[T::KCH], vraw[4];
+  auto load_data = [&](int j0, Pages<T::NPG> pg) {
+    const int mode = mode_of(j0);
+#pragma unroll
+    for (int i = 0; i < T::KCH; ++i)
+      kraw[i] = load_piece(mode, j0, kr0 + T::RSTEP * i, kc * 8, pg, p.k_pool, k_new);
     if (v_unit) {
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        regs.v[k] = load_row8<D, P, FP8>(p.v_pool, p.v_new, bt, j0 + 4 * vkg + k, sq.lp, sq.ls,
-                                         sq.cu, hkv, kvh, vdg * 8);
-    }
-    if constexpr (FP8) {
-      if (tid < BLOCK_N) {
-        const int j = j0 + tid;
-        regs.ks = 1.f;
-        regs.vs = 1.f;
-        if (j < sq.lp) {
-          const size_t si = size_t(bt[j / P]) * hkv + kvh;
-          regs.ks = p.k_scale[si];
-          regs.vs = p.v_scale[si];
-        }
-      }
+        vraw[k] = load_piece(mode, j0, 4 * vkg + k, vdg * 8, pg, p.v_pool, v_new);
     }
   };
-  auto store_tile = [&]() {
+  auto widen = [&](int mode, int j, u32x4 v) -> u32x4 {
+    if constexpr (FP8) {
+      const u32x4 w = fp8x8_to_bf16x8(u32x2{v.x, v.y});
+      if (mode == MODE_PREFIX) return w;
+      if (mode == MODE_MIXED) return j < lp ? w : v;
+    }
+    return v;
+  };
+  auto store_tile = [&](int j0) {
+    const int mode = mode_of(j0);
 #pragma unroll
-    for (int i = 0; i < T::K_CHUNKS; ++i) {
-      const int cidx = tid + THREADS * i;
-      const int row = cidx / (D / 8), c8 = cidx % (D / 8);
-      *reinterpret_cast<u32x4*>(k_lds + swap_bits_2_3(row) * T::KROW + c8 * 8) = regs.k[i];
+    for (int i = 0; i < T::KCH; ++i) {
+      const int row = kr0 + T::RSTEP * i;
+      *reinterpret_cast<u32x4*>(k_lds + swap_bits_2_3(row) * T::KROW + kc * 8) =
+          widen(mode, j0 + row, kraw[i]);
     }
     if (v_unit) {
+      u32x4 x[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) x[k] = widen(mode, j0 + 4 * vkg + k, vraw[k]);
       // transpose 4 keys x 8 dims: dword w of row k holds dims 2w (low) and 2w+1 (high)
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const uint32_t a0 = regs.v[0][w], a1 = regs.v[1][w], a2 = regs.v[2][w], a3 = regs.v[3][w];
+        const uint32_t a0 = x[0][w], a1 = x[1][w], a2 = x[2][w], a3 = x[3][w];
         u32x2 lo, hi;
         lo.x = (a0 & 0xFFFFu) | (a1 << 16);
         lo.y = (a2 & 0xFFFFu) | (a3 << 16);
@@ -211,20 +262,33 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
         *reinterpret_cast<u32x2*>(v_lds + (vdg * 8 + 2 * w + 1) * T::VROW + 4 * vkg) = hi;
       }
     }
-    if constexpr (FP8) {
-      if (tid < BLOCK_N) {
-        ks_lds[tid] = regs.ks;
-        vs_lds[tid] = regs.vs;
-      }
-    }
   };
 
-  if (it.kv_begin < it.kv_end) load_tile(it.kv_begin);
+  // three-stage pipeline: page ids two tiles ahead, scales and data one ahead
+  Pages<T::NPG> pg_next{};
+  Scales<T::NPG> sc_cur, sc_next;
+#pragma unroll
+  for (int q = 0; q < T::NPG; ++q) sc_cur.k[q] = sc_cur.v[q] = sc_next.k[q] = sc_next.v[q] = 1.f;
+  if (it.kv_begin < it.kv_end) {
+    const Pages<T::NPG> pg0 = load_pages(it.kv_begin);
+    load_data(it.kv_begin, pg0);
+    if constexpr (FP8) sc_next = load_scales(it.kv_begin, pg0);
+    if (it.kv_begin + BLOCK_N < it.kv_end) pg_next = load_pages(it.kv_begin + BLOCK_N);
+  }
+
   for (int j0 = it.kv_begin; j0 < it.kv_end; j0 += BLOCK_N) {
+    const int mode = mode_of(j0);
     __syncthreads();  // every wave is done reading the previous tile
-    store_tile();
+    store_tile(j0);
+    sc_cur = sc_next;
     __syncthreads();
-    if (j0 + BLOCK_N < it.kv_end) load_tile(j0 + BLOCK_N);  // in flight during the math
+    const int jn = j0 + BLOCK_N;
+    if (jn < it.kv_end) {  // next tile's data and scales, the one after's page ids
+      const Pages<T::NPG> pg1 = pg_next;
+      load_data(jn, pg1);
+      if constexpr (FP8) sc_next = load_scales(jn, pg1);
+      if (jn + BLOCK_N < it.kv_end) pg_next = load_pages(jn + BLOCK_N);
+    }
 
     if (!wave_active || j0 >= wave_max_lim) continue;  // nothing visible for this wave
 
@@ -241,44 +305,85 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
       }
     }
 
-    // scores in log2 units, masked
-    const bool need_mask = j0 + BLOCK_N > wave_min_lim;
+    // element i of block blk holds key j0 + 32 blk + 16 (i / 8) + 8 h + i % 8;
+    // the eight keys of group gi = 2 blk + i / 8 (for either half) lie in one page
+    if (j0 + BLOCK_N > wave_min_lim) {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (j0 + 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7) >= lim) s[blk][i] = -INFINITY;
+    }
+    // per-group factor from raw score to log2 units.  fp8: times the K scale of
+    // the key's page; a tile that crosses the prefix end scales per key instead.
+    float cg[4];
+#pragma unroll
+    for (int gi = 0; gi < 4; ++gi) cg[gi] = c;
+    if constexpr (FP8) {
+      if (mode == MODE_PREFIX) {
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) cg[gi] = c * sc_cur.k[(16 * gi + 8 * h) / P];
+      } else if (mode == MODE_MIXED) {
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int kl = 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7);
+            if (j0 + kl < lp) s[blk][i] *= sc_cur.k[kl / P];
+          }
+      }
+    }
     float mx = -INFINITY;
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
+    for (int gi = 0; gi < 4; ++gi) {
+      float gm = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int kl = 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7);  // key within the tile
-        float x;
-        if constexpr (FP8) x = s[blk][i] * (c * ks_lds[kl]);
-        else x = s[blk][i];
-        if (need_mask && j0 + kl >= lim) x = -INFINITY;
-        s[blk][i] = x;
-        mx = fmaxf(mx, x);
-      }
+      for (int e = 0; e < 8; ++e) gm = fmaxf(gm, s[gi >> 1][8 * (gi & 1) + e]);
+      mx = fmaxf(mx, gm * cg[gi]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, FP8 ? mx : mx * c);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    {
+      // lanes l and l + 32 hold the two halves of one row's keys
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    // lazy rescale: keep a stale running max until some row's max exceeds it
+    // by more than 8 (log2 units); the weights then stay below 2^8
+    if (__any(mx > m_run + 8.f)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
+    }
 
     bf16x8 pf[4];
-    float psum = 0.f;
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
+    for (int gi = 0; gi < 4; ++gi) {
+      float pv[8];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float pv;
-        if constexpr (FP8) pv = __builtin_amdgcn_exp2f(s[blk][i] - m_new);
-        else pv = __builtin_amdgcn_exp2f(fmaf(s[blk][i], c, -m_new));
-        psum += pv;
-        if constexpr (FP8) pv *= vs_lds[32 * blk + 16 * (i >> 3) + 8 * h + (i & 7)];
-        pf[2 * blk + (i >> 3)][i & 7] = static_cast<__bf16>(pv);
+      for (int e = 0; e < 8; ++e)
+        pv[e] = __builtin_amdgcn_exp2f(fmaf(s[gi >> 1][8 * (gi & 1) + e], cg[gi], -m_run));
+      if constexpr (FP8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int kl = 16 * gi + 8 * h + e;
+          const float vsc = (mode == MODE_PREFIX || (mode == MODE_MIXED && j0 + kl < lp))
+                                ? sc_cur.v[kl / P] : 1.f;
+          l_run += pv[e];
+          pf[gi][e] = static_cast<__bf16>(pv[e] * vsc);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[gi][e] = static_cast<__bf16>(pv[e]);
+        // row sum of the rounded weights, so numerator and denominator agree
+        const bf16x2 one = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2)
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, l_run, false);
       }
     }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
 
     // O^T += V^T P^T over four 16-key slices
 #pragma unroll

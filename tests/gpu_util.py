@@ -51,7 +51,12 @@ def as_f64(t: torch.Tensor) -> np.ndarray:
 
 def assert_close(got: np.ndarray, ref: np.ndarray, max_abs: float, mean_abs: float = None, what=""):
     assert got.shape == ref.shape, (got.shape, ref.shape)
-    assert np.all(np.isfinite(got)), f"{what}: non-finite GPU output"
+    bad = ~np.isfinite(got)
+    if bad.any():
+        idx = np.argwhere(bad)
+        print(f"[{what}] {int(bad.sum())} non-finite values; first indices {idx[:12].tolist()}; "
+              f"rows with any: {np.unique(idx[:, 0]).tolist()[:40]}", flush=True)
+    assert not bad.any(), f"{what}: non-finite GPU output"
     err = np.abs(got - ref)
     mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
     print(f"[{what}] max_abs={mx:.3e} mean_abs={mean:.3e} n={err.size}", flush=True)

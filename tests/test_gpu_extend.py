@@ -81,7 +81,9 @@ def test_forced_split_matches_unsplit(chunk_tiles):
     ref, _ = oracle.extend_attention_blocked(paged_inputs(w))
     assert_close(as_f64(out), ref, BF16_MAX_ABS, BF16_MEAN_ABS, "split vs oracle")
     assert_close(as_f64(out), as_f64(base), 2 ** -7, None, "split vs unsplit")
-    assert_close(lse.cpu().double().numpy(), base_lse.cpu().double().numpy(), 1e-4, None, "lse")
+    # the row sums add the bf16-rounded weights (relative error <= 2^-9 each), so two
+    # different splits of the keys may differ by up to 2 * 2^-9 in lse
+    assert_close(lse.cpu().double().numpy(), base_lse.cpu().double().numpy(), 2 ** -8, None, "lse")
 
 
 def test_page_permutation_bitwise():
