@@ -275,7 +275,8 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   }
   hipError_t e = hipSuccess;
   if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  e = launch_extend(p, head_dim, page_size, kv_dtype == CW_KV_FP8_E4M3FN, stream);
+  e = kv_dtype == CW_KV_FP8_E4M3FN ? launch_extend(p, head_dim, page_size, true, stream)
+                                   : launch_extend_lds(p, head_dim, page_size, stream);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
   if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if (p.n_groups > 0) {

@@ -95,6 +95,7 @@ struct WriteParams {
 // Kernel launchers (each defined in the translation unit of its kernel).
 hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream);
+hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream);
 hipError_t launch_combine(const ExtendParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size, bool fp8,
                               hipStream_t stream);

@@ -148,10 +148,14 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
   float m_run = kNegBig, l_run = 0.f;
   const float c = p.scale_log2;
 
-  // staging geometry: K chunk i = row kr0 + RSTEP i, dims 8 kc .. +7;
-  // V unit = keys 4 vkg .. +3, dims 8 vdg .. +7 (threads below VUNITS)
+  // staging geometry: K chunk i = row kr0 + RSTEP i, dims 8 kc .. +7 (eight
+  // consecutive lanes fill one 128-byte stretch of a K row in LDS);
+  // V unit = keys 4 vkg .. +3, dims 8 vdg .. +7 (threads below VUNITS).  The 16
+  // lanes of a V store group have 16 different key groups: V^T rows 8 apart are
+  // 288 dwords apart (a multiple of the 32 banks), so distinct key columns are
+  // what keeps the 8-byte transposed stores conflict-free.
   const int kr0 = tid / T::CPR, kc = tid % T::CPR;
-  const int vkg = tid / T::CPR, vdg = tid % T::CPR;
+  const int vkg = tid & 15, vdg = tid >> 4;
   const bool v_unit = tid < T::VUNITS;
 
   auto mode_of = [&](int j0) {
@@ -292,17 +296,18 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
 
     if (!wave_active || j0 >= wave_max_lim) continue;  // nothing visible for this wave
 
-    // S^T = K Q^T for two 32-key blocks
-    f32x16 s[2];
+    // S^T = K Q^T for two 32-key blocks; the two accumulators alternate so that
+    // consecutive MFMAs are independent
+    f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-      s[blk] = f32x16{};
+    for (int kk = 0; kk < T::KT; ++kk) {
+      bf16x8 kf[2];
 #pragma unroll
-      for (int kk = 0; kk < T::KT; ++kk) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-            k_lds + (32 * blk + col) * T::KROW + 16 * kk + 8 * h);
-        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[blk], 0, 0, 0);
-      }
+      for (int blk = 0; blk < 2; ++blk)
+        kf[blk] = *reinterpret_cast<const bf16x8*>(k_lds + (32 * blk + col) * T::KROW + 16 * kk + 8 * h);
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[blk], qf[kk], s[blk], 0, 0, 0);
     }
 
     // element i of block blk holds key j0 + 32 blk + 16 (i / 8) + 8 h + i % 8;
@@ -385,15 +390,16 @@ __global__ __launch_bounds__(THREADS) void extend_kernel(ExtendParams p) {
       }
     }
 
-    // O^T += V^T P^T over four 16-key slices
+    // O^T += V^T P^T over four 16-key slices (the DB accumulators alternate)
 #pragma unroll
-    for (int b = 0; b < T::DB; ++b) {
+    for (int u = 0; u < 4; ++u) {
+      bf16x8 vf[T::DB];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
-            v_lds + (32 * b + col) * T::VROW + 16 * u + 8 * h);
-        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], o[b], 0, 0, 0);
-      }
+      for (int b = 0; b < T::DB; ++b)
+        vf[b] = *reinterpret_cast<const bf16x8*>(v_lds + (32 * b + col) * T::VROW + 16 * u + 8 * h);
+#pragma unroll
+      for (int b = 0; b < T::DB; ++b)
+        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b], pf[u], o[b], 0, 0, 0);
     }
   }
 
