@@ -9,8 +9,7 @@
 //
 // LDS holds K and V rows in their natural [key][dim] order, 16-byte chunks
 // XOR-swizzled per row so that every fragment read is bank-conflict free:
-//   K row R, chunk c at position c ^ (swap_bits_2_3(R) & 7)
-//   V row R, chunk c at position c ^ (2 (R & 3))
+//   K row R, chunk c at position c ^ k_swz(R);  V row R, chunk c at c ^ v_swz(R)
 // The DMA writes lane l's 16 bytes at base + 16 l, so each lane simply fetches
 // the global chunk that belongs at its position.
 //
@@ -57,6 +56,24 @@ __device__ __forceinline__ int swap_bits_2_3(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
+// Chunk swizzles.  The LDS serves 256 bytes per clock (64 banks of 4 bytes), so a
+// fragment read is conflict free when the lanes served together hit distinct
+// 16-byte positions modulo 256 bytes.
+//  K (ds_read_b128, 16 lanes per clock): lane m reads row swap_bits_2_3(m);
+//    XOR-ing the chunk with swap_bits_2_3(row) & 15 (D=128, 256-byte rows) or
+//    (swap_bits_2_3(row) >> 1) & 7 (D=64, two rows per 256 bytes) spreads them.
+//  V (ds_read_b64_tr_b16, 32 lanes per clock): four consecutive key rows x
+//    four chunks per clock; XOR-ing with 4 (row & 3) (D=128) or 4 ((row >> 1) & 1)
+//    (D=64) spreads them.
+template <int D>
+__device__ __forceinline__ int k_swz(int row) {
+  return D == 128 ? (swap_bits_2_3(row) & 15) : ((swap_bits_2_3(row) >> 1) & 7);
+}
+template <int D>
+__device__ __forceinline__ int v_swz(int row) {
+  return D == 128 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
+}
+
 template <int D, int P>
 struct LGeo {
   static constexpr int RB = 2 * D;                    // bytes per K/V row
@@ -82,7 +99,8 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
   if (it.seq < 0) return;  // idle padding item (uniform across the workgroup)
   const SeqInfo sq = p.seqs[it.seq];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int h = lane >> 5, col = lane & 31;
   const int G = p.gqa_group, hkv = p.num_kv_heads, hq = hkv * G;
   const int kvh = it.kvh;
@@ -130,8 +148,8 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
 #pragma unroll
   for (int j = 0; j < T::NI; ++j) {
     const int R = (wave * T::NI + j) * T::RPI + dma_row;
-    const int kc = dma_pos ^ (swap_bits_2_3(R) & 7);
-    const int vc = dma_pos ^ (2 * (R & 3));
+    const int kc = dma_pos ^ k_swz<D>(R);
+    const int vc = dma_pos ^ v_swz<D>(R);
     k_lane_off[j] = (R % P) * T::RB + 16 * kc;
     v_lane_off[j] = (R % P) * T::RB + 16 * vc;
     kf_lane_off[j] = R * hkv * T::RB + 16 * kc;
@@ -149,37 +167,52 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
   auto load_page = [&](int j0) -> int {
     return (j0 + wq * P < lp) ? __builtin_amdgcn_readfirstlane(bt[j0 / P + wq]) : 0;
   };
-  // issue the K and V DMA of the tile at j0 into stage `st`
+  // issue the K and V DMA of the tile at j0 into stage `st`.  Whole-prefix and
+  // whole-suffix tiles use a wave-uniform base plus the per-lane offsets;
+  // a tile that crosses the prefix end or the sequence end picks per lane.
   auto issue_tile = [&](int j0, int st, int pg) __attribute__((always_inline)) {
     uint8_t* kdst = lds + (2 * st) * T::TILE;
     uint8_t* vdst = lds + (2 * st + 1) * T::TILE;
     const int mode = mode_of(j0);
+    if (mode != MODE_MIXED) {
+      if (mode == MODE_PREFIX) {
+        const size_t base = (size_t(pg) * hkv + kvh) * page_bytes;
+#pragma unroll
+        for (int j = 0; j < T::NI; ++j) {
+          const int r0 = (wave * T::NI + j) * T::RPI;
+          dma16(k_pool + base + k_lane_off[j], (lds_void*)(kdst + r0 * T::RB));
+          dma16(v_pool + base + v_lane_off[j], (lds_void*)(vdst + r0 * T::RB));
+        }
+      } else {
+        const size_t base = (size_t(sq.cu + j0 - lp) * hkv + kvh) * T::RB;
+#pragma unroll
+        for (int j = 0; j < T::NI; ++j) {
+          const int r0 = (wave * T::NI + j) * T::RPI;
+          dma16(k_new + base + kf_lane_off[j], (lds_void*)(kdst + r0 * T::RB));
+          dma16(v_new + base + vf_lane_off[j], (lds_void*)(vdst + r0 * T::RB));
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < T::NI; ++j) {
       const int r0 = (wave * T::NI + j) * T::RPI;
-      lds_void* kd = (lds_void*)(kdst + r0 * T::RB);
-      lds_void* vd = (lds_void*)(vdst + r0 * T::RB);
-      if (mode == MODE_PREFIX) {
+      const int key = j0 + r0 + dma_row;
+      const uint8_t* ksrc = nullptr;
+      const uint8_t* vsrc = nullptr;
+      if (key < lp) {
         const size_t base = (size_t(pg) * hkv + kvh) * page_bytes;
-        dma16(k_pool + base + k_lane_off[j], kd);
-        dma16(v_pool + base + v_lane_off[j], vd);
-      } else if (mode == MODE_SUFFIX) {
-        const size_t base = (size_t(sq.cu + j0 - lp) * hkv + kvh) * T::RB;
-        dma16(k_new + base + kf_lane_off[j], kd);
-        dma16(v_new + base + vf_lane_off[j], vd);
-      } else {
-        const int key = j0 + r0 + dma_row;
-        if (key < lp) {
-          const size_t base = (size_t(pg) * hkv + kvh) * page_bytes;
-          dma16(k_pool + base + k_lane_off[j], kd);
-          dma16(v_pool + base + v_lane_off[j], vd);
-        } else if (key < total_len) {
-          const size_t base = (size_t(sq.cu + key - lp) * hkv + kvh) * T::RB;
-          const uint32_t ko = kf_lane_off[j] - (r0 + dma_row) * hkv * T::RB;  // 16 kc
-          const uint32_t vo = vf_lane_off[j] - (r0 + dma_row) * hkv * T::RB;
-          dma16(k_new + base + ko, kd);
-          dma16(v_new + base + vo, vd);
-        }
+        ksrc = k_pool + base + k_lane_off[j];
+        vsrc = v_pool + base + v_lane_off[j];
+      } else if (key < total_len) {
+        // kf/vf offsets hold R * hkv * RB + 16 c; the row is in the base here
+        const size_t base = (size_t(sq.cu + key - lp) * hkv + kvh) * T::RB;
+        ksrc = k_new + base + (kf_lane_off[j] - (r0 + dma_row) * hkv * T::RB);
+        vsrc = v_new + base + (vf_lane_off[j] - (r0 + dma_row) * hkv * T::RB);
+      }
+      if (ksrc != nullptr) {
+        dma16(ksrc, (lds_void*)(kdst + r0 * T::RB));
+        dma16(vsrc, (lds_void*)(vdst + r0 * T::RB));
       }
     }
   };
@@ -221,7 +254,7 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
         const int R = swap_bits_2_3(col) + 32 * blk;
-        const int pos = (2 * kk + h) ^ (col & 7);
+        const int pos = (2 * kk + h) ^ k_swz<D>(R);
         kf[blk] = *reinterpret_cast<const bf16x8*>(ks + R * T::RB + 16 * pos);
       }
 #pragma unroll
@@ -288,7 +321,7 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
 #pragma unroll
           for (int e4 = 0; e4 < 2; ++e4) {
             const int R = 16 * u + 8 * h + 4 * e4 + kq;
-            const int off = R * T::RB + 16 * (chunk ^ (2 * (R & 3))) + 8 * (a & 1);
+            const int off = R * T::RB + 16 * (chunk ^ v_swz<D>(R)) + 8 * (a & 1);
             half[e4] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vs + off));
           }
           vf[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7));
