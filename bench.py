@@ -42,12 +42,52 @@ WORKLOAD_DESC = {
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="turn", choices=list(WORKLOAD_DESC))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (for "
+                         "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return ap.parse_args()
+
+
+def calibrate_copy(mib: int):
+    """A plain copy of known size, for reading HBM byte counters against."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "copy", "bytes_read": n, "bytes_written": n, "launches": 3}))
+
+
+KERNEL_SOURCES = {  # dominant kernel per pool dtype: (kernel, source, profile summary)
+    "bf16": ("extend_lds_kernel", "paper_2606_16824_amd/csrc/kernels/extend_lds.hip", "extend_lds_{wl}.md"),
+    "fp8": ("extend_kernel", "paper_2606_16824_amd/csrc/kernels/extend_attn.hip", "extend_fp8_{wl}.md"),
+}
+
+
+def measured_traffic(kv_dtype: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, or None when the
+    summary is missing or was taken on a different version of the kernel source."""
+    import hashlib
+    import re
+    kernel, src, prof = KERNEL_SOURCES[kv_dtype]
+    path = os.path.join(ROOT, "profiles", prof.format(wl=workload))
+    try:
+        text = open(path).read()
+        sha = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
+    except OSError:
+        return None
+    m = re.search(r"traffic_bytes_per_launch=(\d+) kernel_source_sha256=([0-9a-f]+)", text)
+    if not m or m.group(2) != sha:
+        return None
+    return int(m.group(1))
 
 
 def cpu_baseline(w, target_s: float):
@@ -88,6 +128,9 @@ def cpu_baseline(w, target_s: float):
 
 def main():
     args = parse()
+    if args.calibrate_copy_mib:
+        calibrate_copy(args.calibrate_copy_mib)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
@@ -169,7 +212,8 @@ def main():
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "extend_kernel", "kernel_ms": round(kern_ms, 5)},
+                     "traffic": measured_traffic(s.kv_dtype, args.workload),
+                     "kernel": KERNEL_SOURCES[s.kv_dtype][0], "kernel_ms": round(kern_ms, 5)},
     }
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
