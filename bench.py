@@ -36,6 +36,9 @@ WORKLOAD_DESC = {
     "batch16": "16 agent turns sharing an 8192-token prefix, prefix lognormal(20k) 4k-64k, suffix U[200,4000], 32q/8kv, D=128, P=16, bf16",
     "long": "long-session extend: prefix 131072, suffix 8192, 64q/8kv (GQA 8), D=128, P=64, bf16",
     "mixed": "mixed step: 48 decodes + 16 extends, 32q/8kv, D=128, P=16, fp8-e4m3fn pool",
+    "decode": "decode: the 48 decodes of the mixed step (prefix U[2k,32k]), 32q/8kv, D=128, P=16, fp8-e4m3fn pool",
+    "decode_bf16": "decode: the 48 decodes of the mixed step, 32q/8kv, D=128, P=16, bf16 pool",
+    "decode_long": "decode: 1 sequence, prefix 131072, 64q/8kv (GQA 8), D=128, P=64, bf16 pool",
 }
 
 
@@ -45,6 +48,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="turn", choices=list(WORKLOAD_DESC))
+    ap.add_argument("--decode-steps", type=int, default=50,
+                    help="steps of the decode measurement added to an extend run (0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -126,6 +131,70 @@ def cpu_baseline(w, target_s: float):
             "tok_s": n / dt}
 
 
+def run_workload(name: str, steps: int, warmup: int):
+    """Times `steps` hot-path steps (page write + attention) of a named workload."""
+    import torch
+    import cw_workloads as cw
+    import paper_2606_16824_amd as cwlib
+
+    dev = torch.device("cuda:0")
+    w = cw.make(name)
+    s = w.spec
+    decode = name.startswith("decode")
+    print(f"[bench] workload {name}: {s.num_seqs} seqs, {s.total_new_tokens} new tokens, "
+          f"{s.flops() / 1e12:.3f} TFLOP", file=sys.stderr, flush=True)
+    mv = lambda t: None if t is None else t.to(dev).contiguous()
+    q, kn, vn, kp, vp = mv(w.q), mv(w.k_new), mv(w.v_new), mv(w.k_pool), mv(w.v_pool)
+    ks, vs, bt = mv(w.k_scale), mv(w.v_scale), mv(w.block_table)
+    out = torch.empty_like(q)
+    lse = torch.empty(q.shape[0], q.shape[1], device=dev, dtype=torch.float32)
+    if decode:
+        nb = cwlib.decode_workspace_bytes(s.prefix_lens, s.num_kv_heads, s.gqa_group, s.head_dim,
+                                          s.page_size)
+    else:
+        nb = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
+                                          s.gqa_group, s.head_dim, s.page_size)
+    ws_att = torch.empty(nb, dtype=torch.uint8, device=dev)
+    ws_wr = torch.empty(cwlib.write_pages_workspace_bytes(s.num_seqs), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        cwlib.kv_write_pages(kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, k_scale=ks,
+                             v_scale=vs, workspace=ws_wr)
+        if decode:
+            cwlib.decode_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.gqa_group,
+                                   s.softmax_scale, k_scale=ks, v_scale=vs, out=out, lse=lse,
+                                   workspace=ws_att)
+        else:
+            cwlib.extend_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
+                                   s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs, out=out,
+                                   lse=lse, workspace=ws_att)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    # timed region: exactly `steps` steps; the library records kernel-only events
+    lib = cwlib.library()
+    k_starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    k_stops = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    for e in k_starts + k_stops:  # torch creates the HIP event on first record
+        e.record(stream)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(steps):
+        lib.cw_set_timing_events(k_starts[i].cuda_event, k_stops[i].cuda_event)
+        step()
+    t_stop.record(stream)
+    torch.cuda.synchronize()
+    lib.cw_set_timing_events(None, None)
+    ms = t_start.elapsed_time(t_stop) / steps
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)]))
+    kernel = KERNEL_SOURCES[s.kv_dtype][0]
+    return {"spec": s, "workload": w, "ms": ms, "kern_ms": kern_ms, "kernel": kernel}
+
+
 def main():
     args = parse()
     if args.calibrate_copy_mib:
@@ -141,63 +210,34 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
-    dev = torch.device("cuda:0")
-    w = cw.make(args.workload)
-    s = w.spec
-    print(f"[bench] workload {args.workload}: {s.num_seqs} seqs, {s.total_new_tokens} new tokens, "
-          f"{s.flops() / 1e12:.3f} TFLOP", file=sys.stderr, flush=True)
-    mv = lambda t: None if t is None else t.to(dev).contiguous()
-    q, kn, vn, kp, vp = mv(w.q), mv(w.k_new), mv(w.v_new), mv(w.k_pool), mv(w.v_pool)
-    ks, vs, bt = mv(w.k_scale), mv(w.v_scale), mv(w.block_table)
-    out = torch.empty_like(q)
-    lse = torch.empty(q.shape[0], q.shape[1], device=dev, dtype=torch.float32)
-    ws_ext = torch.empty(cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
-                                                      s.gqa_group, s.head_dim, s.page_size),
-                         dtype=torch.uint8, device=dev)
-    ws_wr = torch.empty(cwlib.write_pages_workspace_bytes(s.num_seqs), dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream()
-
-    def step():
-        cwlib.kv_write_pages(kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, k_scale=ks,
-                             v_scale=vs, workspace=ws_wr)
-        cwlib.extend_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, s.gqa_group,
-                               s.softmax_scale, k_scale=ks, v_scale=vs, out=out, lse=lse,
-                               workspace=ws_ext)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # timed region: exactly `steps` steps, kernel-only events recorded by the library
-    lib = cwlib.library()
-    k_starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    k_stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_stop = torch.cuda.Event(enable_timing=True)
-    for e in k_starts + k_stops:  # torch creates the HIP event on first record
-        e.record(stream)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(args.steps):
-        lib.cw_set_timing_events(k_starts[i].cuda_event, k_stops[i].cuda_event)
-        assert k_starts[i].cuda_event and k_stops[i].cuda_event
-        step()
-    t_stop.record(stream)
-    torch.cuda.synchronize()
-    lib.cw_set_timing_events(None, None)
-    total_ms = t_start.elapsed_time(t_stop)
-    ms = total_ms / args.steps
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)]))
-    flops = s.flops()
-    value = flops / (ms * 1e-3) / 1e12
-    achieved = flops / (kern_ms * 1e-3) / 1e12
-    print(f"[bench] step {ms:.4f} ms, extend kernel {kern_ms:.4f} ms, {achieved:.1f} TFLOP/s kernel",
+    res = run_workload(args.workload, args.steps, args.warmup)
+    s, w = res["spec"], res["workload"]
+    ms, kern_ms = res["ms"], res["kern_ms"]
+    decode = s.suffix_lens.max() == 1 and args.workload.startswith("decode")
+    if decode:
+        nbytes = cw.decode_bytes(s)
+        value = nbytes / (ms * 1e-3) / 1e9
+        achieved = nbytes / (kern_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "kernel": res["kernel"], "kernel_ms": round(kern_ms, 5)}
+        unit = "GB/s"
+    else:
+        flops = s.flops()
+        value = flops / (ms * 1e-3) / 1e12
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": measured_traffic(s.kv_dtype, args.workload),
+                "kernel": res["kernel"], "kernel_ms": round(kern_ms, 5)}
+        unit = "TFLOP/s"
+    print(f"[bench] step {ms:.4f} ms, main kernel {kern_ms:.4f} ms, {achieved:.1f} {unit} kernel",
           file=sys.stderr, flush=True)
 
     result = {
         "metric": "extend-attn TFLOP/s (% bf16 MFMA peak) + new tok/s; decode HBM GB/s % peak",
         "value": round(value, 2),
-        "unit": "TFLOP/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -208,13 +248,22 @@ def main():
         "dtype": "bf16" if s.kv_dtype == "bf16" else "bf16+fp8kv",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_DESC[args.workload], "new_tokens": s.total_new_tokens,
-                   "tflop_per_step": round(flops / 1e12, 5), "seed": s.seed},
+                   "tflop_per_step": round(s.flops() / 1e12, 5), "seed": s.seed},
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(s.kv_dtype, args.workload),
-                     "kernel": KERNEL_SOURCES[s.kv_dtype][0], "kernel_ms": round(kern_ms, 5)},
+        "roofline": roof,
     }
+    if not decode and args.decode_steps > 0:
+        # the decode side of the metric: the mixed step's 48 decodes, fp8 pool
+        d = run_workload("decode", args.decode_steps, 10)
+        nbytes = cw.decode_bytes(d["spec"])
+        result["decode"] = {
+            "workload": WORKLOAD_DESC["decode"], "ms_per_step": round(d["ms"], 5),
+            "GB_s": round(nbytes / (d["ms"] * 1e-3) / 1e9, 1),
+            "kernel_GB_s": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9, 1),
+            "frac_hbm_peak": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "algorithmic_bytes": nbytes, "kernel": d["kernel"]}
+        print(f"[bench] decode step {d['ms']:.4f} ms, kernel {d['kern_ms']:.4f} ms", file=sys.stderr,
+              flush=True)
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

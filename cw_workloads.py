@@ -47,6 +47,9 @@ FP8_NAN_CODE = 0x7F
 BT_UNUSED = np.iinfo(np.int32).max  # block-table entries past a sequence
 
 CONFIG_NAMES = ("tiny", "turn", "batch16", "long", "mixed")
+# decode-only workloads (every suffix length 1): the 48 decodes of the mixed step
+# with its fp8 pool, the same lengths with a bf16 pool, and one 131072-token decode
+DECODE_NAMES = ("decode", "decode_bf16", "decode_long")
 
 
 @dataclasses.dataclass
@@ -137,6 +140,8 @@ def _pool_size(pages_required: int) -> int:
 
 def spec_for(name: str, seed: Optional[int] = None) -> WorkloadSpec:
     """Draw the lengths of one of the named workloads."""
+    if name in DECODE_NAMES:
+        return _decode_spec(name, seed)
     idx = CONFIG_NAMES.index(name)
     seed = 1000 + idx if seed is None else seed
     rng = np.random.default_rng(seed)
@@ -166,6 +171,34 @@ def spec_for(name: str, seed: Optional[int] = None) -> WorkloadSpec:
         spec.num_pages = _pool_size(int(spec.pages_needed().sum()))
         return spec
     raise ValueError(name)
+
+
+def _decode_spec(name: str, seed: Optional[int]) -> WorkloadSpec:
+    if name == "decode_long":
+        seed = 1007 if seed is None else seed
+        return WorkloadSpec(name, np.asarray([131072], np.int32), np.asarray([1], np.int32), 8, 8,
+                            128, 64, 4096, seed=seed)
+    mixed = spec_for("mixed")
+    dec = decode_subset(mixed)
+    lp = mixed.prefix_lens[dec].astype(np.int32)
+    seed = (1005 if name == "decode" else 1006) if seed is None else seed
+    spec = WorkloadSpec(name, lp, np.ones_like(lp), 8, 4, 128, 16, 0,
+                        kv_dtype="fp8" if name == "decode" else "bf16", seed=seed)
+    spec.num_pages = _pool_size(int(spec.pages_needed().sum()))
+    return spec
+
+
+def decode_bytes(spec: WorkloadSpec) -> int:
+    """Algorithmic HBM bytes of one decode call: every cached K/V element once, the
+    fp8 scales and block-table entries of the prefix pages, q/out and the new K/V."""
+    lp = spec.prefix_lens.astype(np.int64)
+    pages = (lp + spec.page_size - 1) // spec.page_size
+    elem = 1 if spec.kv_dtype == "fp8" else 2
+    hkv, d = spec.num_kv_heads, spec.head_dim
+    kv = 2 * lp * hkv * d * elem
+    scales = 2 * pages * hkv * 4 if spec.kv_dtype == "fp8" else 0
+    per_seq = kv + scales + pages * 4 + 2 * spec.num_q_heads * d * 2 + 2 * hkv * d * 2
+    return int(per_seq.sum())
 
 
 def custom_spec(prefix_lens, suffix_lens, *, num_kv_heads=1, gqa_group=1, head_dim=64,

@@ -205,13 +205,25 @@ ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int
                            current_tuning());
 }
 
+// Decode plans are built with the larger of the two dtypes' tile lengths so
+// that the workspace size does not depend on the pool dtype.
+ExtendPlan make_decode_plan(const int32_t* lp, int32_t num_seqs, int32_t num_kv_heads,
+                            int32_t gqa_group, int32_t head_dim, int32_t page_size) {
+  int32_t cus = 256, xcds = 8;
+  device_shape(&cus, &xcds);
+  const int32_t kpt = std::max(decode_keys_per_tile(head_dim, true), decode_keys_per_tile(head_dim, false));
+  return build_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kpt, cus,
+                           current_tuning());
+}
+
 cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, const void* k_pool,
                         const void* v_pool, const float* k_scale, const float* v_scale,
                         const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
                         const int32_t* lp, const int32_t* ls, int32_t num_seqs,
                         int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
                         int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype, void* out,
-                        float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                        float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                        bool decode) {
   cw_status_t s = check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size);
   if (s != CW_OK) return s;
   s = check_dtype(kv_dtype, k_scale, v_scale);
@@ -234,7 +246,8 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   if (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)) return fail(CW_ERR_ALIGN, "lse not 4-byte aligned");
   if ((reinterpret_cast<uintptr_t>(block_table) & 3u)) return fail(CW_ERR_ALIGN, "block_table not 4-byte aligned");
 
-  ExtendPlan plan = make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim);
+  ExtendPlan plan = decode ? make_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size)
+                           : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim);
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
 
@@ -267,6 +280,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   p.scale_log2 = softmax_scale * 1.4426950408889634f;
   p.n_items = static_cast<int32_t>(plan.items.size());
   p.n_groups = static_cast<int32_t>(plan.groups.size());
+  p.part_rows = plan.part_rows;
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   {
     std::lock_guard<std::mutex> g(g_tuning_mu);
@@ -275,12 +289,16 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   }
   hipError_t e = hipSuccess;
   if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  e = kv_dtype == CW_KV_FP8_E4M3FN ? launch_extend(p, head_dim, page_size, true, stream)
-                                   : launch_extend_lds(p, head_dim, page_size, stream);
+  const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
+  else if (fp8) e = launch_extend(p, head_dim, page_size, true, stream);
+  else e = launch_extend_lds(p, head_dim, page_size, stream);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
   if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if (p.n_groups > 0) {
-    e = launch_combine(p, head_dim, stream);
+    int max_parts = 0;
+    for (const CombineGroup& g : plan.groups) max_parts = std::max(max_parts, g.n_parts);
+    e = launch_combine(p, head_dim, max_parts, stream);
     if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
   }
   return CW_OK;
@@ -372,7 +390,7 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
   return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
                      num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
                      head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
-                     workspace_bytes, stream);
+                     workspace_bytes, stream, false);
 }
 
 size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
@@ -380,8 +398,12 @@ size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
                                  int32_t page_size) {
   if (num_seqs < 0) return 0;
   std::vector<int32_t> ones(num_seqs, 1);
-  return cw_extend_workspace_bytes(prefix_lens_h, ones.data(), num_seqs, num_kv_heads, gqa_group,
-                                   head_dim, page_size);
+  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+  if (check_lens(prefix_lens_h, ones.data(), num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                 head_dim, false) != CW_OK)
+    return 0;
+  if (num_seqs == 0) return 256;
+  return make_decode_plan(prefix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, page_size).total_bytes;
 }
 
 cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_new,
@@ -398,7 +420,7 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
   return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
                      num_pages, prefix_lens_h, ones.data(), num_seqs, num_kv_heads, gqa_group,
                      head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
-                     workspace_bytes, stream);
+                     workspace_bytes, stream, true);
 }
 
 cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {

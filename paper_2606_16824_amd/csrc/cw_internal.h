@@ -74,7 +74,7 @@ struct ExtendParams {
   float scale_log2;  // softmax_scale * log2(e)
   int32_t n_items;
   int32_t n_groups;
-  int32_t pad;
+  int32_t part_rows;  // rows per split-K partial slot (BLOCK_M for extend, G for decode)
 };
 
 struct WriteParams {
@@ -96,7 +96,10 @@ struct WriteParams {
 hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream);
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream);
-hipError_t launch_combine(const ExtendParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream);
+hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
+                         hipStream_t stream);
+int decode_keys_per_tile(int head_dim, bool fp8);
 hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size, bool fp8,
                               hipStream_t stream);
 

@@ -353,7 +353,7 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
     if (p.lse != nullptr && h == 0)
       p.lse[size_t(sq.cu + t) * hq + size_t(kvh) * G + g] = (m_run + __log2f(l_tot)) * kLn2;
   } else {
-    float* po = p.part_o + (size_t(it.part) * BLOCK_M + r_local) * D;
+    float* po = p.part_o + (size_t(it.part) * p.part_rows + r_local) * D;
 #pragma unroll
     for (int b = 0; b < T::DB; ++b) {
 #pragma unroll
@@ -364,7 +364,7 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
       }
     }
     if (h == 0) {
-      float* ml = p.part_ml + (size_t(it.part) * BLOCK_M + r_local) * 2;
+      float* ml = p.part_ml + (size_t(it.part) * p.part_rows + r_local) * 2;
       ml[0] = m_run;
       ml[1] = l_tot;
     }

@@ -36,6 +36,8 @@ struct Bundle {
   int64_t cost = 0;  // key tiles
 };
 
+void layout_workspace(ExtendPlan& plan, int32_t head_dim);
+
 }  // namespace
 
 ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
@@ -175,13 +177,72 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
   while (!plan.items.empty() && plan.items.back().seq < 0) plan.items.pop_back();
 
   // 6. workspace layout
+  plan.part_rows = BLOCK_M;
+  layout_workspace(plan, head_dim);
+  return plan;
+}
+
+namespace {
+void layout_workspace(ExtendPlan& plan, int32_t head_dim) {
   plan.off_seqs = 0;
   plan.off_items = align256(plan.off_seqs + plan.seqs.size() * sizeof(SeqInfo));
   plan.off_groups = align256(plan.off_items + plan.items.size() * sizeof(WorkItem));
   plan.meta_bytes = align256(plan.off_groups + plan.groups.size() * sizeof(CombineGroup));
   plan.off_part_o = plan.meta_bytes;
-  plan.off_part_ml = align256(plan.off_part_o + size_t(plan.n_parts) * BLOCK_M * head_dim * sizeof(float));
-  plan.total_bytes = align256(plan.off_part_ml + size_t(plan.n_parts) * BLOCK_M * 2 * sizeof(float));
+  plan.off_part_ml = align256(plan.off_part_o + size_t(plan.n_parts) * plan.part_rows * head_dim * sizeof(float));
+  plan.total_bytes = align256(plan.off_part_ml + size_t(plan.n_parts) * plan.part_rows * 2 * sizeof(float));
+}
+}  // namespace
+
+// Decode planning.  The cached prefix of each (sequence, kv head) is cut into
+// chunks of whole decode tiles and whole pages (at most 64 pages, the kernel
+// keeps one page id per lane); the chunk count is chosen so that about four
+// waves per CU slot exist (a decode wave is bound by its share of HBM
+// bandwidth, so more waves in flight means more bytes in flight).  The new
+// token's own key rides with the last chunk.
+ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32_t num_kv_heads,
+                             int32_t gqa_group, int32_t head_dim, int32_t page_size,
+                             int32_t keys_per_tile, int32_t num_cus, const Tuning& tuning) {
+  ExtendPlan plan;
+  plan.part_rows = gqa_group;
+  plan.seqs.resize(num_seqs);
+  int64_t total_tiles = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    plan.seqs[b] = SeqInfo{prefix_lens[b], 1, b, 0};
+    total_tiles += (int64_t(prefix_lens[b]) + keys_per_tile) / keys_per_tile * num_kv_heads;
+  }
+  const int64_t unit = std::max<int64_t>(keys_per_tile, page_size);  // chunk granule
+  const int64_t max_chunk = int64_t(64) * page_size;                 // keys
+  int64_t chunk;
+  if (tuning.kv_chunk_tiles > 0) {
+    chunk = int64_t(tuning.kv_chunk_tiles) * keys_per_tile;
+  } else {
+    const int64_t target = tuning.target_wgs > 0 ? tuning.target_wgs : int64_t(num_cus) * 3 * 4;
+    const int64_t tiles = std::max<int64_t>(2, (total_tiles + target - 1) / target);
+    chunk = tiles * keys_per_tile;
+  }
+  chunk = std::min(max_chunk, std::max(unit, (chunk + unit - 1) / unit * unit));
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    const int64_t n = int64_t(prefix_lens[b]) + 1;  // keys including the new one
+    const int64_t n_c = (n + chunk - 1) / chunk;
+    for (int32_t h = 0; h < num_kv_heads; ++h) {
+      int32_t part0 = -1;
+      if (n_c > 1) {
+        part0 = static_cast<int32_t>(plan.n_parts);
+        plan.groups.push_back(CombineGroup{b, h, 0, gqa_group, part0, static_cast<int32_t>(n_c), 0, 0});
+        plan.n_parts += n_c;
+      }
+      for (int64_t c = 0; c < n_c; ++c)
+        plan.items.push_back(WorkItem{b, h, 0, static_cast<int32_t>(c * chunk),
+                                      static_cast<int32_t>(std::min(n, (c + 1) * chunk)),
+                                      n_c > 1 ? static_cast<int32_t>(part0 + c) : -1, gqa_group, 0});
+    }
+  }
+  // longest chunks first so that short tails fill in at the end
+  std::stable_sort(plan.items.begin(), plan.items.end(), [](const WorkItem& a, const WorkItem& c) {
+    return (a.kv_end - a.kv_begin) > (c.kv_end - c.kv_begin);
+  });
+  layout_workspace(plan, head_dim);
   return plan;
 }
 
