@@ -1,28 +1,43 @@
-// Prefix-cached paged extend attention, bf16 pools: direct-to-LDS staging.
+// Prefix-cached paged extend attention, bf16 pools: direct-to-LDS staging with
+// a software-pipelined tile loop.
 //
-// Same work decomposition and math as the register-staged kernel (one
-// workgroup = four wave64s = 128 packed query rows of one (sequence, kv head);
-// S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_32x32x16_bf16; base-2 online
-// softmax with lazy rescaling), but K and V tiles travel from HBM straight into
-// LDS with global_load_lds_dwordx4, two stages deep, so staging costs no VGPRs
-// and no VALU, and each 64-key tile needs a single barrier.
+// Work decomposition and math follow the register-staged kernel (one workgroup
+// = four wave64s = 128 packed query rows of one (sequence, kv head);
+// S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_32x32x16_bf16), with three
+// changes aimed at the CDNA4 issue model, where every MFMA holds the vector
+// issue port for half its duration and the exponentials of the softmax cost as
+// much port time as the matrix products:
+//
+//  * Pipelining.  While the MFMAs of tile j+1's scores run, the same wave
+//    computes tile j's weights (exp2, bf16 pack, row sums); while tile j's
+//    P V MFMAs run, it scales and masks tile j+1's scores.  K tiles and V tiles
+//    rotate through separate two-stage rings: in iteration j the wave reads
+//    K_{j+1} and V_j while K_{j+2} and V_{j+1} land, one barrier per tile.
+//
+//  * A max-free fast path.  The running max m is only raised when it has to
+//    be: the weights exp2(s c - m) of a tile are computed against the current
+//    m, and only if some half-row's weight sum exceeds 2^16 (or is not finite)
+//    is the tile's row max taken, m raised and the tile's weights recomputed
+//    (the final O / l and the log-sum-exp do not depend on which m was used).
+//    The first tile of an item sets m to its exact row max.
+//
+//  * Buffer-addressed DMA.  K and V tiles travel from HBM straight into LDS
+//    with buffer_load_dwordx4 ... lds: the page base sits in the scalar buffer
+//    descriptor and each lane's offset within the page is a constant register,
+//    so issuing a tile costs no vector instructions.
 //
 // LDS holds K and V rows in their natural [key][dim] order, 16-byte chunks
 // XOR-swizzled per row so that every fragment read is bank-conflict free:
 //   K row R, chunk c at position c ^ k_swz(R);  V row R, chunk c at c ^ v_swz(R)
-// The DMA writes lane l's 16 bytes at base + 16 l, so each lane simply fetches
-// the global chunk that belongs at its position.
+// The DMA writes lane l's 16 bytes at base + 16 l, so each lane fetches the
+// global chunk that belongs at its position.  Each wave fetches 16 consecutive
+// rows of a tile, which lie in one page (P = 16 or 64).
 //
 // V^T operand: ds_read_b64_tr_b16 hands lane i of each 16-lane group element
 // in[4k + i/4][i % 4] of the 4-element rows its group's lanes point at.  Lanes
 // (k, a) = (i / 4, i % 4) point at key 4k-offset rows and dims 4a .. 4a+3, so
 // lane L receives V[keys 4e .. 4e+3 of its 8-key slot][dim 32b + L % 32]: half of
 // the A operand of V^T P^T; two reads give all eight keys.
-//
-// Pages: each wave fetches 16 consecutive key rows of a tile, which lie in one
-// page (P = 16 or 64), so a wave needs one page id per tile (a uniform value,
-// loaded a tile ahead) and each lane adds an offset that is the same for every
-// tile.
 #include <hip/hip_runtime.h>
 
 #include "../cw_internal.h"
@@ -43,13 +58,23 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr float kNegBig = -1.0e30f;
 constexpr float kLn2 = 0.69314718055994531f;
+// A half-row weight sum above this (or not finite) makes the tile raise the
+// running max: weights then stay below 2^16 and fp32 accumulators far from
+// overflow.
+constexpr float kSumLimit = 65536.f;
 
-// 16 bytes per lane from global memory straight into LDS (lane l's bytes land
-// at dst + 16 l).  Kept in a non-template function: referenced directly from
-// the kernel template, the builtin keeps the host pass from emitting the
+// Raw buffer descriptor for `base` (no stride, no range limit in practice).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_at(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, -1, 0x00020000);
+}
+
+// 16 bytes per lane from base + voff + soff straight into LDS (lane l's bytes
+// land at dst + 16 l).  Kept in a non-template function: referenced directly
+// from the kernel template, the builtin keeps the host pass from emitting the
 // kernel's launch stub.
-__device__ __forceinline__ void dma16(const void* src, lds_void* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_void* dst, uint32_t voff,
+                                      uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
 }
 
 __device__ __forceinline__ int swap_bits_2_3(int r) {
@@ -81,19 +106,21 @@ struct LGeo {
   static constexpr int RPI = 64 / CPR;                // rows per wave DMA instruction
   static constexpr int NI = BLOCK_N / RPI / WAVES;    // DMA instructions per wave per matrix
   static constexpr int TILE = BLOCK_N * RB;           // bytes of one K (or V) tile
-  static constexpr int NPG = BLOCK_N / P;             // pages per tile
   static constexpr int KT = D / 16;                   // k-steps of K Q^T
   static constexpr int DB = D / 32;                   // 32-row blocks of O^T
+  static_assert(NI * RPI == 16, "each wave fetches 16 rows of a tile");
 };
 
-enum : int { MODE_PREFIX = 0, MODE_SUFFIX = 1, MODE_MIXED = 2 };
-
-
 template <int D, int P>
-__global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2)))
+void extend_lds_kernel(ExtendParams p) {
   using T = LGeo<D, P>;
-  // [stage][K | V][tile]
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * 2 * T::TILE];
+  // two-stage rings of K and V tiles, each stage its own array so the compiler
+  // can tell that reads of one stage never alias the DMA in flight into another
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[T::TILE];
 
   const WorkItem it = p.items[blockIdx.x];
   if (it.seq < 0) return;  // idle padding item (uniform across the workgroup)
@@ -123,8 +150,12 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
   const int wave_max_lim = lp + wave_last_row / G + 1;
 
   // stale LDS must be finite: rows past the sequence are never fetched
-  for (int i = tid; i < 2 * 2 * T::TILE / 16; i += THREADS)
-    reinterpret_cast<u32x4*>(lds)[i] = u32x4{0u, 0u, 0u, 0u};
+  for (int i = tid; i < T::TILE / 16; i += THREADS) {
+    reinterpret_cast<u32x4*>(lds_k0)[i] = u32x4{0u, 0u, 0u, 0u};
+    reinterpret_cast<u32x4*>(lds_k1)[i] = u32x4{0u, 0u, 0u, 0u};
+    reinterpret_cast<u32x4*>(lds_v0)[i] = u32x4{0u, 0u, 0u, 0u};
+    reinterpret_cast<u32x4*>(lds_v1)[i] = u32x4{0u, 0u, 0u, 0u};
+  }
 
   // Q^T as the B operand: k-step kk holds dims 16 kk + 8 h + [0, 8) of this row
   bf16x8 qf[T::KT];
@@ -139,130 +170,121 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
     }
   }
 
-  // DMA geometry: wave w covers tile rows [16 w, 16 w + 16), which lie in one page
-  // (its page index in the tile is wq); its instruction j covers rows r0_j ..
-  // r0_j + RPI - 1 and lane l fetches row r0_j + l / CPR into position l % CPR
+  // ---- DMA geometry.  Wave w fetches tile rows [16 w, 16 w + 16); its
+  // instruction j covers rows R0_j = 16 w + RPI j .. + RPI - 1 and lane l fetches
+  // row R0_j + l / CPR into position l % CPR.  Within a page block the lane's
+  // source offset is (R % P) RB + 16 chunk; a suffix row lives at R hkv RB +
+  // 16 chunk from the tile's first new row, which is the same offset plus
+  // sfx_lane (per lane) plus sfx_uniform(j) (per instruction).
   const int dma_row = lane / T::CPR, dma_pos = lane % T::CPR;
-  uint32_t k_lane_off[T::NI], v_lane_off[T::NI];  // within a page (pool) block
-  uint32_t kf_lane_off[T::NI], vf_lane_off[T::NI];  // relative to the tile's first new row
+  const int wrow0 = 16 * wave;
+  uint32_t k_off[T::NI], v_off[T::NI];
 #pragma unroll
   for (int j = 0; j < T::NI; ++j) {
-    const int R = (wave * T::NI + j) * T::RPI + dma_row;
-    const int kc = dma_pos ^ k_swz<D>(R);
-    const int vc = dma_pos ^ v_swz<D>(R);
-    k_lane_off[j] = (R % P) * T::RB + 16 * kc;
-    v_lane_off[j] = (R % P) * T::RB + 16 * vc;
-    kf_lane_off[j] = R * hkv * T::RB + 16 * kc;
-    vf_lane_off[j] = R * hkv * T::RB + 16 * vc;
+    const int R = wrow0 + T::RPI * j + dma_row;
+    k_off[j] = (R % P) * T::RB + 16 * (dma_pos ^ k_swz<D>(R));
+    v_off[j] = (R % P) * T::RB + 16 * (dma_pos ^ v_swz<D>(R));
   }
+  const uint32_t sfx_lane = uint32_t(dma_row * (hkv - 1) * T::RB);
+  auto sfx_uniform = [&](int j) -> uint32_t {
+    const int R0 = wrow0 + T::RPI * j;
+    return uint32_t((R0 * hkv - R0 % P) * T::RB);
+  };
   const size_t page_bytes = size_t(P) * T::RB;  // one (page, kv head) block
-  const int wq = (wave * T::NI * T::RPI) / P;
 
-  auto mode_of = [&](int j0) {
-    if (j0 + BLOCK_N <= lp) return int(MODE_PREFIX);
-    if (j0 >= lp && j0 + BLOCK_N <= total_len) return int(MODE_SUFFIX);
-    return int(MODE_MIXED);
-  };
-  // physical page of this wave's rows of the tile at j0 (0 if they hold no prefix key)
-  auto load_page = [&](int j0) -> int {
-    return (j0 + wq * P < lp) ? __builtin_amdgcn_readfirstlane(bt[j0 / P + wq]) : 0;
-  };
-  // issue the K and V DMA of the tile at j0 into stage `st`.  Whole-prefix and
-  // whole-suffix tiles use a wave-uniform base plus the per-lane offsets;
-  // a tile that crosses the prefix end or the sequence end picks per lane.
-  auto issue_tile = [&](int j0, int st, int pg) __attribute__((always_inline)) {
-    uint8_t* kdst = lds + (2 * st) * T::TILE;
-    uint8_t* vdst = lds + (2 * st + 1) * T::TILE;
-    const int mode = mode_of(j0);
-    if (mode != MODE_MIXED) {
-      if (mode == MODE_PREFIX) {
-        const size_t base = (size_t(pg) * hkv + kvh) * page_bytes;
+  // physical page of this wave's rows of the tile at j0 (0 if they hold no
+  // prefix key).  The load stays a vector register until the tile is issued an
+  // iteration later, so waiting for it never waits for the DMA issued meanwhile.
+  auto load_page = [&](int j0) -> int { return (j0 + wrow0 < lp) ? bt[(j0 + wrow0) / P] : 0; };
+
+  // DMA of one matrix (K or V) of the tile at j0 into dst.  Rows of the cached
+  // prefix come from the pool page `pg`, rows of the suffix from the new
+  // tokens; rows past the sequence are left as they are (their scores are
+  // masked).  Wave-uniform branches except where the wave's rows straddle the
+  // prefix end or the sequence end.
+  auto issue = [&](int j0, uint8_t* dst, int pg, const uint8_t* pool, const uint8_t* fresh,
+                   const uint32_t(&off)[T::NI]) __attribute__((always_inline)) {
+    const int k_first = j0 + wrow0, k_last = k_first + 15;
+    if (k_first < lp) {
+      const auto rs = rsrc_at(pool + (size_t(pg) * hkv + kvh) * page_bytes);
+      if (k_last < lp) {
 #pragma unroll
-        for (int j = 0; j < T::NI; ++j) {
-          const int r0 = (wave * T::NI + j) * T::RPI;
-          dma16(k_pool + base + k_lane_off[j], (lds_void*)(kdst + r0 * T::RB));
-          dma16(v_pool + base + v_lane_off[j], (lds_void*)(vdst + r0 * T::RB));
-        }
+        for (int j = 0; j < T::NI; ++j)
+          dma16(rs, (lds_void*)(dst + (wrow0 + T::RPI * j) * T::RB), off[j], 0);
       } else {
-        const size_t base = (size_t(sq.cu + j0 - lp) * hkv + kvh) * T::RB;
+#pragma unroll
+        for (int j = 0; j < T::NI; ++j)
+          if (k_first + T::RPI * j + dma_row < lp)
+            dma16(rs, (lds_void*)(dst + (wrow0 + T::RPI * j) * T::RB), off[j], 0);
+      }
+    }
+    if (k_last >= lp && k_first < total_len) {
+      // base of the tile's first key as if it were a new token (it may lie
+      // before the buffer when the tile straddles the prefix end; only rows
+      // at or past the prefix end are fetched from it)
+      const ptrdiff_t row0 = ptrdiff_t(sq.cu) + j0 - lp;
+      const auto rs = rsrc_at(fresh + (row0 * hkv + kvh) * T::RB);
+      if (k_first >= lp && k_last < total_len) {
+#pragma unroll
+        for (int j = 0; j < T::NI; ++j)
+          dma16(rs, (lds_void*)(dst + (wrow0 + T::RPI * j) * T::RB), off[j] + sfx_lane,
+                sfx_uniform(j));
+      } else {
 #pragma unroll
         for (int j = 0; j < T::NI; ++j) {
-          const int r0 = (wave * T::NI + j) * T::RPI;
-          dma16(k_new + base + kf_lane_off[j], (lds_void*)(kdst + r0 * T::RB));
-          dma16(v_new + base + vf_lane_off[j], (lds_void*)(vdst + r0 * T::RB));
+          const int key = k_first + T::RPI * j + dma_row;
+          if (key >= lp && key < total_len)
+            dma16(rs, (lds_void*)(dst + (wrow0 + T::RPI * j) * T::RB), off[j] + sfx_lane,
+                  sfx_uniform(j));
         }
-      }
-      return;
-    }
-#pragma unroll
-    for (int j = 0; j < T::NI; ++j) {
-      const int r0 = (wave * T::NI + j) * T::RPI;
-      const int key = j0 + r0 + dma_row;
-      const uint8_t* ksrc = nullptr;
-      const uint8_t* vsrc = nullptr;
-      if (key < lp) {
-        const size_t base = (size_t(pg) * hkv + kvh) * page_bytes;
-        ksrc = k_pool + base + k_lane_off[j];
-        vsrc = v_pool + base + v_lane_off[j];
-      } else if (key < total_len) {
-        // kf/vf offsets hold R * hkv * RB + 16 c; the row is in the base here
-        const size_t base = (size_t(sq.cu + key - lp) * hkv + kvh) * T::RB;
-        ksrc = k_new + base + (kf_lane_off[j] - (r0 + dma_row) * hkv * T::RB);
-        vsrc = v_new + base + (vf_lane_off[j] - (r0 + dma_row) * hkv * T::RB);
-      }
-      if (ksrc != nullptr) {
-        dma16(ksrc, (lds_void*)(kdst + r0 * T::RB));
-        dma16(vsrc, (lds_void*)(vdst + r0 * T::RB));
       }
     }
   };
 
+  // ---- LDS fragment addresses (relative to a stage's base).
+  // K: k-step kk of block blk reads row swap_bits_2_3(col) + 32 blk, position
+  //    (2 kk + h) ^ k_swz(row); the swizzle of row + 32 equals that of row.
+  uint32_t k_addr[T::KT];
+  {
+    const int R = swap_bits_2_3(col);
+#pragma unroll
+    for (int kk = 0; kk < T::KT; ++kk) k_addr[kk] = R * T::RB + 16 * ((2 * kk + h) ^ k_swz<D>(R));
+  }
+  // V: slice u, block b, half e4 reads row 16 u + 8 h + 4 e4 + kq at chunk
+  //    (4 b + 2 (grp & 1) + (a >> 1)) ^ v_swz(row); v_swz depends on kq only,
+  //    so (u, e4) become immediate offsets.
+  uint32_t v_addr[T::DB];
+  {
+    const int grp = lane >> 4, ri = lane & 15;
+    const int kq = ri >> 2, a = ri & 3;
+#pragma unroll
+    for (int b = 0; b < T::DB; ++b) {
+      const int chunk = 4 * b + 2 * (grp & 1) + (a >> 1);
+      v_addr[b] = (8 * h + kq) * T::RB + 16 * (chunk ^ v_swz<D>(kq)) + 8 * (a & 1);
+    }
+  }
+
+  const float c = p.scale_log2;
   f32x16 o[T::DB];
 #pragma unroll
   for (int b = 0; b < T::DB; ++b) o[b] = f32x16{};
-  float m_run = kNegBig, l_run = 0.f;
-  const float c = p.scale_log2;
+  float m_run = 0.f, l_run = 0.f;
 
-  // page ids of the next tile (prefix keys only), loaded a tile ahead
-  int pg_next = 0;
-
-  __syncthreads();  // zero fill done before any DMA lands
-  if (it.kv_begin < it.kv_end) {
-    issue_tile(it.kv_begin, 0, load_page(it.kv_begin));
-    if (it.kv_begin + BLOCK_N < it.kv_end) pg_next = load_page(it.kv_begin + BLOCK_N);
-  }
-
-  int st = 0;
-  for (int j0 = it.kv_begin; j0 < it.kv_end; j0 += BLOCK_N, st ^= 1) {
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA of tile j0 has landed
-    __syncthreads();                // everyone's has; stage st^1 is free again
-    const int jn = j0 + BLOCK_N;
-    if (jn < it.kv_end) {
-      issue_tile(jn, st ^ 1, pg_next);
-      if (jn + BLOCK_N < it.kv_end) pg_next = load_page(jn + BLOCK_N);
-    }
-
-    if (!wave_active || j0 >= wave_max_lim) continue;  // nothing visible for this wave
-    const uint8_t* ks = lds + (2 * st) * T::TILE;
-    const uint8_t* vs = lds + (2 * st + 1) * T::TILE;
-
-    // S^T = K Q^T for two 32-key blocks (row m of block blk reads key swap(m))
-    f32x16 s[2] = {f32x16{}, f32x16{}};
+  // raw scores S^T = K Q^T of the tile in `ks`, two 32-key blocks
+  auto scores = [&](const uint8_t* ks, f32x16(&s)[2]) __attribute__((always_inline)) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < T::KT; ++kk) {
-      bf16x8 kf[2];
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        const int R = swap_bits_2_3(col) + 32 * blk;
-        const int pos = (2 * kk + h) ^ k_swz<D>(R);
-        kf[blk] = *reinterpret_cast<const bf16x8*>(ks + R * T::RB + 16 * pos);
-      }
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-        s[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[blk], qf[kk], s[blk], 0, 0, 0);
+      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(ks + k_addr[kk]);
+      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(ks + k_addr[kk] + 32 * T::RB);
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[kk], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[kk], s[1], 0, 0, 0);
     }
-
-    // element i of block blk holds key j0 + 32 blk + 16 (i / 8) + 8 h + i % 8
+  };
+  // causal mask (only tiles that cross some row's limit).  Element i of block
+  // blk holds key j0 + 32 blk + 16 (i / 8) + 8 h + i % 8.
+  auto mask = [&](int j0, f32x16(&s)[2]) __attribute__((always_inline)) {
     if (j0 + BLOCK_N > wave_min_lim) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
@@ -270,67 +292,167 @@ __global__ __launch_bounds__(THREADS) void extend_lds_kernel(ExtendParams p) {
         for (int i = 0; i < 16; ++i)
           if (j0 + 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7) >= lim) s[blk][i] = -INFINITY;
     }
-    float mx = -INFINITY;
+  };
+  // log2 units relative to the running max
+  auto to_log2 = [&](f32x16(&s)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[blk][i]);
-    mx *= c;
-    {
-      // lanes l and l + 32 hold the two halves of one row's keys
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
-                                                       false, false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    }
-    // lazy rescale: keep a stale running max until some row's max exceeds it
-    // by more than 8 (log2 units); the weights then stay below 2^8
-    if (__any(mx > m_run + 8.f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
-    }
-
-    bf16x8 pf[4];
+      for (int i = 0; i < 16; ++i) s[blk][i] = fmaf(s[blk][i], c, -m_run);
+  };
+  // bf16 weights of 16-key slice gi in B-operand order, and their half-row sum
+  // (of the rounded weights, so numerator and denominator agree)
+  auto weights = [&](const f32x16(&x)[2], bf16x8(&pf)[4], float& lsum) __attribute__((always_inline)) {
     const bf16x2 one = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
+    float la = 0.f, lb = 0.f;
 #pragma unroll
     for (int gi = 0; gi < 4; ++gi) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        pf[gi][e] = static_cast<__bf16>(
-            __builtin_amdgcn_exp2f(fmaf(s[gi >> 1][8 * (gi & 1) + e], c, -m_run)));
-      // row sum of the rounded weights, so numerator and denominator agree
+        pf[gi][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(x[gi >> 1][8 * (gi & 1) + e]));
 #pragma unroll
-      for (int e = 0; e < 8; e += 2)
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, l_run, false);
-    }
-
-    // O^T += V^T P^T over four 16-key slices; V^T fragments by transposing reads
-    {
-      const int grp = lane >> 4, ri = lane & 15;
-      const int kq = ri >> 2, a = ri & 3;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        bf16x8 vf[T::DB];
-#pragma unroll
-        for (int b = 0; b < T::DB; ++b) {
-          const int chunk = 4 * b + 2 * (grp & 1) + (a >> 1);
-          i16x4 half[2];
-#pragma unroll
-          for (int e4 = 0; e4 < 2; ++e4) {
-            const int R = 16 * u + 8 * h + 4 * e4 + kq;
-            const int off = R * T::RB + 16 * (chunk ^ v_swz<D>(R)) + 8 * (a & 1);
-            half[e4] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vs + off));
-          }
-          vf[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7));
-        }
-#pragma unroll
-        for (int b = 0; b < T::DB; ++b)
-          o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b], pf[u], o[b], 0, 0, 0);
+      for (int e = 0; e < 8; e += 4) {
+        la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, la, false);
+        lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e + 2], pf[gi][e + 3]}, one, lb, false);
       }
     }
+    lsum = la + lb;
+  };
+  // row max of x over both halves of the row (lanes l and l + 32)
+  auto row_max = [&](const f32x16(&x)[2]) -> float {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, x[blk][i]);
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                     false, false);
+    return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+  };
+  // O^T += V^T P^T over four 16-key slices of the V tile in `vs`
+  auto accumulate = [&](const uint8_t* vs, const bf16x8(&pf)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      bf16x8 vf[T::DB];
+#pragma unroll
+      for (int b = 0; b < T::DB; ++b) {
+        i16x4 half[2];
+#pragma unroll
+        for (int e4 = 0; e4 < 2; ++e4)
+          half[e4] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(vs + v_addr[b] + (16 * u + 4 * e4) * T::RB));
+        vf[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int b = 0; b < T::DB; ++b)
+        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b], pf[u], o[b], 0, 0, 0);
+    }
+  };
+
+  // Instruction interleaving for the scheduler (masks: 0x8 MFMA, 0x2 VALU,
+  // 0x400 transcendental, 0x100 LDS read).  Scores of the next tile: four K
+  // fragment reads ahead, then per MFMA two exponentials, two other vector ops
+  // and one more read.
+  auto interleave_scores_weights = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int i = 0; i < 2 * T::KT; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x400, 32 / (2 * T::KT), 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 32 / (2 * T::KT), 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+  };
+  // P V: one slice of V fragments ahead, then per MFMA two scaling FMAs and
+  // two more reads
+  auto interleave_pv_scale = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * T::DB, 0);
+#pragma unroll
+    for (int i = 0; i < 4 * T::DB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 32 / (4 * T::DB), 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+  };
+
+  const int n_tiles = (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
+  auto tile0 = [&](int j) { return it.kv_begin + j * BLOCK_N; };
+  auto visible = [&](int j) { return wave_active && tile0(j) < wave_max_lim; };
+
+  // ---- prologue: K_0, V_0 and K_1 in flight, tile 0's scores against its exact max
+  f32x16 x[2] = {f32x16{}, f32x16{}};
+  int pg_v = 0;      // page of V_{j+1} (uniform)
+  int pg_k_raw = 0;  // page of K_{j+2}, still a vector register
+  __syncthreads();   // zero fill done before any DMA lands
+  if (n_tiles > 0) {
+    const int pg0 = __builtin_amdgcn_readfirstlane(load_page(tile0(0)));
+    const int pg1 = n_tiles > 1 ? __builtin_amdgcn_readfirstlane(load_page(tile0(1))) : 0;
+    issue(tile0(0), lds_k0, pg0, k_pool, k_new, k_off);
+    issue(tile0(0), lds_v0, pg0, v_pool, v_new, v_off);
+    if (n_tiles > 1) issue(tile0(1), lds_k1, pg1, k_pool, k_new, k_off);
+    pg_v = pg1;
+    if (n_tiles > 2) pg_k_raw = load_page(tile0(2));
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (visible(0)) {
+      scores(lds_k0, x);
+      mask(tile0(0), x);
+      to_log2(x);  // m_run = 0 here
+      const float mx = row_max(x);
+      // a row with no visible key in the first tile sees none in the item
+      const float d = mx == -INFINITY ? 0.f : mx;
+      m_run = mx == -INFINITY ? kNegBig : mx;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
+    }
+  }
+
+  // iteration j: K_{j+1} and V_j are resident; K_{j+2} goes to K_j's stage,
+  // V_{j+1} to V_{j-1}'s
+  auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
+                       uint8_t* v_nxt) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA of K_{j+1} and V_j has landed
+    __syncthreads();                // everyone's has; K_j and V_{j-1} are no longer read
+    const int pg_k = __builtin_amdgcn_readfirstlane(pg_k_raw);
+    if (j + 2 < n_tiles) issue(tile0(j + 2), k_cur, pg_k, k_pool, k_new, k_off);
+    if (j + 1 < n_tiles) issue(tile0(j + 1), v_nxt, pg_v, v_pool, v_new, v_off);
+    pg_v = pg_k;
+    if (j + 3 < n_tiles) pg_k_raw = load_page(tile0(j + 3));
+
+    if (!visible(j)) return;  // nothing visible for this wave from here on
+    // tile j+1's scores (discarded after the last visible tile: the stage then
+    // holds finite stale data) while tile j's weights are formed
+    f32x16 s[2];
+    bf16x8 pf[4];
+    float lsum;
+    scores(k_nxt, s);
+    weights(x, pf, lsum);
+    interleave_scores_weights();
+    if (__any(!(lsum <= kSumLimit))) {
+      // raise the running max to this tile's row max and redo its weights
+      const float d = fmaxf(row_max(x), 0.f);
+      m_run += d;
+      const float alpha = __builtin_amdgcn_exp2f(-d);
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
+      weights(x, pf, lsum);
+    }
+    l_run += lsum;
+    mask(tile0(j + 1), s);
+    // tile j's P V while tile j+1's scores are scaled
+    accumulate(v_cur, pf);
+    to_log2(s);
+    interleave_pv_scale();
+    x[0] = s[0];
+    x[1] = s[1];
+  };
+
+  for (int j = 0; j < n_tiles; j += 2) {
+    iteration(j, lds_k0, lds_k1, lds_v0, lds_v1);
+    if (j + 1 < n_tiles) iteration(j + 1, lds_k1, lds_k0, lds_v1, lds_v0);
   }
 
   if (!wave_active) return;
