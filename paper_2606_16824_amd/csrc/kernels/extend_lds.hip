@@ -407,21 +407,12 @@ void extend_lds_kernel(ExtendParams p) {
     }
   }
 
-  // iteration j: K_{j+1} and V_j are resident; K_{j+2} goes to K_j's stage,
-  // V_{j+1} to V_{j-1}'s
-  auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
-                       uint8_t* v_nxt) __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA of K_{j+1} and V_j has landed
-    __syncthreads();                // everyone's has; K_j and V_{j-1} are no longer read
-    const int pg_k = __builtin_amdgcn_readfirstlane(pg_k_raw);
-    if (j + 2 < n_tiles) issue(tile0(j + 2), k_cur, pg_k, k_pool, k_new, k_off);
-    if (j + 1 < n_tiles) issue(tile0(j + 1), v_nxt, pg_v, v_pool, v_new, v_off);
-    pg_v = pg_k;
-    if (j + 3 < n_tiles) pg_k_raw = load_page(tile0(j + 3));
-
-    if (!visible(j)) return;  // nothing visible for this wave from here on
-    // tile j+1's scores (discarded after the last visible tile: the stage then
-    // holds finite stale data) while tile j's weights are formed
+  // the work of iteration j after its DMA is issued: tile j+1's scores
+  // (discarded after the last visible tile: the stage then holds finite stale
+  // data) while tile j's weights are formed, then tile j's P V while tile j+1's
+  // scores are scaled
+  auto compute = [&](int j, const uint8_t* k_nxt, const uint8_t* v_cur,
+                     bool may_mask) __attribute__((always_inline)) {
     f32x16 s[2];
     bf16x8 pf[4];
     float lsum;
@@ -441,8 +432,7 @@ void extend_lds_kernel(ExtendParams p) {
       weights(x, pf, lsum);
     }
     l_run += lsum;
-    mask(tile0(j + 1), s);
-    // tile j's P V while tile j+1's scores are scaled
+    if (may_mask) mask(tile0(j + 1), s);
     accumulate(v_cur, pf);
     to_log2(s);
     interleave_pv_scale();
@@ -450,7 +440,62 @@ void extend_lds_kernel(ExtendParams p) {
     x[1] = s[1];
   };
 
-  for (int j = 0; j < n_tiles; j += 2) {
+  // iteration j: K_{j+1} and V_j are resident; K_{j+2} goes to K_j's stage,
+  // V_{j+1} to V_{j-1}'s
+  auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
+                       uint8_t* v_nxt) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA of K_{j+1} and V_j has landed
+    __syncthreads();                // everyone's has; K_j and V_{j-1} are no longer read
+    const int pg_k = __builtin_amdgcn_readfirstlane(pg_k_raw);
+    if (j + 2 < n_tiles) issue(tile0(j + 2), k_cur, pg_k, k_pool, k_new, k_off);
+    if (j + 1 < n_tiles) issue(tile0(j + 1), v_nxt, pg_v, v_pool, v_new, v_off);
+    pg_v = pg_k;
+    if (j + 3 < n_tiles) pg_k_raw = load_page(tile0(j + 3));
+    if (!visible(j)) return;  // nothing visible for this wave from here on
+    compute(j, k_nxt, v_cur, true);
+  };
+
+  // Iterations whose tiles j .. j+2 lie wholly in the cached prefix: every row
+  // sees all their keys (no mask) and their DMA comes from one pool page per
+  // wave, so the loop carries no per-tile mode decisions.
+  const uint8_t* k_pool_kvh = k_pool + size_t(kvh) * page_bytes;
+  const uint8_t* v_pool_kvh = v_pool + size_t(kvh) * page_bytes;
+  const size_t page_stride = size_t(hkv) * page_bytes;
+  auto issue_prefix = [&](uint8_t* dst, int pg, const uint8_t* pool_kvh,
+                          const uint32_t(&off)[T::NI]) __attribute__((always_inline)) {
+    const auto rs = rsrc_at(pool_kvh + size_t(pg) * page_stride);
+#pragma unroll
+    for (int j = 0; j < T::NI; ++j)
+      dma16(rs, (lds_void*)(dst + (wrow0 + T::RPI * j) * T::RB), off[j], 0);
+  };
+  auto steady = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
+                    uint8_t* v_nxt) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const int pg_k = __builtin_amdgcn_readfirstlane(pg_k_raw);
+    issue_prefix(k_cur, pg_k, k_pool_kvh, k_off);
+    issue_prefix(v_nxt, pg_v, v_pool_kvh, v_off);
+    pg_v = pg_k;
+    pg_k_raw = load_page(tile0(j + 3));  // an in-range entry whenever it is a prefix page
+    if (wave_active) compute(j, k_nxt, v_cur, false);
+  };
+
+  const int n_prefix = lp > it.kv_begin ? min(n_tiles, (lp - it.kv_begin) / BLOCK_N) : 0;
+  const int n_steady = max(0, n_prefix - 2);
+  int j = 0;
+  for (; j + 1 < n_steady; j += 2) {
+    steady(j, lds_k0, lds_k1, lds_v0, lds_v1);
+    steady(j + 1, lds_k1, lds_k0, lds_v1, lds_v0);
+  }
+  if (j < n_steady) {
+    steady(j, lds_k0, lds_k1, lds_v0, lds_v1);
+    ++j;
+  }
+  if ((j & 1) && j < n_tiles) {
+    iteration(j, lds_k1, lds_k0, lds_v1, lds_v0);
+    ++j;
+  }
+  for (; j < n_tiles; j += 2) {
     iteration(j, lds_k0, lds_k1, lds_v0, lds_v1);
     if (j + 1 < n_tiles) iteration(j + 1, lds_k1, lds_k0, lds_v1, lds_v0);
   }
