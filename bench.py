@@ -153,7 +153,7 @@ def run_workload(name: str, steps: int, warmup: int):
                                           s.page_size)
     else:
         nb = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
-                                          s.gqa_group, s.head_dim, s.page_size)
+                                          s.gqa_group, s.head_dim, s.page_size, s.kv_dtype)
     ws_att = torch.empty(nb, dtype=torch.uint8, device=dev)
     ws_wr = torch.empty(cwlib.write_pages_workspace_bytes(s.num_seqs), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()

@@ -92,11 +92,13 @@ cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool
                               int32_t page_size, cw_kv_dtype_t kv_dtype, void* workspace,
                               size_t workspace_bytes, hipStream_t stream);
 
-/* Workspace bytes cw_extend_attention needs for these lengths on the current
- * device (work list plus split-K partials).  0 if the arguments are invalid. */
+/* Workspace bytes cw_extend_attention needs for these lengths and this pool
+ * dtype on the current device (work list plus split-K partials; the two pool
+ * dtypes run kernels with different row blocks, so their work lists differ).
+ * 0 if the arguments are invalid. */
 size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                  int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                                 int32_t head_dim, int32_t page_size);
+                                 int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype);
 
 /* Prefix-cached paged extend attention (CacheWise Sec. 2-3: a request that
  * extends a cached prefix computes attention only for its new tokens, over the
@@ -153,12 +155,13 @@ cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop);
  * to `capacity` work items of 8 int32 each, in launch order
  * {seq, kv_head, first packed row, key begin, key end, partial slot or -1,
  *  rows in tile, 0}; a seq of -1 marks an idle padding item.  Returns the
- * number of items, or -1 if the arguments are invalid.  Makes no HIP call
+ * number of items, or -1 if the arguments are invalid.  The plan is the one
+ * cw_extend_attention uses for a pool of `kv_dtype`.  Makes no HIP call
  * other than a cached device-property query, and works without a GPU. */
 int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                             int32_t head_dim, int32_t page_size, int32_t* items_out,
-                             int64_t capacity);
+                             int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype,
+                             int32_t* items_out, int64_t capacity);
 
 const char* cw_status_string(cw_status_t status);
 const char* cw_last_error_message(void);

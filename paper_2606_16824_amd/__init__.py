@@ -88,11 +88,20 @@ def write_pages_workspace_bytes(num_seqs: int) -> int:
     return int(library().cw_write_pages_workspace_bytes(num_seqs))
 
 
+def _dtype_code(kv_dtype) -> int:
+    if kv_dtype in ("bf16", L.CW_KV_BF16):
+        return L.CW_KV_BF16
+    if kv_dtype in ("fp8", "fp8_e4m3fn", L.CW_KV_FP8_E4M3FN):
+        return L.CW_KV_FP8_E4M3FN
+    raise ValueError(f"unsupported kv dtype {kv_dtype!r}")
+
+
 def extend_workspace_bytes(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim,
-                           page_size) -> int:
+                           page_size, kv_dtype="bf16") -> int:
     lp, ls = _lens(prefix_lens), _lens(suffix_lens)
     return int(library().cw_extend_workspace_bytes(_ptr(lp), _ptr(ls), len(lp), num_kv_heads,
-                                                   gqa_group, head_dim, page_size))
+                                                   gqa_group, head_dim, page_size,
+                                                   _dtype_code(kv_dtype)))
 
 
 def decode_workspace_bytes(prefix_lens, num_kv_heads, gqa_group, head_dim, page_size) -> int:
@@ -105,17 +114,19 @@ def set_tuning(key: int, value: int):
     _check(library().cw_set_tuning(key, value))
 
 
-def plan_items(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page_size) -> np.ndarray:
+def plan_items(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page_size,
+               kv_dtype="bf16") -> np.ndarray:
     """The extend work list in launch order, int32 [n, 8] (see cw_extend_plan_items)."""
     lp, ls = _lens(prefix_lens), _lens(suffix_lens)
     lib = library()
+    dt = _dtype_code(kv_dtype)
     n = lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
-                                 page_size, None, 0)
+                                 page_size, dt, None, 0)
     if n < 0:
         raise CWError(L.CW_ERR_UNSUPPORTED, "invalid plan arguments")
     out = np.zeros((max(n, 1), 8), dtype=np.int32)
     lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
-                             page_size, out.ctypes.data, n)
+                             page_size, dt, out.ctypes.data, n)
     return out[:n]
 
 
@@ -138,7 +149,8 @@ def extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, 
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
-        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page), q.device, None)
+        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
+                               q.device, None)
     _check(library().cw_extend_attention(
         _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
         _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),

@@ -21,7 +21,7 @@ SIGNATURES = {
     "cw_write_pages_workspace_bytes": (_sz, [_i32]),
     "cw_kv_write_pages": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32,
                                     _i32, _i32, _i32, C.c_int, _vp, _sz, _vp]),
-    "cw_extend_workspace_bytes": (_sz, [_vp, _vp, _i32, _i32, _i32, _i32, _i32]),
+    "cw_extend_workspace_bytes": (_sz, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32]),
     "cw_extend_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                       _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
                                       _vp, _sz, _vp]),
@@ -31,7 +31,7 @@ SIGNATURES = {
                                       _vp, _sz, _vp]),
     "cw_set_tuning": (C.c_int, [C.c_int, _i32]),
     "cw_set_timing_events": (C.c_int, [_vp, _vp]),
-    "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),
+    "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),
     "cw_status_string": (C.c_char_p, [C.c_int]),
     "cw_last_error_message": (C.c_char_p, []),
     "cw_version": (_i32, []),

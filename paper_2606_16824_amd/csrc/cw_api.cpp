@@ -197,12 +197,15 @@ int64_t sum_suffix(const int32_t* ls, int32_t num_seqs) {
   return t;
 }
 
+// bf16 pools run the direct-to-LDS kernel (LDS_BLOCK_M rows, one workgroup
+// per CU), fp8 pools the register-staged one (BLOCK_M rows, two per CU).
 ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t num_kv_heads,
-                     int32_t gqa_group, int32_t head_dim) {
+                     int32_t gqa_group, int32_t head_dim, cw_kv_dtype_t kv_dtype) {
   int32_t cus = 256, xcds = 8;
   device_shape(&cus, &xcds);
-  return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, cus, xcds,
-                           current_tuning());
+  const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim,
+                           fp8 ? BLOCK_M : LDS_BLOCK_M, fp8 ? 2 : 1, cus, xcds, current_tuning());
 }
 
 // Decode plans are built with the larger of the two dtypes' tile lengths so
@@ -247,7 +250,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   if ((reinterpret_cast<uintptr_t>(block_table) & 3u)) return fail(CW_ERR_ALIGN, "block_table not 4-byte aligned");
 
   ExtendPlan plan = decode ? make_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size)
-                           : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim);
+                           : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype);
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
 
@@ -369,13 +372,15 @@ cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool
 
 size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                  int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                                 int32_t head_dim, int32_t page_size) {
+                                 int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype) {
   if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
   if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
                  head_dim, false) != CW_OK)
     return 0;
   if (num_seqs == 0) return 256;
-  return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim).total_bytes;
+  return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype)
+      .total_bytes;
 }
 
 cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_new,
@@ -442,13 +447,15 @@ cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop) {
 
 int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                             int32_t head_dim, int32_t page_size, int32_t* items_out,
-                             int64_t capacity) {
+                             int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype,
+                             int32_t* items_out, int64_t capacity) {
   if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return -1;
+  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return -1;
   if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
                  head_dim, false) != CW_OK)
     return -1;
-  ExtendPlan plan = make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim);
+  ExtendPlan plan =
+      make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype);
   const int64_t n = static_cast<int64_t>(plan.items.size());
   if (items_out) {
     for (int64_t i = 0; i < std::min(n, capacity); ++i) {
@@ -476,6 +483,6 @@ const char* cw_status_string(cw_status_t status) {
 
 const char* cw_last_error_message(void) { return g_last_error.c_str(); }
 
-int32_t cw_version(void) { return 100; }
+int32_t cw_version(void) { return 101; }
 
 }  // extern "C"

@@ -8,13 +8,20 @@
 
 namespace cw {
 
-// Tile shape of the extend kernel: a workgroup owns BLOCK_M packed query rows
-// (row = token * G + group member) of one (sequence, kv head) and walks keys
-// BLOCK_N at a time.
+// Tile shapes of the extend kernels: a workgroup owns a block of packed query
+// rows (row = token * G + group member) of one (sequence, kv head) and walks
+// keys BLOCK_N at a time.  Every wave64 owns 32 rows.
+//  - register-staged kernel (fp8 pools): BLOCK_M rows, four waves, two
+//    workgroups per CU;
+//  - direct-to-LDS kernel (bf16 pools): LDS_BLOCK_M rows, eight waves, one
+//    workgroup per CU, so each staged K/V tile serves twice as many rows.
 constexpr int BLOCK_M = 128;
 constexpr int BLOCK_N = 64;
-constexpr int WAVES = 4;  // four wave64s, 32 query rows each
+constexpr int WAVES = 4;
 constexpr int THREADS = WAVES * 64;
+constexpr int LDS_WAVES = 8;
+constexpr int LDS_THREADS = LDS_WAVES * 64;
+constexpr int LDS_BLOCK_M = LDS_WAVES * 32;
 
 // Per-sequence metadata on the device.
 struct SeqInfo {
@@ -65,8 +72,8 @@ struct ExtendParams {
   const SeqInfo* seqs;
   const WorkItem* items;
   const CombineGroup* groups;
-  float* part_o;   // [n_parts, BLOCK_M, D]
-  float* part_ml;  // [n_parts, BLOCK_M, 2]  (running max in log2 units, sum)
+  float* part_o;   // [n_parts, part_rows, D]
+  float* part_ml;  // [n_parts, part_rows, 2]  (running max in log2 units, sum)
   int32_t bt_stride;
   int32_t num_kv_heads;
   int32_t gqa_group;
@@ -74,7 +81,7 @@ struct ExtendParams {
   float scale_log2;  // softmax_scale * log2(e)
   int32_t n_items;
   int32_t n_groups;
-  int32_t part_rows;  // rows per split-K partial slot (BLOCK_M for extend, G for decode)
+  int32_t part_rows;  // rows per split-K partial slot (the row block for extend, G for decode)
 };
 
 struct WriteParams {

@@ -1,10 +1,12 @@
 // Prefix-cached paged extend attention, bf16 pools: direct-to-LDS staging with
 // a software-pipelined tile loop.
 //
-// Work decomposition and math follow the register-staged kernel (one workgroup
-// = four wave64s = 128 packed query rows of one (sequence, kv head);
-// S^T = K Q^T and O^T += V^T P^T with v_mfma_f32_32x32x16_bf16), with three
-// changes aimed at the CDNA4 issue model, where every MFMA holds the vector
+// The math follows the register-staged kernel (each wave64 owns 32 packed
+// query rows of one (sequence, kv head); S^T = K Q^T and O^T += V^T P^T with
+// v_mfma_f32_32x32x16_bf16), but a workgroup is eight waves = 256 rows, one
+// per CU, so every K/V tile brought into LDS serves twice the rows (the
+// tile DMA's share of the LDS and vector-memory pipes halves per FLOP).  Three
+// more changes aim at the CDNA4 issue model, where every MFMA holds the vector
 // issue port for half its duration and the exponentials of the softmax cost as
 // much port time as the matrix products:
 //
@@ -30,7 +32,7 @@
 // XOR-swizzled per row so that every fragment read is bank-conflict free:
 //   K row R, chunk c at position c ^ k_swz(R);  V row R, chunk c at c ^ v_swz(R)
 // The DMA writes lane l's 16 bytes at base + 16 l, so each lane fetches the
-// global chunk that belongs at its position.  Each wave fetches 16 consecutive
+// global chunk that belongs at its position.  Each wave fetches 8 consecutive
 // rows of a tile, which lie in one page (P = 16 or 64).
 //
 // V^T operand: ds_read_b64_tr_b16 hands lane i of each 16-lane group element
@@ -104,15 +106,15 @@ struct LGeo {
   static constexpr int RB = 2 * D;                    // bytes per K/V row
   static constexpr int CPR = D / 8;                   // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;                // rows per wave DMA instruction
-  static constexpr int NI = BLOCK_N / RPI / WAVES;    // DMA instructions per wave per matrix
+  static constexpr int NI = BLOCK_N / RPI / LDS_WAVES;  // DMA instructions per wave per matrix
   static constexpr int TILE = BLOCK_N * RB;           // bytes of one K (or V) tile
   static constexpr int KT = D / 16;                   // k-steps of K Q^T
   static constexpr int DB = D / 32;                   // 32-row blocks of O^T
-  static_assert(NI * RPI == 16, "each wave fetches 16 rows of a tile");
+  static_assert(NI * RPI == 8, "each wave fetches 8 rows of a tile");
 };
 
 template <int D, int P>
-__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(LDS_THREADS) __attribute__((amdgpu_waves_per_eu(2)))
 void extend_lds_kernel(ExtendParams p) {
   using T = LGeo<D, P>;
   // two-stage rings of K and V tiles, each stage its own array so the compiler
@@ -150,7 +152,7 @@ void extend_lds_kernel(ExtendParams p) {
   const int wave_max_lim = lp + wave_last_row / G + 1;
 
   // stale LDS must be finite: rows past the sequence are never fetched
-  for (int i = tid; i < T::TILE / 16; i += THREADS) {
+  for (int i = tid; i < T::TILE / 16; i += LDS_THREADS) {
     reinterpret_cast<u32x4*>(lds_k0)[i] = u32x4{0u, 0u, 0u, 0u};
     reinterpret_cast<u32x4*>(lds_k1)[i] = u32x4{0u, 0u, 0u, 0u};
     reinterpret_cast<u32x4*>(lds_v0)[i] = u32x4{0u, 0u, 0u, 0u};
@@ -170,14 +172,14 @@ void extend_lds_kernel(ExtendParams p) {
     }
   }
 
-  // ---- DMA geometry.  Wave w fetches tile rows [16 w, 16 w + 16); its
-  // instruction j covers rows R0_j = 16 w + RPI j .. + RPI - 1 and lane l fetches
+  // ---- DMA geometry.  Wave w fetches tile rows [8 w, 8 w + 8); its
+  // instruction j covers rows R0_j = 8 w + RPI j .. + RPI - 1 and lane l fetches
   // row R0_j + l / CPR into position l % CPR.  Within a page block the lane's
   // source offset is (R % P) RB + 16 chunk; a suffix row lives at R hkv RB +
   // 16 chunk from the tile's first new row, which is the same offset plus
   // sfx_lane (per lane) plus sfx_uniform(j) (per instruction).
   const int dma_row = lane / T::CPR, dma_pos = lane % T::CPR;
-  const int wrow0 = 16 * wave;
+  const int wrow0 = 8 * wave;
   uint32_t k_off[T::NI], v_off[T::NI];
 #pragma unroll
   for (int j = 0; j < T::NI; ++j) {
@@ -195,7 +197,12 @@ void extend_lds_kernel(ExtendParams p) {
   // physical page of this wave's rows of the tile at j0 (0 if they hold no
   // prefix key).  The load stays a vector register until the tile is issued an
   // iteration later, so waiting for it never waits for the DMA issued meanwhile.
-  auto load_page = [&](int j0) -> int { return (j0 + wrow0 < lp) ? bt[(j0 + wrow0) / P] : 0; };
+  // Read through the constant address space so the load is a scalar one: it
+  // counts against lgkmcnt instead of vmcnt, so waiting for it never waits for
+  // tile DMA issued before it.
+  typedef __attribute__((address_space(4))) const int32_t const_i32;
+  const_i32* bt_s = (const_i32*)bt;
+  auto load_page = [&](int j0) -> int { return (j0 + wrow0 < lp) ? bt_s[(j0 + wrow0) / P] : 0; };
 
   // DMA of one matrix (K or V) of the tile at j0 into dst.  Rows of the cached
   // prefix come from the pool page `pg`, rows of the suffix from the new
@@ -204,7 +211,7 @@ void extend_lds_kernel(ExtendParams p) {
   // prefix end or the sequence end.
   auto issue = [&](int j0, uint8_t* dst, int pg, const uint8_t* pool, const uint8_t* fresh,
                    const uint32_t(&off)[T::NI]) __attribute__((always_inline)) {
-    const int k_first = j0 + wrow0, k_last = k_first + 15;
+    const int k_first = j0 + wrow0, k_last = k_first + 7;
     if (k_first < lp) {
       const auto rs = rsrc_at(pool + (size_t(pg) * hkv + kvh) * page_bytes);
       if (k_last < lp) {
@@ -540,7 +547,7 @@ void extend_lds_kernel(ExtendParams p) {
 
 template <int D, int P>
 hipError_t launch_t(const ExtendParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((extend_lds_kernel<D, P>), dim3(p.n_items), dim3(THREADS), 0, stream, p);
+  hipLaunchKernelGGL((extend_lds_kernel<D, P>), dim3(p.n_items), dim3(LDS_THREADS), 0, stream, p);
   return hipGetLastError();
 }
 

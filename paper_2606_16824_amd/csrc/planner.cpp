@@ -1,6 +1,6 @@
 // Extend work planner (host).
 //
-// Work unit: one query tile (BLOCK_M packed rows of one sequence and kv head)
+// Work unit: one query tile (block_m packed rows of one sequence and kv head)
 // over a contiguous range of keys.  A tile whose rows end at token t_last needs
 // keys [0, Lp + t_last + 1) (bottom-right causal).  When there are too few
 // tiles to fill the GPU, each tile's key range is split into chunks of about
@@ -42,8 +42,8 @@ void layout_workspace(ExtendPlan& plan, int32_t head_dim);
 
 ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                             int32_t head_dim, int32_t num_cus, int32_t num_xcds,
-                             const Tuning& tuning) {
+                             int32_t head_dim, int32_t block_m, int32_t wgs_per_cu,
+                             int32_t num_cus, int32_t num_xcds, const Tuning& tuning) {
   ExtendPlan plan;
   plan.seqs.resize(num_seqs);
   int64_t cu = 0;
@@ -57,8 +57,8 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
   int64_t total_kt = 0;
   for (int32_t b = 0; b < num_seqs; ++b) {
     const int64_t rows = int64_t(suffix_lens[b]) * gqa_group;
-    for (int64_t r0 = 0; r0 < rows; r0 += BLOCK_M) {
-      const int32_t nr = static_cast<int32_t>(std::min<int64_t>(BLOCK_M, rows - r0));
+    for (int64_t r0 = 0; r0 < rows; r0 += block_m) {
+      const int32_t nr = static_cast<int32_t>(std::min<int64_t>(block_m, rows - r0));
       const int64_t t_last = (r0 + nr - 1) / gqa_group;
       const int32_t kv_len = static_cast<int32_t>(prefix_lens[b] + t_last + 1);
       const int32_t n_kt = (kv_len + BLOCK_N - 1) / BLOCK_N;
@@ -70,10 +70,11 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
   }
 
   // 2. split-K: number of chunks per tile.  Automatic: when there are fewer
-  // tiles than `target` workgroups (two resident per CU), each tile gets about
-  // n_kt / (total_kt / target) chunks, so chunks are of about equal length and
-  // their count is close to the target.
-  const int64_t target = tuning.target_wgs > 0 ? tuning.target_wgs : 2LL * num_cus;
+  // tiles than `target` workgroups (all resident at once), each tile gets
+  // about n_kt / (total_kt / target) chunks, so chunks are of about equal
+  // length and their count is close to the target.
+  const int64_t target =
+      tuning.target_wgs > 0 ? tuning.target_wgs : int64_t(std::max(1, wgs_per_cu)) * num_cus;
   double chunk_len = 0.0;  // 0: no split
   if (tuning.kv_chunk_tiles > 0) {
     chunk_len = tuning.kv_chunk_tiles;
@@ -177,7 +178,7 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
   while (!plan.items.empty() && plan.items.back().seq < 0) plan.items.pop_back();
 
   // 6. workspace layout
-  plan.part_rows = BLOCK_M;
+  plan.part_rows = block_m;
   layout_workspace(plan, head_dim);
   return plan;
 }

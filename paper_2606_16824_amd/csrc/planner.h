@@ -24,15 +24,16 @@ struct ExtendPlan {
   size_t off_seqs = 0, off_items = 0, off_groups = 0, off_part_o = 0, off_part_ml = 0;
   size_t meta_bytes = 0;  // seqs + items + groups: the part uploaded per call
   size_t total_bytes = 0;
-  int32_t part_rows = BLOCK_M;  // rows per partial slot
+  int32_t part_rows = 0;  // rows per partial slot
 };
 
-// Builds the plan.  `num_cus` and `num_xcds` describe the device.
-// Lengths must already be validated.
+// Builds the plan for a kernel whose workgroups own `block_m` rows and of
+// which `wgs_per_cu` are resident per CU.  `num_cus` and `num_xcds` describe
+// the device.  Lengths must already be validated.
 ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                             int32_t head_dim, int32_t num_cus, int32_t num_xcds,
-                             const Tuning& tuning);
+                             int32_t head_dim, int32_t block_m, int32_t wgs_per_cu,
+                             int32_t num_cus, int32_t num_xcds, const Tuning& tuning);
 
 // Decode plan (every suffix length 1): one item per (sequence, kv head, key
 // chunk) with `gqa_group` rows; `keys_per_tile` is the decode kernel's tile.

@@ -113,8 +113,10 @@ def test_write_pages_validation():
 def test_workspace_query_rejects_bad_args():
     lp = np.array([5], dtype=np.int32)
     ls = np.array([-1], dtype=np.int32)
-    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, ls.ctypes.data, 1, 1, 1, 64, 16) == 0
-    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 72, 16) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, ls.ctypes.data, 1, 1, 1, 64, 16, 0) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 72, 16, 0) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16, 7) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16, 0) > 0
 
 
 def test_tuning_keys():

@@ -4,11 +4,13 @@ import pytest
 
 import paper_2606_16824_amd as cwlib
 
-BM, BN = 128, 64
+BN = 64
+BM = {"bf16": 256, "fp8": 128}  # rows per work item of each pool dtype's kernel
 
 
-def check_plan(lp, ls, hkv, g, d=128, p=16):
-    items = cwlib.plan_items(lp, ls, hkv, g, d, p)
+def check_plan(lp, ls, hkv, g, d=128, p=16, dt="bf16"):
+    items = cwlib.plan_items(lp, ls, hkv, g, d, p, dt)
+    bm = BM[dt]
     real = items[items[:, 0] >= 0]
     # every (seq, kv head, query tile) key range [0, kv_len) is covered exactly once
     cover = {}
@@ -17,8 +19,8 @@ def check_plan(lp, ls, hkv, g, d=128, p=16):
         cover.setdefault((seq, kvh, r0), []).append((kb, ke, part, rows))
     for b in range(len(lp)):
         nrows = ls[b] * g
-        for r0 in range(0, nrows, BM):
-            rows = min(BM, nrows - r0)
+        for r0 in range(0, nrows, bm):
+            rows = min(bm, nrows - r0)
             kv_len = lp[b] + (r0 + rows - 1) // g + 1
             for h in range(hkv):
                 ch = sorted(cover.pop((b, h, r0)))
@@ -37,19 +39,22 @@ def check_plan(lp, ls, hkv, g, d=128, p=16):
     return items
 
 
-def test_turn_plan_fills_two_workgroups_per_cu():
-    items = check_plan([16384], [1024], 8, 4)
-    assert len(items) == 512
-    # XCD-aware: workgroup i runs on XCD i % 8; all work of a kv head on one XCD
-    for x in range(8):
-        assert len(set(items[x::8, 1].tolist())) == 1
+def test_turn_plan_fills_every_cu():
+    # bf16: 256-row items, one resident per CU; fp8: 128-row items, two per CU
+    for dt, n in (("bf16", 256), ("fp8", 512)):
+        items = check_plan([16384], [1024], 8, 4, dt=dt)
+        assert len(items) == n
+        # XCD-aware: workgroup i runs on XCD i % 8; all work of a kv head on one XCD
+        for x in range(8):
+            assert len(set(items[x::8, 1].tolist())) == 1
 
 
 def test_long_plan_is_unsplit_and_head_aligned():
-    items = check_plan([131072], [8192], 8, 8, p=64)
-    assert len(items) == 4096 and np.all(items[:, 5] == -1)
-    for x in range(8):
-        assert len(set(items[x::8, 1].tolist())) == 1
+    for dt, n in (("bf16", 2048), ("fp8", 4096)):
+        items = check_plan([131072], [8192], 8, 8, p=64, dt=dt)
+        assert len(items) == n and np.all(items[:, 5] == -1)
+        for x in range(8):
+            assert len(set(items[x::8, 1].tolist())) == 1
 
 
 @pytest.mark.parametrize("lp,ls,hkv,g", [
@@ -59,14 +64,15 @@ def test_long_plan_is_unsplit_and_head_aligned():
     ([5000, 30000, 12000], [1, 1, 1], 8, 4),
     ([100] * 40, [300] * 40, 4, 2),
 ])
-def test_plan_coverage(lp, ls, hkv, g):
-    check_plan(np.array(lp), np.array(ls), hkv, g)
+@pytest.mark.parametrize("dt", ["bf16", "fp8"])
+def test_plan_coverage(lp, ls, hkv, g, dt):
+    check_plan(np.array(lp), np.array(ls), hkv, g, dt=dt)
 
 
 def test_forced_chunking():
     cwlib.set_tuning(0, 3)
     try:
-        items = check_plan(np.array([700]), np.array([150]), 2, 4)
+        items = check_plan(np.array([700]), np.array([150]), 2, 4, dt="fp8")
         real = items[items[:, 0] >= 0]
         assert np.all(real[:, 4] - real[:, 3] <= 3 * BN)
     finally:
