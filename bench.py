@@ -73,7 +73,7 @@ def calibrate_copy(mib: int):
 
 KERNEL_SOURCES = {  # dominant kernel per pool dtype: (kernel, source, profile summary)
     "bf16": ("extend_lds_kernel", "paper_2606_16824_amd/csrc/kernels/extend_lds.hip", "extend_lds_{wl}.md"),
-    "fp8": ("extend_kernel", "paper_2606_16824_amd/csrc/kernels/extend_attn.hip", "extend_fp8_{wl}.md"),
+    "fp8": ("extend_lds_kernel", "paper_2606_16824_amd/csrc/kernels/extend_lds.hip", "extend_lds_{wl}.md"),
 }
 
 
@@ -191,7 +191,7 @@ def run_workload(name: str, steps: int, warmup: int):
     lib.cw_set_timing_events(None, None)
     ms = t_start.elapsed_time(t_stop) / steps
     kern_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)]))
-    kernel = KERNEL_SOURCES[s.kv_dtype][0]
+    kernel = "decode_kernel" if decode else KERNEL_SOURCES[s.kv_dtype][0]
     return {"spec": s, "workload": w, "ms": ms, "kern_ms": kern_ms, "kernel": kernel}
 
 

@@ -197,15 +197,15 @@ int64_t sum_suffix(const int32_t* ls, int32_t num_seqs) {
   return t;
 }
 
-// bf16 pools run the direct-to-LDS kernel (LDS_BLOCK_M rows, one workgroup
-// per CU), fp8 pools the register-staged one (BLOCK_M rows, two per CU).
+// Both pool dtypes run the LDS-staged kernel: LDS_BLOCK_M rows per work item,
+// one workgroup per CU.
 ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t num_kv_heads,
                      int32_t gqa_group, int32_t head_dim, cw_kv_dtype_t kv_dtype) {
+  (void)kv_dtype;
   int32_t cus = 256, xcds = 8;
   device_shape(&cus, &xcds);
-  const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
-  return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim,
-                           fp8 ? BLOCK_M : LDS_BLOCK_M, fp8 ? 2 : 1, cus, xcds, current_tuning());
+  return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, LDS_BLOCK_M, 1,
+                           cus, xcds, current_tuning());
 }
 
 // Decode plans are built with the larger of the two dtypes' tile lengths so
@@ -294,8 +294,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
   if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
-  else if (fp8) e = launch_extend(p, head_dim, page_size, true, stream);
-  else e = launch_extend_lds(p, head_dim, page_size, stream);
+  else e = launch_extend_lds(p, head_dim, page_size, fp8, stream);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
   if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if (p.n_groups > 0) {

@@ -8,17 +8,11 @@
 
 namespace cw {
 
-// Tile shapes of the extend kernels: a workgroup owns a block of packed query
-// rows (row = token * G + group member) of one (sequence, kv head) and walks
-// keys BLOCK_N at a time.  Every wave64 owns 32 rows.
-//  - register-staged kernel (fp8 pools): BLOCK_M rows, four waves, two
-//    workgroups per CU;
-//  - direct-to-LDS kernel (bf16 pools): LDS_BLOCK_M rows, eight waves, one
-//    workgroup per CU, so each staged K/V tile serves twice as many rows.
-constexpr int BLOCK_M = 128;
+// Tile shape of the extend kernel: a workgroup of LDS_WAVES wave64s owns
+// LDS_BLOCK_M packed query rows (row = token * G + group member, 32 per wave)
+// of one (sequence, kv head) and walks keys BLOCK_N at a time; one workgroup
+// is resident per CU.
 constexpr int BLOCK_N = 64;
-constexpr int WAVES = 4;
-constexpr int THREADS = WAVES * 64;
 constexpr int LDS_WAVES = 8;
 constexpr int LDS_THREADS = LDS_WAVES * 64;
 constexpr int LDS_BLOCK_M = LDS_WAVES * 32;
@@ -100,9 +94,8 @@ struct WriteParams {
 };
 
 // Kernel launchers (each defined in the translation unit of its kernel).
-hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
-                         hipStream_t stream);
-hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream);
+hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
+                             hipStream_t stream);
 hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream);
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream);

@@ -1,0 +1,108 @@
+// Split-K merge of extend / decode partials.
+#include <hip/hip_runtime.h>
+
+#include "../cw_internal.h"
+
+namespace cw {
+namespace {
+
+constexpr float kLn2 = 0.69314718055994531f;
+
+// Merges the split-K partials of query rows: weights 2^(m_c - max m),
+// O = sum w_c O_c / sum w_c l_c.  A workgroup of 256 lanes covers ROWS rows;
+// each row's SLICES slices of 32 lanes fold every SLICES-th partial with an
+// online merge, then the slices are merged through LDS (SLICES = 1 for a few
+// partials per row, 8 for many).  Fixed order, no atomics.
+template <int D, int SLICES>
+__global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
+  constexpr int ROWS = 8 / SLICES;
+  constexpr int PER = D / 32;  // dims per lane
+  __shared__ float sh_o[ROWS][SLICES][D];
+  __shared__ float sh_m[ROWS][SLICES], sh_l[ROWS][SLICES];
+  const int wg_per_group = (p.part_rows + ROWS - 1) / ROWS;
+  const int grp = blockIdx.x / wg_per_group;
+  const int rsub = threadIdx.x / (32 * SLICES);
+  const int lr = (blockIdx.x % wg_per_group) * ROWS + rsub;
+  const CombineGroup cg = p.groups[grp];
+  const bool active = lr < cg.rows;
+  const int slice = (threadIdx.x / 32) % SLICES, d0 = (threadIdx.x % 32) * PER;
+
+  float m = -INFINITY, L = 0.f, acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  for (int c = slice; active && c < cg.n_parts; c += SLICES) {
+    const size_t pr = size_t(cg.part0 + c) * p.part_rows + lr;
+    const float mc = p.part_ml[pr * 2], lc = p.part_ml[pr * 2 + 1];
+    const float m_new = fmaxf(m, mc);
+    const float a = exp2f(m - m_new), w = exp2f(mc - m_new);
+    const float* po = p.part_o + pr * D + d0;
+    L = L * a + w * lc;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = acc[e] * a + w * po[e];
+    m = m_new;
+  }
+  if (SLICES > 1) {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) sh_o[rsub][slice][d0 + e] = acc[e];
+    if (threadIdx.x % 32 == 0) {
+      sh_m[rsub][slice] = m;
+      sh_l[rsub][slice] = L;
+    }
+    __syncthreads();
+  }
+  if (slice != 0 || !active) return;
+  float mstar = -INFINITY;
+  if (SLICES == 1) {
+    mstar = m;
+  } else {
+#pragma unroll
+    for (int s = 0; s < SLICES; ++s) mstar = fmaxf(mstar, sh_m[rsub][s]);
+  }
+  float Lt = 0.f, out[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) out[e] = 0.f;
+  if (SLICES == 1) {
+    Lt = L;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) out[e] = acc[e];
+  } else {
+#pragma unroll
+    for (int s = 0; s < SLICES; ++s) {
+      const float w = sh_m[rsub][s] == -INFINITY ? 0.f : exp2f(sh_m[rsub][s] - mstar);
+      Lt += w * sh_l[rsub][s];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) out[e] += w * sh_o[rsub][s][d0 + e];
+    }
+  }
+  const SeqInfo sq = p.seqs[cg.seq];
+  const int G = p.gqa_group, hq = p.num_kv_heads * G;
+  const int r = cg.q_row0 + lr;
+  const int t = r / G, g = r - t * G;
+  const float inv = 1.f / Lt;
+  uint16_t* orow = static_cast<uint16_t*>(p.out) + (size_t(sq.cu + t) * hq + size_t(cg.kvh) * G + g) * D + d0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) orow[e] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(out[e] * inv));
+  if (p.lse != nullptr && threadIdx.x % 32 == 0)
+    p.lse[size_t(sq.cu + t) * hq + size_t(cg.kvh) * G + g] = (mstar + log2f(Lt)) * kLn2;
+}
+
+}  // namespace
+
+hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream) {
+  if (p.n_groups <= 0) return hipSuccess;
+  const bool many = max_parts > 4;
+  const int rows_per_wg = many ? 1 : 8;
+  const dim3 grid(p.n_groups * ((p.part_rows + rows_per_wg - 1) / rows_per_wg));
+  if (head_dim == 64) {
+    if (many) hipLaunchKernelGGL((combine_kernel<64, 8>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((combine_kernel<64, 1>), grid, dim3(256), 0, stream, p);
+  } else if (head_dim == 128) {
+    if (many) hipLaunchKernelGGL((combine_kernel<128, 8>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((combine_kernel<128, 1>), grid, dim3(256), 0, stream, p);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace cw

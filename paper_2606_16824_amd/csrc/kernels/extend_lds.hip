@@ -1,11 +1,10 @@
-// Prefix-cached paged extend attention, bf16 pools: direct-to-LDS staging with
-// a software-pipelined tile loop.
+// Prefix-cached paged extend attention on LDS-staged tiles, software-pipelined.
 //
 // The math follows the register-staged kernel (each wave64 owns 32 packed
 // query rows of one (sequence, kv head); S^T = K Q^T and O^T += V^T P^T with
 // v_mfma_f32_32x32x16_bf16), but a workgroup is eight waves = 256 rows, one
-// per CU, so every K/V tile brought into LDS serves twice the rows (the
-// tile DMA's share of the LDS and vector-memory pipes halves per FLOP).  Three
+// per CU, so every K/V tile brought into LDS serves twice the rows (the tile
+// staging's share of the LDS and vector-memory pipes halves per FLOP).  Three
 // more changes aim at the CDNA4 issue model, where every MFMA holds the vector
 // issue port for half its duration and the exponentials of the softmax cost as
 // much port time as the matrix products:
@@ -14,7 +13,7 @@
 //    computes tile j's weights (exp2, bf16 pack, row sums); while tile j's
 //    P V MFMAs run, it scales and masks tile j+1's scores.  K tiles and V tiles
 //    rotate through separate two-stage rings: in iteration j the wave reads
-//    K_{j+1} and V_j while K_{j+2} and V_{j+1} land, one barrier per tile.
+//    K_{j+1} and V_j while K_{j+2} and V_{j+1} are staged, one barrier per tile.
 //
 //  * A max-free fast path.  The running max m is only raised when it has to
 //    be: the weights exp2(s c - m) of a tile are computed against the current
@@ -23,16 +22,27 @@
 //    (the final O / l and the log-sum-exp do not depend on which m was used).
 //    The first tile of an item sets m to its exact row max.
 //
-//  * Buffer-addressed DMA.  K and V tiles travel from HBM straight into LDS
-//    with buffer_load_dwordx4 ... lds: the page base sits in the scalar buffer
-//    descriptor and each lane's offset within the page is a constant register,
-//    so issuing a tile costs no vector instructions.
+//  * Buffer-addressed staging.  The page base sits in a scalar buffer
+//    descriptor and each lane's offset within the page is a constant register.
+//    bf16 rows travel from HBM straight into LDS (buffer_load_dwordx4 ... lds);
+//    fp8-e4m3fn pool rows are loaded into registers one iteration ahead,
+//    widened exactly to bf16 (every e4m3fn value is a bf16 value) and stored to
+//    the same LDS layout, each lane converting only the 16 bytes it loaded, so
+//    the compute loop is the same for both pool dtypes.
+//
+// fp8 scales (one K and one V scale per (page, kv head)) never touch the
+// tiles: the K scale multiplies a page's scores and log2 of the V scale is
+// added to their exponent, so P arrives already multiplied by the V scale,
+// rounded to bf16 once, and the row sum divides it back out (dot with the
+// bf16-rounded reciprocal).  A 16-key group of a tile lies in one page; per
+// tile, one wave per page computes the group's three numbers and leaves them in
+// a small LDS ring.  A tile straddling the prefix end treats each key on its own.
 //
 // LDS holds K and V rows in their natural [key][dim] order, 16-byte chunks
 // XOR-swizzled per row so that every fragment read is bank-conflict free:
 //   K row R, chunk c at position c ^ k_swz(R);  V row R, chunk c at c ^ v_swz(R)
 // The DMA writes lane l's 16 bytes at base + 16 l, so each lane fetches the
-// global chunk that belongs at its position.  Each wave fetches 8 consecutive
+// global chunk that belongs at its position.  Each wave stages 8 consecutive
 // rows of a tile, which lie in one page (P = 16 or 64).
 //
 // V^T operand: ds_read_b64_tr_b16 hands lane i of each 16-lane group element
@@ -57,6 +67,11 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+// Read through the constant address space so that loads with a uniform
+// address are scalar loads: they count against lgkmcnt instead of vmcnt, so
+// waiting for them never waits for tile staging issued before them.
+typedef __attribute__((address_space(4))) const int32_t const_i32;
+typedef __attribute__((address_space(4))) const float const_f32;
 
 constexpr float kNegBig = -1.0e30f;
 constexpr float kLn2 = 0.69314718055994531f;
@@ -64,6 +79,7 @@ constexpr float kLn2 = 0.69314718055994531f;
 // running max: weights then stay below 2^16 and fp32 accumulators far from
 // overflow.
 constexpr float kSumLimit = 65536.f;
+constexpr uint32_t kOnePair = 0x3F803F80u;  // bf16 pair (1, 1)
 
 // Raw buffer descriptor for `base` (no stride, no range limit in practice).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_at(const void* base) {
@@ -77,6 +93,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_at(const void* base) {
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_void* dst, uint32_t voff,
                                       uint32_t soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+}
+
+// Two e4m3fn codes (bytes 0,1 or 2,3 of `w`) -> two bf16 in one dword, exact
+// (a unit scale leaves the value as it is).
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(uint32_t,
+                            __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(static_cast<int>(w), 1.0f, HI));
+}
+__device__ __forceinline__ u32x4 fp8x8_bf16x8(uint32_t lo, uint32_t hi) {
+  return u32x4{fp8x2_bf16x2<false>(lo), fp8x2_bf16x2<true>(lo), fp8x2_bf16x2<false>(hi),
+               fp8x2_bf16x2<true>(hi)};
 }
 
 __device__ __forceinline__ int swap_bits_2_3(int r) {
@@ -101,28 +129,33 @@ __device__ __forceinline__ int v_swz(int row) {
   return D == 128 ? 4 * (row & 3) : 4 * ((row >> 1) & 1);
 }
 
-template <int D, int P>
+template <int D, int P, bool FP8>
 struct LGeo {
-  static constexpr int RB = 2 * D;                    // bytes per K/V row
+  static constexpr int RB = 2 * D;                    // bytes per bf16 K/V row in LDS
   static constexpr int CPR = D / 8;                   // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;                // rows per wave DMA instruction
   static constexpr int NI = BLOCK_N / RPI / LDS_WAVES;  // DMA instructions per wave per matrix
   static constexpr int TILE = BLOCK_N * RB;           // bytes of one K (or V) tile
   static constexpr int KT = D / 16;                   // k-steps of K Q^T
   static constexpr int DB = D / 32;                   // 32-row blocks of O^T
-  static_assert(NI * RPI == 8, "each wave fetches 8 rows of a tile");
+  static constexpr int PRB = FP8 ? D : RB;            // bytes per pool row
+  static constexpr int B8 = D / 8;                    // fp8 bytes each lane stages per matrix
+  static_assert(NI * RPI == 8, "each wave stages 8 rows of a tile");
 };
 
-template <int D, int P>
+template <int D, int P, bool FP8>
 __global__ __launch_bounds__(LDS_THREADS) __attribute__((amdgpu_waves_per_eu(2)))
 void extend_lds_kernel(ExtendParams p) {
-  using T = LGeo<D, P>;
+  using T = LGeo<D, P, FP8>;
   // two-stage rings of K and V tiles, each stage its own array so the compiler
   // can tell that reads of one stage never alias the DMA in flight into another
   __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[T::TILE];
+  // fp8: per-tile group numbers, ring of four tiles: [0,4) K scale times the
+  // softmax scale, [4,8) log2 of the V scale, [8,12) 1 / V scale (fp32 bits)
+  __shared__ __attribute__((aligned(16))) uint32_t prm[4][12];
 
   const WorkItem it = p.items[blockIdx.x];
   if (it.seq < 0) return;  // idle padding item (uniform across the workgroup)
@@ -151,7 +184,7 @@ void extend_lds_kernel(ExtendParams p) {
   const int wave_last_row = it.q_row0 + min(wave * 32 + 31, it.rows - 1);
   const int wave_max_lim = lp + wave_last_row / G + 1;
 
-  // stale LDS must be finite: rows past the sequence are never fetched
+  // stale LDS must be finite: rows past the sequence are never staged
   for (int i = tid; i < T::TILE / 16; i += LDS_THREADS) {
     reinterpret_cast<u32x4*>(lds_k0)[i] = u32x4{0u, 0u, 0u, 0u};
     reinterpret_cast<u32x4*>(lds_k1)[i] = u32x4{0u, 0u, 0u, 0u};
@@ -172,12 +205,12 @@ void extend_lds_kernel(ExtendParams p) {
     }
   }
 
-  // ---- DMA geometry.  Wave w fetches tile rows [8 w, 8 w + 8); its
-  // instruction j covers rows R0_j = 8 w + RPI j .. + RPI - 1 and lane l fetches
-  // row R0_j + l / CPR into position l % CPR.  Within a page block the lane's
-  // source offset is (R % P) RB + 16 chunk; a suffix row lives at R hkv RB +
-  // 16 chunk from the tile's first new row, which is the same offset plus
-  // sfx_lane (per lane) plus sfx_uniform(j) (per instruction).
+  // ---- staging geometry.  Wave w stages tile rows [8 w, 8 w + 8).
+  // bf16 rows: DMA instruction j covers rows R0_j = 8 w + RPI j .. + RPI - 1 and
+  // lane l fetches row R0_j + l / CPR into position l % CPR.  Within a page
+  // block the lane's source offset is (R % P) RB + 16 chunk; a suffix row lives
+  // at R hkv RB + 16 chunk from the tile's first new row, which is the same
+  // offset plus sfx_lane (per lane) plus sfx_uniform(j) (per instruction).
   const int dma_row = lane / T::CPR, dma_pos = lane % T::CPR;
   const int wrow0 = 8 * wave;
   uint32_t k_off[T::NI], v_off[T::NI];
@@ -192,27 +225,25 @@ void extend_lds_kernel(ExtendParams p) {
     const int R0 = wrow0 + T::RPI * j;
     return uint32_t((R0 * hkv - R0 % P) * T::RB);
   };
-  const size_t page_bytes = size_t(P) * T::RB;  // one (page, kv head) block
+  const size_t page_bytes = size_t(P) * T::PRB;  // one (page, kv head) block
+  // fp8 rows: lane l stages bytes [B8 (l % 8), B8 (l % 8 + 1)) of row 8 w + l / 8
+  const int r8 = wrow0 + (lane >> 3), q8 = lane & 7;
+  const uint32_t off8 = uint32_t((r8 % P) * D + q8 * T::B8);
 
-  // physical page of this wave's rows of the tile at j0 (0 if they hold no
-  // prefix key).  The load stays a vector register until the tile is issued an
-  // iteration later, so waiting for it never waits for the DMA issued meanwhile.
-  // Read through the constant address space so the load is a scalar one: it
-  // counts against lgkmcnt instead of vmcnt, so waiting for it never waits for
-  // tile DMA issued before it.
-  typedef __attribute__((address_space(4))) const int32_t const_i32;
   const_i32* bt_s = (const_i32*)bt;
+  // physical page of this wave's rows of the tile at j0 (0 if they hold no prefix key)
   auto load_page = [&](int j0) -> int { return (j0 + wrow0 < lp) ? bt_s[(j0 + wrow0) / P] : 0; };
 
   // DMA of one matrix (K or V) of the tile at j0 into dst.  Rows of the cached
-  // prefix come from the pool page `pg`, rows of the suffix from the new
-  // tokens; rows past the sequence are left as they are (their scores are
-  // masked).  Wave-uniform branches except where the wave's rows straddle the
-  // prefix end or the sequence end.
+  // prefix come from the pool page `pg` (bf16 pools only: fp8 rows are widened
+  // through registers), rows of the suffix from the new tokens; rows past the
+  // sequence are left as they are (their scores are masked).  Wave-uniform
+  // branches except where the wave's rows straddle the prefix end or the
+  // sequence end.
   auto issue = [&](int j0, uint8_t* dst, int pg, const uint8_t* pool, const uint8_t* fresh,
                    const uint32_t(&off)[T::NI]) __attribute__((always_inline)) {
     const int k_first = j0 + wrow0, k_last = k_first + 7;
-    if (k_first < lp) {
+    if (!FP8 && k_first < lp) {
       const auto rs = rsrc_at(pool + (size_t(pg) * hkv + kvh) * page_bytes);
       if (k_last < lp) {
 #pragma unroll
@@ -248,6 +279,36 @@ void extend_lds_kernel(ExtendParams p) {
     }
   };
 
+  // fp8 pool rows of the tile at j0 into registers (nothing when this wave's
+  // rows hold no prefix key; rows of the page past the prefix end are loaded
+  // but never stored)
+  auto load8 = [&](int j0, int pg, const uint8_t* pool) __attribute__((always_inline)) -> u32x4 {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (j0 + wrow0 < lp) {
+      const auto rs = rsrc_at(pool + (size_t(pg) * hkv + kvh) * page_bytes);
+      if constexpr (T::B8 == 16) {
+        v = __builtin_amdgcn_raw_buffer_load_b128(rs, off8, 0, 0);
+      } else {
+        const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(rs, off8, 0, 0);
+        v = u32x4{w.x, w.y, 0u, 0u};
+      }
+    }
+    return v;
+  };
+  // ... widened to bf16 and stored at the swizzled positions of their rows
+  auto store8 = [&](int j0, u32x4 v, uint8_t* dst, bool is_k) __attribute__((always_inline)) {
+    if (j0 + wrow0 < lp && j0 + r8 < lp) {
+      const int swz = is_k ? k_swz<D>(r8) : v_swz<D>(r8);
+      uint8_t* row = dst + r8 * T::RB;
+      if constexpr (T::B8 == 16) {
+        *reinterpret_cast<u32x4*>(row + 16 * ((2 * q8) ^ swz)) = fp8x8_bf16x8(v.x, v.y);
+        *reinterpret_cast<u32x4*>(row + 16 * ((2 * q8 + 1) ^ swz)) = fp8x8_bf16x8(v.z, v.w);
+      } else {
+        *reinterpret_cast<u32x4*>(row + 16 * (q8 ^ swz)) = fp8x8_bf16x8(v.x, v.y);
+      }
+    }
+  };
+
   // ---- LDS fragment addresses (relative to a stage's base).
   // K: k-step kk of block blk reads row swap_bits_2_3(col) + 32 blk, position
   //    (2 kk + h) ^ k_swz(row); the swizzle of row + 32 equals that of row.
@@ -277,6 +338,37 @@ void extend_lds_kernel(ExtendParams p) {
   for (int b = 0; b < T::DB; ++b) o[b] = f32x16{};
   float m_run = 0.f, l_run = 0.f;
 
+  const int n_tiles = (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
+  auto tile0 = [&](int j) { return it.kv_begin + j * BLOCK_N; };
+  auto visible = [&](int j) { return wave_active && tile0(j) < wave_max_lim; };
+  // tile crosses the prefix end: fp8 scales apply key by key
+  auto straddles = [&](int j0) { return j0 < lp && lp < j0 + BLOCK_N; };
+
+  // ---- fp8 group numbers.  Group gi (keys 16 gi .. 16 gi + 15 of a tile) lies
+  // in page (16 gi) / P of the tile; the wave staging the group's first rows
+  // (P = 16: wave 2 gi; P = 64: wave 0 for all four groups) writes them.
+  const_f32* ks_s = (const_f32*)p.k_scale;
+  const_f32* vs_s = (const_f32*)p.v_scale;
+  const bool prm_writer = P == 16 ? (wave & 1) == 0 : wave == 0;
+  // this wave's page scales for the tile at j0 (1 where its rows hold no prefix key)
+  auto load_scales = [&](int j0, int pg, float& ksc, float& vsc) __attribute__((always_inline)) {
+    const bool pre = j0 + wrow0 < lp;
+    const size_t si = size_t(pg) * hkv + kvh;
+    ksc = pre ? ks_s[si] : 1.f;
+    vsc = pre ? vs_s[si] : 1.f;
+  };
+  auto write_params = [&](int j0, int slot, float ksc, float vsc) __attribute__((always_inline)) {
+    if (!prm_writer || lane != 0) return;
+    const float cg = c * ksc, lv = __builtin_amdgcn_logf(vsc), iv = 1.f / vsc;
+    const int g0 = P == 16 ? (wave >> 1) : 0, g1 = P == 16 ? g0 + 1 : 4;
+    for (int gi = g0; gi < g1; ++gi) {
+      const bool pre = j0 + 16 * gi < lp;  // any prefix key in the group
+      prm[slot][gi] = __float_as_uint(pre ? cg : c);
+      prm[slot][4 + gi] = __float_as_uint(pre ? lv : 0.f);
+      prm[slot][8 + gi] = __float_as_uint(pre ? iv : 1.f);
+    }
+  };
+
   // raw scores S^T = K Q^T of the tile in `ks`, two 32-key blocks
   auto scores = [&](const uint8_t* ks, f32x16(&s)[2]) __attribute__((always_inline)) {
     s[0] = f32x16{};
@@ -290,7 +382,8 @@ void extend_lds_kernel(ExtendParams p) {
     }
   };
   // causal mask (only tiles that cross some row's limit).  Element i of block
-  // blk holds key j0 + 32 blk + 16 (i / 8) + 8 h + i % 8.
+  // blk holds key j0 + 32 blk + 16 (i / 8) + 8 h + i % 8, which is in group
+  // 2 blk + i / 8.
   auto mask = [&](int j0, f32x16(&s)[2]) __attribute__((always_inline)) {
     if (j0 + BLOCK_N > wave_min_lim) {
 #pragma unroll
@@ -300,30 +393,90 @@ void extend_lds_kernel(ExtendParams p) {
           if (j0 + 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7) >= lim) s[blk][i] = -INFINITY;
     }
   };
-  // log2 units relative to the running max
-  auto to_log2 = [&](f32x16(&s)[2]) __attribute__((always_inline)) {
+  // log2 units relative to the running max (fp8: times the page's K scale,
+  // plus log2 of its V scale)
+  auto to_log2 = [&](int j0, int slot, f32x16(&s)[2]) __attribute__((always_inline)) {
+    if constexpr (!FP8) {
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk)
+      for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s[blk][i] = fmaf(s[blk][i], c, -m_run);
+        for (int i = 0; i < 16; ++i) s[blk][i] = fmaf(s[blk][i], c, -m_run);
+    } else {
+      uint32_t cgv[4], lvv[4];
+#pragma unroll
+      for (int gi = 0; gi < 4; ++gi) {
+        cgv[gi] = prm[slot][gi];
+        lvv[gi] = prm[slot][4 + gi];
+      }
+      if (!straddles(j0)) {
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) {
+          const float cg = __uint_as_float(cgv[gi]), lo = __uint_as_float(lvv[gi]) - m_run;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            s[gi >> 1][8 * (gi & 1) + e] = fmaf(s[gi >> 1][8 * (gi & 1) + e], cg, lo);
+        }
+      } else {
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bool pre = j0 + 16 * gi + 8 * h + e < lp;
+            s[gi >> 1][8 * (gi & 1) + e] =
+                fmaf(s[gi >> 1][8 * (gi & 1) + e], pre ? __uint_as_float(cgv[gi]) : c,
+                     (pre ? __uint_as_float(lvv[gi]) : 0.f) - m_run);
+          }
+      }
+    }
   };
   // bf16 weights of 16-key slice gi in B-operand order, and their half-row sum
-  // (of the rounded weights, so numerator and denominator agree)
-  auto weights = [&](const f32x16(&x)[2], bf16x8(&pf)[4], float& lsum) __attribute__((always_inline)) {
-    const bf16x2 one = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
-    float la = 0.f, lb = 0.f;
+  // (of the rounded weights, so numerator and denominator agree).  fp8: each
+  // weight carries its page's V scale, which the sum divides back out: per
+  // 16-key group the rounded weights are summed, then scaled by 1 / V scale in
+  // fp32 (key by key in a tile straddling the prefix end).
+  auto weights = [&](int j0, int slot, const f32x16(&x)[2], bf16x8(&pf)[4],
+                     float& lsum) __attribute__((always_inline)) {
+    const bf16x2 one = __builtin_bit_cast(bf16x2, kOnePair);
 #pragma unroll
-    for (int gi = 0; gi < 4; ++gi) {
+    for (int gi = 0; gi < 4; ++gi)
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         pf[gi][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(x[gi >> 1][8 * (gi & 1) + e]));
+    if constexpr (!FP8) {
+      float la = 0.f, lb = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; e += 4) {
-        la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, la, false);
-        lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e + 2], pf[gi][e + 3]}, one, lb, false);
+      for (int gi = 0; gi < 4; ++gi)
+#pragma unroll
+        for (int e = 0; e < 8; e += 4) {
+          la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, la, false);
+          lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e + 2], pf[gi][e + 3]}, one, lb, false);
+        }
+      lsum = la + lb;
+    } else {
+      float iv[4];
+#pragma unroll
+      for (int gi = 0; gi < 4; ++gi) iv[gi] = __uint_as_float(prm[slot][8 + gi]);
+      float acc = 0.f;
+      if (!straddles(j0)) {
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) {
+          float la = 0.f, lb = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; e += 4) {
+            la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, la, false);
+            lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e + 2], pf[gi][e + 3]}, one, lb, false);
+          }
+          acc = fmaf(la + lb, iv[gi], acc);
+        }
+      } else {
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi)
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            acc = fmaf(static_cast<float>(pf[gi][e]), j0 + 16 * gi + 8 * h + e < lp ? iv[gi] : 1.f, acc);
       }
+      lsum = acc;
     }
-    lsum = la + lb;
   };
   // row max of x over both halves of the row (lanes l and l + 32)
   auto row_max = [&](const f32x16(&x)[2]) -> float {
@@ -382,29 +535,53 @@ void extend_lds_kernel(ExtendParams p) {
     }
   };
 
-  const int n_tiles = (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
-  auto tile0 = [&](int j) { return it.kv_begin + j * BLOCK_N; };
-  auto visible = [&](int j) { return wave_active && tile0(j) < wave_max_lim; };
-
-  // ---- prologue: K_0, V_0 and K_1 in flight, tile 0's scores against its exact max
+  // ---- prologue: tiles 0 and 1 of K and tile 0 of V staged, tile 0's scores
+  // against its exact max.  bf16: K_0, V_0, K_1 by DMA, the loop then stages
+  // K_{j+2} and V_{j+1} in iteration j.  fp8: the same tiles widened here, and
+  // the loop's first iteration finds K_2 and V_1 already in registers.
   f32x16 x[2] = {f32x16{}, f32x16{}};
-  int pg_v = 0;      // page of V_{j+1} (uniform)
-  int pg_k_raw = 0;  // page of K_{j+2}, still a vector register
-  __syncthreads();   // zero fill done before any DMA lands
+  int pg_v = 0;    // bf16: page of V_{j+1};  fp8: page of V_{j+2} (uniform)
+  int pg_raw = 0;  // bf16: page of K_{j+2};  fp8: page of K_{j+3} (scalar load in flight)
+  u32x4 k8 = {0u, 0u, 0u, 0u}, v8 = {0u, 0u, 0u, 0u};  // fp8: K_{j+2}, V_{j+1} rows
+  float ks_n = 1.f, vs_n = 1.f;  // fp8: this wave's page scales of tile j+2
+  __syncthreads();  // zero fill done before any tile lands
   if (n_tiles > 0) {
-    const int pg0 = __builtin_amdgcn_readfirstlane(load_page(tile0(0)));
-    const int pg1 = n_tiles > 1 ? __builtin_amdgcn_readfirstlane(load_page(tile0(1))) : 0;
+    const int pg0 = load_page(tile0(0));
+    const int pg1 = n_tiles > 1 ? load_page(tile0(1)) : 0;
     issue(tile0(0), lds_k0, pg0, k_pool, k_new, k_off);
     issue(tile0(0), lds_v0, pg0, v_pool, v_new, v_off);
     if (n_tiles > 1) issue(tile0(1), lds_k1, pg1, k_pool, k_new, k_off);
-    pg_v = pg1;
-    if (n_tiles > 2) pg_k_raw = load_page(tile0(2));
+    if constexpr (!FP8) {
+      pg_v = pg1;
+      if (n_tiles > 2) pg_raw = load_page(tile0(2));
+    } else {
+      const u32x4 a = load8(tile0(0), pg0, k_pool), b = load8(tile0(0), pg0, v_pool);
+      u32x4 k1 = {0u, 0u, 0u, 0u};
+      if (n_tiles > 1) k1 = load8(tile0(1), pg1, k_pool);
+      float ks0, vs0, ks1 = 1.f, vs1 = 1.f;
+      load_scales(tile0(0), pg0, ks0, vs0);
+      if (n_tiles > 1) load_scales(tile0(1), pg1, ks1, vs1);
+      const int pg2 = n_tiles > 2 ? load_page(tile0(2)) : 0;
+      __builtin_amdgcn_s_waitcnt(0);
+      store8(tile0(0), a, lds_k0, true);
+      store8(tile0(0), b, lds_v0, false);
+      if (n_tiles > 1) store8(tile0(1), k1, lds_k1, true);
+      write_params(tile0(0), 0, ks0, vs0);
+      if (n_tiles > 1) write_params(tile0(1), 1, ks1, vs1);
+      if (n_tiles > 2) {
+        k8 = load8(tile0(2), pg2, k_pool);
+        load_scales(tile0(2), pg2, ks_n, vs_n);
+      }
+      if (n_tiles > 1) v8 = load8(tile0(1), pg1, v_pool);
+      pg_v = pg2;
+      if (n_tiles > 3) pg_raw = load_page(tile0(3));
+    }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (visible(0)) {
       scores(lds_k0, x);
       mask(tile0(0), x);
-      to_log2(x);  // m_run = 0 here
+      to_log2(tile0(0), 0, x);  // m_run = 0 here
       const float mx = row_max(x);
       // a row with no visible key in the first tile sees none in the item
       const float d = mx == -INFINITY ? 0.f : mx;
@@ -414,7 +591,7 @@ void extend_lds_kernel(ExtendParams p) {
     }
   }
 
-  // the work of iteration j after its DMA is issued: tile j+1's scores
+  // the work of iteration j after its staging is issued: tile j+1's scores
   // (discarded after the last visible tile: the stage then holds finite stale
   // data) while tile j's weights are formed, then tile j's P V while tile j+1's
   // scores are scaled
@@ -424,7 +601,7 @@ void extend_lds_kernel(ExtendParams p) {
     bf16x8 pf[4];
     float lsum;
     scores(k_nxt, s);
-    weights(x, pf, lsum);
+    weights(tile0(j), j & 3, x, pf, lsum);
     interleave_scores_weights();
     if (__any(!(lsum <= kSumLimit))) {
       // raise the running max to this tile's row max and redo its weights
@@ -436,35 +613,62 @@ void extend_lds_kernel(ExtendParams p) {
       for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
-      weights(x, pf, lsum);
+      weights(tile0(j), j & 3, x, pf, lsum);
     }
     l_run += lsum;
     if (may_mask) mask(tile0(j + 1), s);
     accumulate(v_cur, pf);
-    to_log2(s);
+    to_log2(tile0(j + 1), (j + 1) & 3, s);
     interleave_pv_scale();
     x[0] = s[0];
     x[1] = s[1];
+  };
+
+  // fp8 staging of iteration j (after the barrier): widen K_{j+2} (into K_j's
+  // stage) and V_{j+1} (into V_{j-1}'s) from registers, leave tile j+2's group
+  // numbers, then load K_{j+3} and V_{j+2}
+  auto stage8 = [&](int j, uint8_t* k_cur, uint8_t* v_nxt,
+                    bool all_prefix) __attribute__((always_inline)) {
+    if (all_prefix || j + 2 < n_tiles) {
+      store8(tile0(j + 2), k8, k_cur, true);
+      write_params(tile0(j + 2), (j + 2) & 3, ks_n, vs_n);
+    }
+    if (all_prefix || j + 1 < n_tiles) store8(tile0(j + 1), v8, v_nxt, false);
+    const int pg3 = pg_raw;
+    if (all_prefix || j + 3 < n_tiles) {
+      k8 = load8(tile0(j + 3), pg3, k_pool);
+      load_scales(tile0(j + 3), pg3, ks_n, vs_n);
+    }
+    if (all_prefix || j + 2 < n_tiles) v8 = load8(tile0(j + 2), pg_v, v_pool);
+    pg_v = pg3;
+    pg_raw = load_page(tile0(j + 4));  // an in-range entry whenever it is a prefix page
   };
 
   // iteration j: K_{j+1} and V_j are resident; K_{j+2} goes to K_j's stage,
   // V_{j+1} to V_{j-1}'s
   auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
                        uint8_t* v_nxt) __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's DMA of K_{j+1} and V_j has landed
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's staging of K_{j+1} and V_j has landed
     __syncthreads();                // everyone's has; K_j and V_{j-1} are no longer read
-    const int pg_k = __builtin_amdgcn_readfirstlane(pg_k_raw);
-    if (j + 2 < n_tiles) issue(tile0(j + 2), k_cur, pg_k, k_pool, k_new, k_off);
-    if (j + 1 < n_tiles) issue(tile0(j + 1), v_nxt, pg_v, v_pool, v_new, v_off);
-    pg_v = pg_k;
-    if (j + 3 < n_tiles) pg_k_raw = load_page(tile0(j + 3));
+    if constexpr (!FP8) {
+      const int pg_k = pg_raw;
+      if (j + 2 < n_tiles) issue(tile0(j + 2), k_cur, pg_k, k_pool, k_new, k_off);
+      if (j + 1 < n_tiles) issue(tile0(j + 1), v_nxt, pg_v, v_pool, v_new, v_off);
+      pg_v = pg_k;
+      if (j + 3 < n_tiles) pg_raw = load_page(tile0(j + 3));
+    } else {
+      if (j + 2 < n_tiles) issue(tile0(j + 2), k_cur, 0, k_pool, k_new, k_off);
+      if (j + 1 < n_tiles) issue(tile0(j + 1), v_nxt, 0, v_pool, v_new, v_off);
+      stage8(j, k_cur, v_nxt, false);
+    }
     if (!visible(j)) return;  // nothing visible for this wave from here on
     compute(j, k_nxt, v_cur, true);
   };
 
-  // Iterations whose tiles j .. j+2 lie wholly in the cached prefix: every row
-  // sees all their keys (no mask) and their DMA comes from one pool page per
-  // wave, so the loop carries no per-tile mode decisions.
+  // Iterations whose staged tiles lie wholly in the cached prefix (bf16: tiles
+  // j .. j+2; fp8: j .. j+3): every row sees all their keys (no mask) and
+  // their rows come from one pool page per wave, so the loop carries no
+  // per-tile mode decisions.
   const uint8_t* k_pool_kvh = k_pool + size_t(kvh) * page_bytes;
   const uint8_t* v_pool_kvh = v_pool + size_t(kvh) * page_bytes;
   const size_t page_stride = size_t(hkv) * page_bytes;
@@ -479,16 +683,20 @@ void extend_lds_kernel(ExtendParams p) {
                     uint8_t* v_nxt) __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    const int pg_k = __builtin_amdgcn_readfirstlane(pg_k_raw);
-    issue_prefix(k_cur, pg_k, k_pool_kvh, k_off);
-    issue_prefix(v_nxt, pg_v, v_pool_kvh, v_off);
-    pg_v = pg_k;
-    pg_k_raw = load_page(tile0(j + 3));  // an in-range entry whenever it is a prefix page
+    if constexpr (!FP8) {
+      const int pg_k = pg_raw;
+      issue_prefix(k_cur, pg_k, k_pool_kvh, k_off);
+      issue_prefix(v_nxt, pg_v, v_pool_kvh, v_off);
+      pg_v = pg_k;
+      pg_raw = load_page(tile0(j + 3));  // an in-range entry whenever it is a prefix page
+    } else {
+      stage8(j, k_cur, v_nxt, true);
+    }
     if (wave_active) compute(j, k_nxt, v_cur, false);
   };
 
   const int n_prefix = lp > it.kv_begin ? min(n_tiles, (lp - it.kv_begin) / BLOCK_N) : 0;
-  const int n_steady = max(0, n_prefix - 2);
+  const int n_steady = max(0, n_prefix - (FP8 ? 3 : 2));
   int j = 0;
   for (; j + 1 < n_steady; j += 2) {
     steady(j, lds_k0, lds_k1, lds_v0, lds_v1);
@@ -545,21 +753,25 @@ void extend_lds_kernel(ExtendParams p) {
   }
 }
 
-template <int D, int P>
+template <int D, int P, bool FP8>
 hipError_t launch_t(const ExtendParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((extend_lds_kernel<D, P>), dim3(p.n_items), dim3(LDS_THREADS), 0, stream, p);
+  hipLaunchKernelGGL((extend_lds_kernel<D, P, FP8>), dim3(p.n_items), dim3(LDS_THREADS), 0, stream, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size,
+hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                              hipStream_t stream) {
   if (p.n_items <= 0) return hipSuccess;
-  if (head_dim == 64 && page_size == 16) return launch_t<64, 16>(p, stream);
-  if (head_dim == 64 && page_size == 64) return launch_t<64, 64>(p, stream);
-  if (head_dim == 128 && page_size == 16) return launch_t<128, 16>(p, stream);
-  if (head_dim == 128 && page_size == 64) return launch_t<128, 64>(p, stream);
+#define CW_LDS_CASE(D_, P_)                                                        \
+  if (head_dim == D_ && page_size == P_)                                           \
+    return fp8 ? launch_t<D_, P_, true>(p, stream) : launch_t<D_, P_, false>(p, stream);
+  CW_LDS_CASE(64, 16)
+  CW_LDS_CASE(64, 64)
+  CW_LDS_CASE(128, 16)
+  CW_LDS_CASE(128, 64)
+#undef CW_LDS_CASE
   return hipErrorInvalidValue;
 }
 
