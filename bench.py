@@ -74,15 +74,17 @@ def calibrate_copy(mib: int):
 KERNEL_SOURCES = {  # dominant kernel per pool dtype: (kernel, source, profile summary)
     "bf16": ("extend_lds_kernel", "paper_2606_16824_amd/csrc/kernels/extend_lds.hip", "extend_lds_{wl}.md"),
     "fp8": ("extend_lds_kernel", "paper_2606_16824_amd/csrc/kernels/extend_lds.hip", "extend_lds_{wl}.md"),
+    "decode": ("decode_kernel", "paper_2606_16824_amd/csrc/kernels/decode.hip", "decode_kernel_{wl}.md"),
 }
 
 
-def measured_traffic(kv_dtype: str, workload: str):
+def measured_traffic(kind: str, workload: str):
     """HBM bytes per launch from the committed counter summary, or None when the
-    summary is missing or was taken on a different version of the kernel source."""
+    summary is missing or was taken on a different version of the kernel source.
+    `kind` is the pool dtype of an extend workload, or "decode"."""
     import hashlib
     import re
-    kernel, src, prof = KERNEL_SOURCES[kv_dtype]
+    kernel, src, prof = KERNEL_SOURCES[kind]
     path = os.path.join(ROOT, "profiles", prof.format(wl=workload))
     try:
         text = open(path).read()
@@ -219,7 +221,7 @@ def main():
         value = nbytes / (ms * 1e-3) / 1e9
         achieved = nbytes / (kern_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode", args.workload),
                 "kernel": res["kernel"], "kernel_ms": round(kern_ms, 5)}
         unit = "GB/s"
     else:
@@ -261,7 +263,8 @@ def main():
             "GB_s": round(nbytes / (d["ms"] * 1e-3) / 1e9, 1),
             "kernel_GB_s": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9, 1),
             "frac_hbm_peak": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "algorithmic_bytes": nbytes, "kernel": d["kernel"]}
+            "algorithmic_bytes": nbytes, "traffic": measured_traffic("decode", "decode"),
+            "kernel": d["kernel"]}
         print(f"[bench] decode step {d['ms']:.4f} ms, kernel {d['kern_ms']:.4f} ms", file=sys.stderr,
               flush=True)
     if args.cpu_seconds > 0:
