@@ -4,8 +4,9 @@
 // against a chunk of at most 64 pages of one sequence's cached prefix, plus the
 // new token's own key when the chunk ends the sequence.  A decode step reads
 // each cached K/V byte once, so the kernel is bound by HBM bandwidth; it keeps
-// three 16 KB tiles per wave in flight with global_load_lds_dwordx4 and uses no
-// barriers (every wave owns its LDS).  Three waves fit a CU (144 KB of LDS).
+// three tiles per wave in flight with global_load_lds_dwordx4 (16 KB tiles for
+// bf16 pools, three waves per CU; 8 KB for fp8 pools, six waves per CU: 144 KB
+// of LDS either way) and uses no barriers (every wave owns its LDS).
 //
 // Math per tile (same formulation as the extend kernels): S^T = K Q^T with
 // v_mfma_f32_32x32x16_bf16 (queries padded to 32 columns), base-2 online softmax
@@ -41,20 +42,34 @@ typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 constexpr float kNegBig = -1.0e30f;
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr int kStages = 3;
-constexpr int kTileBytes = 16384;  // K + V of one tile
+// K + V bytes of one tile: 16 KB for bf16 pools (three waves per CU), 8 KB for
+// fp8 pools, whose tiles cost twice the math per byte: six waves per CU (two
+// per SIMD) hide each other's MFMA and LDS latencies with the same bytes in
+// flight per CU
+__host__ __device__ constexpr int tile_bytes(bool fp8) { return fp8 ? 8192 : 16384; }
 
-// 16 bytes per lane from global memory straight into LDS (lane l at dst + 16 l);
-// kept out of the kernel template (see the extend kernel for why).
-__device__ __forceinline__ void dma16(const void* src, lds_void* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+// 16 bytes per lane from global memory straight into LDS (lane l at LDS
+// address m0 + 16 l).  Issued as inline assembly, so the compiler neither
+// counts these loads nor guards LDS reads against them: the kernel's own
+// vmcnt waits, whose counts are exact (every tile issues the same number of
+// DMA instructions), order each stage's reads after its DMA.  The compiler's
+// own tracking merges its per-array state conservatively at the loop header
+// and would drain every DMA in flight there.  Loads it does count stay
+// correct: extra outstanding DMA only makes its count-based waits stricter.
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds_addr) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds_addr) : "memory");
 }
 
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+// s_waitcnt on one counter, also a compiler barrier for memory accesses
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void*)p));
 }
 
 __device__ __forceinline__ int swap_bits_2_3(int r) {
@@ -79,7 +94,8 @@ template <int D, int P, bool FP8>
 struct DGeo {
   static constexpr int ELEM = FP8 ? 1 : 2;
   static constexpr int RB = D * ELEM;                  // bytes per K/V row
-  static constexpr int KPT = kTileBytes / (2 * RB);    // keys per tile
+  static constexpr int TILE = tile_bytes(FP8);         // K + V bytes per tile
+  static constexpr int KPT = TILE / (2 * RB);          // keys per tile
   static constexpr int CPR = RB / 16;                  // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;                 // rows per DMA instruction
   static constexpr int NI = KPT / RPI;                 // DMA instructions per matrix per tile
@@ -112,7 +128,12 @@ __device__ __forceinline__ int v_swz8(int row) {
 template <int D, int P, bool FP8>
 __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   using T = DGeo<D, P, FP8>;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kTileBytes];
+  // one array per stage; the tile loop is unrolled by the stage count, so
+  // every step addresses a fixed array
+  static_assert(kStages == 3, "the tile loop below is unrolled by three");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_s0[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_s1[T::TILE];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_s2[T::TILE];
 
   const WorkItem it = p.items[blockIdx.x];
   if (it.seq < 0) return;
@@ -133,9 +154,6 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   const int ke = min(it.kv_end, lp);
   const bool has_new = it.kv_end > lp;
   const int n_tiles = ke > kb ? (ke - kb + T::KPT - 1) / T::KPT : 0;
-
-  for (int i = lane; i < kStages * kTileBytes / 16; i += 64)
-    reinterpret_cast<u32x4*>(lds)[i] = u32x4{0u, 0u, 0u, 0u};
 
   // page ids (and fp8 scales) of the chunk: lane j holds page kb / P + j
   const int page0 = kb / P;
@@ -167,26 +185,26 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   }
 
   // DMA: instruction j covers tile rows [j RPI, (j+1) RPI); lane fetches row
-  // j RPI + lane / CPR into chunk position lane % CPR
+  // j RPI + lane / CPR into chunk position lane % CPR.  Rows past the chunk's
+  // prefix end fetch the chunk's last key again (same page as the instruction's
+  // first row, whose scores are masked), so every tile issues exactly 2 NI
+  // instructions and the vmcnt arithmetic below is exact.
   const int dma_row = lane / T::CPR, dma_pos = lane % T::CPR;
-  auto issue_tile = [&](int t, int st) __attribute__((always_inline)) {
+  auto issue_tile = [&](int t, uint32_t kdst) __attribute__((always_inline)) {
     const int j0 = kb + t * T::KPT;
-    uint8_t* kdst = lds + st * kTileBytes;
-    uint8_t* vdst = kdst + kTileBytes / 2;
+    const uint32_t vdst = kdst + T::TILE / 2;
 #pragma unroll
     for (int j = 0; j < T::NI; ++j) {
       const int R = j * T::RPI + dma_row;
-      const int key = j0 + R;
-      // page index within the chunk (uniform per instruction)
-      const int pg = __builtin_amdgcn_readlane(my_pg, min((j0 + j * T::RPI) / P - page0, 63));
-      const size_t base = (size_t(pg) * hkv + kvh) * P * T::RB + size_t((j0 + j * T::RPI) % P) * T::RB;
-      const uint32_t row_off = dma_row * T::RB;
+      const int key = min(j0 + R, ke - 1);
+      // page index within the chunk (uniform per instruction: its rows lie in one page)
+      const int r0 = min(j0 + j * T::RPI, ke - 1);
+      const int pg = __builtin_amdgcn_readlane(my_pg, min(r0 / P - page0, 63));
+      const size_t base = (size_t(pg) * hkv + kvh) * P * T::RB + size_t(key % P) * T::RB;
       const uint32_t kc = dma_pos ^ k_swz<T::RB>(R);
       const uint32_t vc = dma_pos ^ (FP8 ? v_swz8<T::RB>(R) : v_swz16<T::RB>(R));
-      if (key < ke) {
-        dma16(k_pool + base + row_off + 16 * kc, (lds_void*)(kdst + j * T::RPI * T::RB));
-        dma16(v_pool + base + row_off + 16 * vc, (lds_void*)(vdst + j * T::RPI * T::RB));
-      }
+      dma16(k_pool + base + 16 * kc, kdst + j * T::RPI * T::RB);
+      dma16(v_pool + base + 16 * vc, vdst + j * T::RPI * T::RB);
     }
   };
 
@@ -196,25 +214,19 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   float m_run = kNegBig, l_run = 0.f;
   const float c = p.scale_log2;
 
-  // prologue: tiles 0 .. kStages-2 in flight (always issue kStages-1 groups so
-  // that the vmcnt arithmetic below is exact; empty groups issue nothing, which
-  // only makes the waits stricter)
-#pragma unroll
-  for (int t = 0; t < kStages - 1; ++t)
-    if (t < n_tiles) issue_tile(t, t);
+  // prologue: tiles 0, 1 and 2 in flight.  Q and the page ids land first (the
+  // addresses need the ids), so only DMA is outstanding in the loop; this wait
+  // is the compiler's own, so it knows that Q has landed.
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+  if (n_tiles > 0) {
+    issue_tile(0, lds_addr(lds_s0));
+    issue_tile(1, lds_addr(lds_s1));
+    issue_tile(2, lds_addr(lds_s2));
+  }
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int st = t % kStages;
-    if (t + kStages - 1 < n_tiles) {
-      issue_tile(t + kStages - 1, (t + kStages - 1) % kStages);
-      wait_vmcnt<(kStages - 1) * 2 * T::NI>();  // tile t landed; the later two may fly
-    } else if (t + 1 < n_tiles) {
-      wait_vmcnt<2 * T::NI>();  // only tile t+1 may still fly
-    } else {
-      wait_vmcnt<0>();
-    }
-    const uint8_t* ks = lds + st * kTileBytes;
-    const uint8_t* vs = ks + kTileBytes / 2;
+  // compute on tile t, read from stage ks once it has landed
+  auto compute = [&](int t, const uint8_t* ks) __attribute__((always_inline)) {
+    const uint8_t* vs = ks + T::TILE / 2;
     const int j0 = kb + t * T::KPT;
 
 #pragma unroll
@@ -317,7 +329,24 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
         }
       }
     }
+  };
+  // Tile t lives in stage t % 3.  Every step waits for its tile (the two
+  // issued after it may still fly), computes on it, then refills the stage with
+  // tile t + 3.  Steps past the last tile compute nothing, and issues past it
+  // fetch the chunk's last key again, so each step issues exactly 2 NI
+  // instructions and one fixed wait count holds everywhere.
+  auto step = [&](int t, const uint8_t* st) __attribute__((always_inline)) {
+    wait_vmcnt<2 * 2 * T::NI>();
+    if (t < n_tiles) compute(t, st);
+    wait_lgkmcnt0();  // the stage's reads are done before it is refilled
+    issue_tile(t + 3, lds_addr(st));
+  };
+  for (int t = 0; t < n_tiles; t += 3) {
+    step(t, lds_s0);
+    step(t + 1, lds_s1);
+    step(t + 2, lds_s2);
   }
+  wait_vmcnt<0>();  // no DMA may land in LDS after the wave has ended
 
   // the new token's own key and value (bf16, from k_new / v_new)
   if (has_new) {
@@ -395,7 +424,7 @@ hipError_t launch_t(const ExtendParams& p, hipStream_t stream) {
 
 int decode_max_chunk_keys(int page_size) { return 64 * page_size; }
 
-int decode_keys_per_tile(int head_dim, bool fp8) { return kTileBytes / (2 * head_dim * (fp8 ? 1 : 2)); }
+int decode_keys_per_tile(int head_dim, bool fp8) { return tile_bytes(fp8) / (2 * head_dim * (fp8 ? 1 : 2)); }
 
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream) {
