@@ -152,7 +152,7 @@ def run_workload(name: str, steps: int, warmup: int):
     lse = torch.empty(q.shape[0], q.shape[1], device=dev, dtype=torch.float32)
     if decode:
         nb = cwlib.decode_workspace_bytes(s.prefix_lens, s.num_kv_heads, s.gqa_group, s.head_dim,
-                                          s.page_size)
+                                          s.page_size, s.kv_dtype)
     else:
         nb = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
                                           s.gqa_group, s.head_dim, s.page_size, s.kv_dtype)

@@ -122,7 +122,7 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
  * and the new token sits at position prefix_lens_h[b]. */
 size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
                                  int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
-                                 int32_t page_size);
+                                 int32_t page_size, cw_kv_dtype_t kv_dtype);
 cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_new,
                                 const void* k_pool, const void* v_pool, const float* k_scale,
                                 const float* v_scale, const int32_t* block_table,

@@ -104,10 +104,11 @@ def extend_workspace_bytes(prefix_lens, suffix_lens, num_kv_heads, gqa_group, he
                                                    _dtype_code(kv_dtype)))
 
 
-def decode_workspace_bytes(prefix_lens, num_kv_heads, gqa_group, head_dim, page_size) -> int:
+def decode_workspace_bytes(prefix_lens, num_kv_heads, gqa_group, head_dim, page_size,
+                           kv_dtype="bf16") -> int:
     lp = _lens(prefix_lens)
     return int(library().cw_decode_workspace_bytes(_ptr(lp), len(lp), num_kv_heads, gqa_group,
-                                                   head_dim, page_size))
+                                                   head_dim, page_size, _dtype_code(kv_dtype)))
 
 
 def set_tuning(key: int, value: int):
@@ -166,7 +167,8 @@ def decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, 
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
-        workspace = _workspace(decode_workspace_bytes(lp, hkv, gqa_group, d, page), q.device, None)
+        workspace = _workspace(decode_workspace_bytes(lp, hkv, gqa_group, d, page,
+                                                      _kv_dtype(k_pool)), q.device, None)
     _check(library().cw_decode_attention(
         _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
         _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), len(lp),

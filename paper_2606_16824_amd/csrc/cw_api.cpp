@@ -208,14 +208,16 @@ ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int
                            cus, xcds, current_tuning());
 }
 
-// Decode plans are built with the larger of the two dtypes' tile lengths so
-// that the workspace size does not depend on the pool dtype.
+// Decode plans follow the pool dtype's tile length and residency (three
+// 16 KB-tile waves per CU for bf16, six 8 KB-tile waves for fp8).
 ExtendPlan make_decode_plan(const int32_t* lp, int32_t num_seqs, int32_t num_kv_heads,
-                            int32_t gqa_group, int32_t head_dim, int32_t page_size) {
+                            int32_t gqa_group, int32_t head_dim, int32_t page_size,
+                            cw_kv_dtype_t kv_dtype) {
   int32_t cus = 256, xcds = 8;
   device_shape(&cus, &xcds);
-  const int32_t kpt = std::max(decode_keys_per_tile(head_dim, true), decode_keys_per_tile(head_dim, false));
-  return build_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kpt, cus,
+  const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  return build_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size,
+                           decode_keys_per_tile(head_dim, fp8), decode_waves_per_cu(fp8), cus,
                            current_tuning());
 }
 
@@ -249,7 +251,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   if (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)) return fail(CW_ERR_ALIGN, "lse not 4-byte aligned");
   if ((reinterpret_cast<uintptr_t>(block_table) & 3u)) return fail(CW_ERR_ALIGN, "block_table not 4-byte aligned");
 
-  ExtendPlan plan = decode ? make_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size)
+  ExtendPlan plan = decode ? make_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype)
                            : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype);
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
@@ -399,15 +401,17 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
 
 size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
                                  int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
-                                 int32_t page_size) {
+                                 int32_t page_size, cw_kv_dtype_t kv_dtype) {
   if (num_seqs < 0) return 0;
+  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
   std::vector<int32_t> ones(num_seqs, 1);
   if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
   if (check_lens(prefix_lens_h, ones.data(), num_seqs, 0, page_size, num_kv_heads, gqa_group,
                  head_dim, false) != CW_OK)
     return 0;
   if (num_seqs == 0) return 256;
-  return make_decode_plan(prefix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, page_size).total_bytes;
+  return make_decode_plan(prefix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype)
+      .total_bytes;
 }
 
 cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_new,

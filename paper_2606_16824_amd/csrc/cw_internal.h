@@ -100,6 +100,7 @@ hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hi
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream);
 int decode_keys_per_tile(int head_dim, bool fp8);
+int decode_waves_per_cu(bool fp8);  // resident decode waves per CU (LDS-bound)
 hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size, bool fp8,
                               hipStream_t stream);
 

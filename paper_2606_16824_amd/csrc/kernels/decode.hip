@@ -426,6 +426,8 @@ int decode_max_chunk_keys(int page_size) { return 64 * page_size; }
 
 int decode_keys_per_tile(int head_dim, bool fp8) { return tile_bytes(fp8) / (2 * head_dim * (fp8 ? 1 : 2)); }
 
+int decode_waves_per_cu(bool fp8) { return (160 * 1024) / (kStages * tile_bytes(fp8)); }  // 160 KB of LDS per CU
+
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream) {
   if (p.n_items <= 0) return hipSuccess;

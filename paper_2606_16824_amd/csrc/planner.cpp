@@ -197,13 +197,15 @@ void layout_workspace(ExtendPlan& plan, int32_t head_dim) {
 
 // Decode planning.  The cached prefix of each (sequence, kv head) is cut into
 // chunks of whole decode tiles and whole pages (at most 64 pages, the kernel
-// keeps one page id per lane); the chunk count is chosen so that about four
-// waves per CU slot exist (a decode wave is bound by its share of HBM
-// bandwidth, so more waves in flight means more bytes in flight).  The new
-// token's own key rides with the last chunk.
+// keeps one page id per lane).  Chunks are as long as one wave per resident
+// slot allows (a decode wave streams its chunk at its share of HBM bandwidth;
+// every wave pays one start-up latency for its page ids and first tile, so
+// fewer, longer waves waste less), within the 64-page cap.  The new token's
+// own key rides with the last chunk.
 ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32_t num_kv_heads,
                              int32_t gqa_group, int32_t head_dim, int32_t page_size,
-                             int32_t keys_per_tile, int32_t num_cus, const Tuning& tuning) {
+                             int32_t keys_per_tile, int32_t waves_per_cu, int32_t num_cus,
+                             const Tuning& tuning) {
   ExtendPlan plan;
   plan.part_rows = gqa_group;
   plan.seqs.resize(num_seqs);
@@ -218,7 +220,7 @@ ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32
   if (tuning.kv_chunk_tiles > 0) {
     chunk = int64_t(tuning.kv_chunk_tiles) * keys_per_tile;
   } else {
-    const int64_t target = tuning.target_wgs > 0 ? tuning.target_wgs : int64_t(num_cus) * 3 * 4;
+    const int64_t target = tuning.target_wgs > 0 ? tuning.target_wgs : int64_t(num_cus) * waves_per_cu;
     const int64_t tiles = std::max<int64_t>(2, (total_tiles + target - 1) / target);
     chunk = tiles * keys_per_tile;
   }

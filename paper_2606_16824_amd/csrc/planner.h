@@ -39,7 +39,8 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
 // chunk) with `gqa_group` rows; `keys_per_tile` is the decode kernel's tile.
 ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32_t num_kv_heads,
                              int32_t gqa_group, int32_t head_dim, int32_t page_size,
-                             int32_t keys_per_tile, int32_t num_cus, const Tuning& tuning);
+                             int32_t keys_per_tile, int32_t waves_per_cu, int32_t num_cus,
+                             const Tuning& tuning);
 
 // Serialises seqs, items and groups into `dst` (meta_bytes long) at their offsets.
 void pack_plan_meta(const ExtendPlan& plan, uint8_t* dst);

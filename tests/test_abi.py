@@ -117,6 +117,11 @@ def test_workspace_query_rejects_bad_args():
     assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 72, 16, 0) == 0
     assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16, 7) == 0
     assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16, 0) > 0
+    assert lib().cw_decode_workspace_bytes(lp.ctypes.data, 1, 1, 1, 64, 16, 7) == 0
+    assert lib().cw_decode_workspace_bytes(lp.ctypes.data, 1, 1, 1, 72, 16, 0) == 0
+    assert lib().cw_decode_workspace_bytes(ls.ctypes.data, 1, 1, 1, 64, 16, 0) == 0
+    for dt in (0, 1):
+        assert lib().cw_decode_workspace_bytes(lp.ctypes.data, 1, 1, 1, 64, 16, dt) > 0
 
 
 def test_tuning_keys():
