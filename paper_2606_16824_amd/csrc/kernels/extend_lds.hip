@@ -192,7 +192,10 @@ void extend_lds_kernel(ExtendParams p) {
     reinterpret_cast<u32x4*>(lds_v1)[i] = u32x4{0u, 0u, 0u, 0u};
   }
 
-  // Q^T as the B operand: k-step kk holds dims 16 kk + 8 h + [0, 8) of this row
+  // Q^T as the B operand: k-step kk holds dims 16 kk + 8 h + [0, 8) of this row.
+  // bf16 pools: Q carries the softmax scale in log2 units (q c rounded to bf16),
+  // so the score MFMAs, started from -m, leave s c - m with no vector work.
+  const float c = p.scale_log2;
   bf16x8 qf[T::KT];
   {
     const uint16_t* qrow =
@@ -202,6 +205,10 @@ void extend_lds_kernel(ExtendParams p) {
       u32x4 v = {0u, 0u, 0u, 0u};
       if (row_ok) v = *reinterpret_cast<const u32x4*>(qrow + 16 * kk + 8 * h);
       qf[kk] = __builtin_bit_cast(bf16x8, v);
+      if constexpr (!FP8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[kk][e] = static_cast<__bf16>(static_cast<float>(qf[kk][e]) * c);
+      }
     }
   }
 
@@ -332,11 +339,11 @@ void extend_lds_kernel(ExtendParams p) {
     }
   }
 
-  const float c = p.scale_log2;
   f32x16 o[T::DB];
 #pragma unroll
   for (int b = 0; b < T::DB; ++b) o[b] = f32x16{};
   float m_run = 0.f, l_run = 0.f;
+  f32x16 negm = f32x16{};  // bf16: -m_run in every element (the score MFMAs' start)
 
   const int n_tiles = (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
   auto tile0 = [&](int j) { return it.kv_begin + j * BLOCK_N; };
@@ -369,16 +376,17 @@ void extend_lds_kernel(ExtendParams p) {
     }
   };
 
-  // raw scores S^T = K Q^T of the tile in `ks`, two 32-key blocks
+  // scores S^T = K Q^T of the tile in `ks`, two 32-key blocks: raw for fp8
+  // pools, s c - m_run for bf16 pools (scaled Q, accumulation started at -m_run)
   auto scores = [&](const uint8_t* ks, f32x16(&s)[2]) __attribute__((always_inline)) {
-    s[0] = f32x16{};
-    s[1] = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < T::KT; ++kk) {
       const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(ks + k_addr[kk]);
       const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(ks + k_addr[kk] + 32 * T::RB);
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[kk], s[0], 0, 0, 0);
-      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[kk], s[1], 0, 0, 0);
+      const f32x16 c0 = kk > 0 ? s[0] : FP8 ? f32x16{} : negm;
+      const f32x16 c1 = kk > 0 ? s[1] : FP8 ? f32x16{} : negm;
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[kk], c0, 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[kk], c1, 0, 0, 0);
     }
   };
   // causal mask (only tiles that cross some row's limit).  Element i of block
@@ -393,15 +401,10 @@ void extend_lds_kernel(ExtendParams p) {
           if (j0 + 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7) >= lim) s[blk][i] = -INFINITY;
     }
   };
-  // log2 units relative to the running max (fp8: times the page's K scale,
-  // plus log2 of its V scale)
+  // fp8: log2 units relative to the running max, times the page's K scale,
+  // plus log2 of its V scale (bf16 scores leave the MFMAs in these units)
   auto to_log2 = [&](int j0, int slot, f32x16(&s)[2]) __attribute__((always_inline)) {
-    if constexpr (!FP8) {
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) s[blk][i] = fmaf(s[blk][i], c, -m_run);
-    } else {
+    if constexpr (FP8) {
       uint32_t cgv[4], lvv[4];
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
@@ -539,7 +542,9 @@ void extend_lds_kernel(ExtendParams p) {
   // against its exact max.  bf16: K_0, V_0, K_1 by DMA, the loop then stages
   // K_{j+2} and V_{j+1} in iteration j.  fp8: the same tiles widened here, and
   // the loop's first iteration finds K_2 and V_1 already in registers.
-  f32x16 x[2] = {f32x16{}, f32x16{}};
+  // scores of tile j in log2 units: xa for even j, xb for odd j (the stage
+  // parity), so tile j+1's scores land in place with no copy
+  f32x16 xa[2] = {f32x16{}, f32x16{}}, xb[2] = {f32x16{}, f32x16{}};
   int pg_v = 0;    // bf16: page of V_{j+1};  fp8: page of V_{j+2} (uniform)
   int pg_raw = 0;  // bf16: page of K_{j+2};  fp8: page of K_{j+3} (scalar load in flight)
   u32x4 k8 = {0u, 0u, 0u, 0u}, v8 = {0u, 0u, 0u, 0u};  // fp8: K_{j+2}, V_{j+1} rows
@@ -579,15 +584,16 @@ void extend_lds_kernel(ExtendParams p) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (visible(0)) {
-      scores(lds_k0, x);
-      mask(tile0(0), x);
-      to_log2(tile0(0), 0, x);  // m_run = 0 here
-      const float mx = row_max(x);
+      scores(lds_k0, xa);
+      mask(tile0(0), xa);
+      to_log2(tile0(0), 0, xa);  // m_run = 0 here
+      const float mx = row_max(xa);
       // a row with no visible key in the first tile sees none in the item
       const float d = mx == -INFINITY ? 0.f : mx;
       m_run = mx == -INFINITY ? kNegBig : mx;
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
+      for (int blk = 0; blk < 2; ++blk) xa[blk] -= d;
+      negm = -m_run;
     }
   }
 
@@ -595,9 +601,8 @@ void extend_lds_kernel(ExtendParams p) {
   // (discarded after the last visible tile: the stage then holds finite stale
   // data) while tile j's weights are formed, then tile j's P V while tile j+1's
   // scores are scaled
-  auto compute = [&](int j, const uint8_t* k_nxt, const uint8_t* v_cur,
-                     bool may_mask) __attribute__((always_inline)) {
-    f32x16 s[2];
+  auto compute = [&](int j, const uint8_t* k_nxt, const uint8_t* v_cur, bool may_mask,
+                     f32x16(&x)[2], f32x16(&s)[2]) __attribute__((always_inline)) {
     bf16x8 pf[4];
     float lsum;
     scores(k_nxt, s);
@@ -614,14 +619,18 @@ void extend_lds_kernel(ExtendParams p) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
       weights(tile0(j), j & 3, x, pf, lsum);
+      if constexpr (!FP8) {
+        // tile j+1's scores were started from the old -m_run
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk) s[blk] -= d;
+        negm = -m_run;
+      }
     }
     l_run += lsum;
     if (may_mask) mask(tile0(j + 1), s);
     accumulate(v_cur, pf);
     to_log2(tile0(j + 1), (j + 1) & 3, s);
     interleave_pv_scale();
-    x[0] = s[0];
-    x[1] = s[1];
   };
 
   // fp8 staging of iteration j (after the barrier): widen K_{j+2} (into K_j's
@@ -646,8 +655,8 @@ void extend_lds_kernel(ExtendParams p) {
 
   // iteration j: K_{j+1} and V_j are resident; K_{j+2} goes to K_j's stage,
   // V_{j+1} to V_{j-1}'s
-  auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
-                       uint8_t* v_nxt) __attribute__((always_inline)) {
+  auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_nxt,
+                       f32x16(&x)[2], f32x16(&xn)[2]) __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);  // this wave's staging of K_{j+1} and V_j has landed
     __syncthreads();                // everyone's has; K_j and V_{j-1} are no longer read
     if constexpr (!FP8) {
@@ -662,7 +671,7 @@ void extend_lds_kernel(ExtendParams p) {
       stage8(j, k_cur, v_nxt, false);
     }
     if (!visible(j)) return;  // nothing visible for this wave from here on
-    compute(j, k_nxt, v_cur, true);
+    compute(j, k_nxt, v_cur, true, x, xn);
   };
 
   // Iterations whose staged tiles lie wholly in the cached prefix (bf16: tiles
@@ -679,8 +688,8 @@ void extend_lds_kernel(ExtendParams p) {
     for (int j = 0; j < T::NI; ++j)
       dma16(rs, (lds_void*)(dst + (wrow0 + T::RPI * j) * T::RB), off[j], 0);
   };
-  auto steady = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur,
-                    uint8_t* v_nxt) __attribute__((always_inline)) {
+  auto steady = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_nxt,
+                    f32x16(&x)[2], f32x16(&xn)[2]) __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if constexpr (!FP8) {
@@ -692,27 +701,27 @@ void extend_lds_kernel(ExtendParams p) {
     } else {
       stage8(j, k_cur, v_nxt, true);
     }
-    if (wave_active) compute(j, k_nxt, v_cur, false);
+    if (wave_active) compute(j, k_nxt, v_cur, false, x, xn);
   };
 
   const int n_prefix = lp > it.kv_begin ? min(n_tiles, (lp - it.kv_begin) / BLOCK_N) : 0;
   const int n_steady = max(0, n_prefix - (FP8 ? 3 : 2));
   int j = 0;
   for (; j + 1 < n_steady; j += 2) {
-    steady(j, lds_k0, lds_k1, lds_v0, lds_v1);
-    steady(j + 1, lds_k1, lds_k0, lds_v1, lds_v0);
+    steady(j, lds_k0, lds_k1, lds_v0, lds_v1, xa, xb);
+    steady(j + 1, lds_k1, lds_k0, lds_v1, lds_v0, xb, xa);
   }
   if (j < n_steady) {
-    steady(j, lds_k0, lds_k1, lds_v0, lds_v1);
+    steady(j, lds_k0, lds_k1, lds_v0, lds_v1, xa, xb);
     ++j;
   }
   if ((j & 1) && j < n_tiles) {
-    iteration(j, lds_k1, lds_k0, lds_v1, lds_v0);
+    iteration(j, lds_k1, lds_k0, lds_v1, lds_v0, xb, xa);
     ++j;
   }
   for (; j < n_tiles; j += 2) {
-    iteration(j, lds_k0, lds_k1, lds_v0, lds_v1);
-    if (j + 1 < n_tiles) iteration(j + 1, lds_k1, lds_k0, lds_v1, lds_v0);
+    iteration(j, lds_k0, lds_k1, lds_v0, lds_v1, xa, xb);
+    if (j + 1 < n_tiles) iteration(j + 1, lds_k1, lds_k0, lds_v1, lds_v0, xb, xa);
   }
 
   if (!wave_active) return;
