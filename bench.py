@@ -52,6 +52,9 @@ def parse():
                     help="steps of the decode measurement added to an extend run (0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables)")
+    ap.add_argument("--separate-calls", action="store_true",
+                    help="time an extend step as cw_kv_write_pages + cw_extend_attention instead of "
+                         "the one-launch cw_write_extend_attention")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (for "
                          "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -133,8 +136,10 @@ def cpu_baseline(w, target_s: float):
             "tok_s": n / dt}
 
 
-def run_workload(name: str, steps: int, warmup: int):
-    """Times `steps` hot-path steps (page write + attention) of a named workload."""
+def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
+    """Times `steps` hot-path steps (page write + attention) of a named workload: one
+    cw_write_extend_attention per extend step (two calls with `separate`), and
+    cw_kv_write_pages + cw_decode_attention per decode step."""
     import torch
     import cw_workloads as cw
     import paper_2606_16824_amd as cwlib
@@ -161,6 +166,11 @@ def run_workload(name: str, steps: int, warmup: int):
     stream = torch.cuda.current_stream()
 
     def step():
+        if not decode and not separate:
+            cwlib.write_extend_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
+                                         s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs,
+                                         out=out, lse=lse, workspace=ws_att)
+            return
         cwlib.kv_write_pages(kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, k_scale=ks,
                              v_scale=vs, workspace=ws_wr)
         if decode:
@@ -212,7 +222,7 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
-    res = run_workload(args.workload, args.steps, args.warmup)
+    res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls)
     s, w = res["spec"], res["workload"]
     ms, kern_ms = res["ms"], res["kern_ms"]
     decode = s.suffix_lens.max() == 1 and args.workload.startswith("decode")
@@ -250,6 +260,9 @@ def main():
         "dtype": "bf16" if s.kv_dtype == "bf16" else "bf16+fp8kv",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_DESC[args.workload], "new_tokens": s.total_new_tokens,
+                   "calls": ("cw_decode_attention" if decode else
+                             "cw_kv_write_pages + cw_extend_attention" if args.separate_calls else
+                             "cw_write_extend_attention"),
                    "tflop_per_step": round(s.flops() / 1e12, 5), "seed": s.seed},
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
         "roofline": roof,

@@ -116,6 +116,25 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
                                 cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream);
 
+/* cw_kv_write_pages and cw_extend_attention of the same arguments in one
+ * launch (the extend kernel's workgroups scatter the new K/V into the pools
+ * under their first tiles' latency).  The attention never reads a pool slot
+ * at or past a sequence's prefix end, so the result is that of the two calls
+ * in either order: `out`/`lse` bit-identical to cw_extend_attention, the pools
+ * byte-identical to cw_kv_write_pages.  k_pool and v_pool are required (they
+ * are written) and get the preconditions of cw_kv_write_pages; the workspace
+ * is that of cw_extend_attention (cw_extend_workspace_bytes).  Errors as for
+ * the two calls; nothing is enqueued on an error. */
+cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const void* v_new,
+                                      void* k_pool, void* v_pool, const float* k_scale,
+                                      const float* v_scale, const int32_t* block_table,
+                                      int32_t bt_stride, int32_t num_pages,
+                                      const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                      int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                                      int32_t head_dim, int32_t page_size, float softmax_scale,
+                                      cw_kv_dtype_t kv_dtype, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Decode: every sequence has exactly one new token (CacheWise Sec. 2:
  * continuous batching of decode steps).  Same as cw_extend_attention with all
  * suffix lengths 1: q/out are [num_seqs, Hq, D], k_new/v_new [num_seqs, Hkv, D],

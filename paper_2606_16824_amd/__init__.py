@@ -26,7 +26,7 @@ import torch
 
 from . import _lib as L
 
-__all__ = ["CWError", "extend_attention", "decode_attention", "kv_write_pages",
+__all__ = ["CWError", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
            "set_tuning", "plan_items", "library"]
 
@@ -153,6 +153,25 @@ def extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, 
         workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
                                q.device, None)
     _check(library().cw_extend_attention(
+        _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
+        _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
+        len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),
+        _dptr(lse), _dptr(workspace), workspace.numel(), _stream()))
+    return out
+
+
+def write_extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
+                           gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None,
+                           lse=None, workspace=None):
+    """kv_write_pages + extend_attention in one launch (the pools are written)."""
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    num_pages, hkv, page, d = k_pool.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
+                               q.device, None)
+    _check(library().cw_write_extend_attention(
         _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
         _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
         len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),

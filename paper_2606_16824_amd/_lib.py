@@ -25,6 +25,9 @@ SIGNATURES = {
     "cw_extend_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                       _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
                                       _vp, _sz, _vp]),
+    "cw_write_extend_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
+                                            _vp, _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int,
+                                            _vp, _vp, _vp, _sz, _vp]),
     "cw_decode_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32]),
     "cw_decode_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
                                       _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,

@@ -221,14 +221,14 @@ ExtendPlan make_decode_plan(const int32_t* lp, int32_t num_seqs, int32_t num_kv_
                            current_tuning());
 }
 
-cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, const void* k_pool,
-                        const void* v_pool, const float* k_scale, const float* v_scale,
+cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                        void* v_pool, const float* k_scale, const float* v_scale,
                         const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
                         const int32_t* lp, const int32_t* ls, int32_t num_seqs,
                         int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
                         int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype, void* out,
                         float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
-                        bool decode) {
+                        bool decode, bool write_pages) {
   cw_status_t s = check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size);
   if (s != CW_OK) return s;
   s = check_dtype(kv_dtype, k_scale, v_scale);
@@ -242,7 +242,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   if (total == 0) return CW_OK;  // no rows: nothing to do
   if (!q || !k_new || !v_new || !out || !block_table)
     return fail(CW_ERR_NULL, "q, k_new, v_new, out and block_table are required");
-  bool any_prefix = false;
+  bool any_prefix = write_pages;  // the fused page write needs the pools too
   for (int32_t b = 0; b < num_seqs; ++b) any_prefix |= lp[b] > 0;
   if (any_prefix && (!k_pool || !v_pool)) return fail(CW_ERR_NULL, "k_pool / v_pool is NULL");
   if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out) ||
@@ -286,6 +286,20 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, con
   p.n_items = static_cast<int32_t>(plan.items.size());
   p.n_groups = static_cast<int32_t>(plan.groups.size());
   p.part_rows = plan.part_rows;
+  if (write_pages) {
+    p.w.k_new = k_new;
+    p.w.v_new = v_new;
+    p.w.k_pool = k_pool;
+    p.w.v_pool = v_pool;
+    p.w.k_scale = k_scale;
+    p.w.v_scale = v_scale;
+    p.w.block_table = block_table;
+    p.w.seqs = p.seqs;
+    p.w.bt_stride = bt_stride;
+    p.w.num_seqs = num_seqs;
+    p.w.num_kv_heads = num_kv_heads;
+    p.w.total_tokens = static_cast<int32_t>(total);
+  }
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   {
     std::lock_guard<std::mutex> g(g_tuning_mu);
@@ -393,10 +407,25 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
                                 int32_t head_dim, int32_t page_size, float softmax_scale,
                                 cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream) {
+  return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
+                     v_scale, block_table, bt_stride, num_pages, prefix_lens_h, suffix_lens_h,
+                     num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
+                     out, lse, workspace, workspace_bytes, stream, false, false);
+}
+
+cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const void* v_new,
+                                      void* k_pool, void* v_pool, const float* k_scale,
+                                      const float* v_scale, const int32_t* block_table,
+                                      int32_t bt_stride, int32_t num_pages,
+                                      const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                      int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                                      int32_t head_dim, int32_t page_size, float softmax_scale,
+                                      cw_kv_dtype_t kv_dtype, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
   return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
                      num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
                      head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
-                     workspace_bytes, stream, false);
+                     workspace_bytes, stream, false, true);
 }
 
 size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
@@ -425,10 +454,10 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
                                 hipStream_t stream) {
   if (num_seqs < 0) return fail(CW_ERR_BAD_LENS, "num_seqs = %d is negative", num_seqs);
   std::vector<int32_t> ones(num_seqs, 1);
-  return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
-                     num_pages, prefix_lens_h, ones.data(), num_seqs, num_kv_heads, gqa_group,
-                     head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
-                     workspace_bytes, stream, true);
+  return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
+                     v_scale, block_table, bt_stride, num_pages, prefix_lens_h, ones.data(),
+                     num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
+                     out, lse, workspace, workspace_bytes, stream, true, false);
 }
 
 cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {

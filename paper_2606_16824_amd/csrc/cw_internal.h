@@ -52,6 +52,21 @@ struct CombineGroup {
   int32_t pad1;
 };
 
+struct WriteParams {
+  const void* k_new;
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* block_table;
+  const SeqInfo* seqs;
+  int32_t bt_stride;
+  int32_t num_seqs;
+  int32_t num_kv_heads;
+  int32_t total_tokens;
+};
+
 struct ExtendParams {
   const void* q;
   const void* k_new;
@@ -76,22 +91,9 @@ struct ExtendParams {
   int32_t n_items;
   int32_t n_groups;
   int32_t part_rows;  // rows per split-K partial slot (the row block for extend, G for decode)
+  WriteParams w;      // extend: also scatter the new K/V into the pools when w.total_tokens > 0
 };
 
-struct WriteParams {
-  const void* k_new;
-  const void* v_new;
-  void* k_pool;
-  void* v_pool;
-  const float* k_scale;
-  const float* v_scale;
-  const int32_t* block_table;
-  const SeqInfo* seqs;
-  int32_t bt_stride;
-  int32_t num_seqs;
-  int32_t num_kv_heads;
-  int32_t total_tokens;
-};
 
 // Kernel launchers (each defined in the translation unit of its kernel).
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,

@@ -53,6 +53,7 @@
 #include <hip/hip_runtime.h>
 
 #include "../cw_internal.h"
+#include "page_write.h"
 
 namespace cw {
 namespace {
@@ -157,8 +158,22 @@ void extend_lds_kernel(ExtendParams p) {
   // softmax scale, [4,8) log2 of the V scale, [8,12) 1 / V scale (fp32 bits)
   __shared__ __attribute__((aligned(16))) uint32_t prm[4][12];
 
+  // Fused page write: this workgroup's share of the new rows' 16-byte pieces
+  // goes to the pools.  The extend never reads a slot at or past a sequence's
+  // prefix end from the pool, so the writes and the attention are independent.
+  auto fused_write = [&]() __attribute__((always_inline)) {
+    const int64_t total = int64_t(p.w.total_tokens) * p.w.num_kv_heads * (D / 8);
+    const int64_t per = (total + gridDim.x - 1) / gridDim.x;
+    const int64_t end = min(total, int64_t(blockIdx.x + 1) * per);
+    for (int64_t idx = int64_t(blockIdx.x) * per + threadIdx.x; idx < end; idx += LDS_THREADS)
+      pw::write_piece<D, P, FP8>(p.w, idx);
+  };
+
   const WorkItem it = p.items[blockIdx.x];
-  if (it.seq < 0) return;  // idle padding item (uniform across the workgroup)
+  if (it.seq < 0) {  // idle padding item (uniform across the workgroup)
+    if (p.w.total_tokens > 0) fused_write();
+    return;
+  }
   const SeqInfo sq = p.seqs[it.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -581,6 +596,7 @@ void extend_lds_kernel(ExtendParams p) {
       pg_v = pg2;
       if (n_tiles > 3) pg_raw = load_page(tile0(3));
     }
+    if (p.w.total_tokens > 0) fused_write();  // under the first tiles' latency
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (visible(0)) {
@@ -595,6 +611,8 @@ void extend_lds_kernel(ExtendParams p) {
       for (int blk = 0; blk < 2; ++blk) xa[blk] -= d;
       negm = -m_run;
     }
+  } else if (p.w.total_tokens > 0) {
+    fused_write();
   }
 
   // the work of iteration j after its staging is issued: tile j+1's scores

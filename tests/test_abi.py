@@ -38,7 +38,7 @@ def test_status_strings():
 FAKE = 0x100000  # a 16-byte-aligned address that is never dereferenced
 
 
-def _extend(**over):
+def _extend(fused=False, **over):
     lp = np.array(over.pop("lp", [10, 20]), dtype=np.int32)
     ls = np.array(over.pop("ls", [5, 6]), dtype=np.int32)
     a = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k_pool=FAKE, v_pool=FAKE, k_scale=None, v_scale=None,
@@ -46,7 +46,8 @@ def _extend(**over):
              head_dim=128, page_size=16, scale=0.088, kv_dtype=0, out=FAKE, lse=None,
              workspace=FAKE, workspace_bytes=1 << 40)
     a.update(over)
-    return lib().cw_extend_attention(
+    fn = lib().cw_write_extend_attention if fused else lib().cw_extend_attention
+    return fn(
         a["q"], a["k_new"], a["v_new"], a["k_pool"], a["v_pool"], a["k_scale"], a["v_scale"],
         a["block_table"], a["bt_stride"], a["num_pages"], lp.ctypes.data, ls.ctypes.data, len(lp),
         a["num_kv_heads"], a["gqa_group"], a["head_dim"], a["page_size"], a["scale"],
@@ -76,9 +77,17 @@ def _extend(**over):
     (dict(workspace_bytes=16), L.CW_ERR_WORKSPACE),
     (dict(workspace=None), L.CW_ERR_WORKSPACE),
 ])
-def test_extend_rejects_before_any_gpu_work(over, status):
-    assert _extend(**over) == status
+@pytest.mark.parametrize("fused", [False, True])
+def test_extend_rejects_before_any_gpu_work(over, status, fused):
+    assert _extend(fused=fused, **over) == status
     assert lib().cw_last_error_message().decode()
+
+
+def test_fused_write_needs_the_pools_even_without_a_prefix():
+    # the plain extend reads no pool when every prefix is empty; the fused call writes it
+    assert _extend(lp=[0, 0], k_pool=None, v_pool=None, workspace_bytes=1) == L.CW_ERR_WORKSPACE
+    assert _extend(fused=True, lp=[0, 0], k_pool=None) == L.CW_ERR_NULL
+    assert _extend(fused=True, lp=[0, 0], v_pool=None) == L.CW_ERR_NULL
 
 
 def test_all_empty_suffixes_is_a_no_op():
