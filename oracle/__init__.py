@@ -23,6 +23,8 @@ causal softmax attention with the readings listed in the design notes:
 Modules
   codecs           bf16 and OCP fp8-e4m3fn decoding/encoding from their definitions
   paged_attention  page gather/scatter, row-wise and blocked attention
+  page_swap        whole-page copies between the page pool and a host block pool
+                   (the offloading configuration of Sec. 6.4)
 """
 from .codecs import bf16_bits_to_f64, e4m3fn_decode, e4m3fn_encode_rne  # noqa: F401
 from .paged_attention import (  # noqa: F401
@@ -34,5 +36,6 @@ from .paged_attention import (  # noqa: F401
     gather_sequence_kv,
     write_pages,
 )
+from .page_swap import swap_in, swap_out  # noqa: F401
 
 PARITY_UNPINNED = ()  # every function above has at least one independent pin
