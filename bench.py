@@ -52,6 +52,8 @@ def parse():
                     help="steps of the decode measurement added to an extend run (0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables)")
+    ap.add_argument("--no-swap", dest="swap", action="store_false",
+                    help="skip the page swap measurement added to an extend run")
     ap.add_argument("--separate-calls", action="store_true",
                     help="time an extend step as cw_kv_write_pages + cw_extend_attention instead of "
                          "the one-launch cw_write_extend_attention")
@@ -207,6 +209,52 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
     return {"spec": s, "workload": w, "ms": ms, "kern_ms": kern_ms, "kernel": kernel}
 
 
+def run_swap(reps: int = 10):
+    """Swap-out of the turn's cached prefix (1024 pages x 8 kv heads, K and V) to a
+    pinned host block pool and swap-in to other pool pages, against a plain
+    contiguous copy of the same bytes in each direction (the host link's ceiling)."""
+    import torch
+    import cw_workloads as cw
+    import paper_2606_16824_amd as cwlib
+
+    spec = cw.spec_for("turn")
+    w = cw.materialize(spec)
+    n = int(spec.prefix_lens[0]) // spec.page_size
+    pages = w.block_table[0, :n].numpy().astype(np.int32)
+    free = np.setdiff1d(np.arange(spec.num_pages), w.block_table[0].numpy())[:n].astype(np.int32)
+    dk, dv = w.k_pool.cuda(), w.v_pool.cuda()
+    hk = torch.empty((n,) + tuple(dk.shape[1:]), dtype=dk.dtype).pin_memory()
+    hv = torch.empty_like(hk).pin_memory()
+    host = np.arange(n, dtype=np.int32)
+    nbytes = 2 * hk.numel() * hk.element_size()
+    ws = torch.empty(cwlib.swap_workspace_bytes(n), dtype=torch.uint8, device="cuda")
+    flat_d = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    flat_h = torch.empty(nbytes, dtype=torch.uint8).pin_memory()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    out_ms = timed(lambda: cwlib.kv_swap_out(dk, dv, hk, hv, pages, host, workspace=ws))
+    in_ms = timed(lambda: cwlib.kv_swap_in(hk, hv, dk, dv, host, free, workspace=ws))
+    d2h_ms = timed(lambda: flat_h.copy_(flat_d, non_blocking=True))
+    h2d_ms = timed(lambda: flat_d.copy_(flat_h, non_blocking=True))
+    gbs = lambda ms: round(nbytes / (ms * 1e-3) / 1e9, 1)
+    return {"workload": f"turn prefix: {n} pages x {spec.num_kv_heads} kv heads, K and V "
+                        f"({nbytes / 2**20:.0f} MiB) to a pinned host block pool and back",
+            "bound": "host link", "out_GB_s": gbs(out_ms), "in_GB_s": gbs(in_ms),
+            "copy_d2h_GB_s": gbs(d2h_ms), "copy_h2d_GB_s": gbs(h2d_ms),
+            "frac_out": round(d2h_ms / out_ms, 4), "frac_in": round(h2d_ms / in_ms, 4),
+            "kernel": "swap_kernel"}
+
+
 def main():
     args = parse()
     if args.calibrate_copy_mib:
@@ -280,6 +328,9 @@ def main():
             "kernel": d["kernel"]}
         print(f"[bench] decode step {d['ms']:.4f} ms, kernel {d['kern_ms']:.4f} ms", file=sys.stderr,
               flush=True)
+    if not decode and args.swap:
+        result["swap"] = run_swap()
+        print(f"[bench] swap {result['swap']}", file=sys.stderr, flush=True)
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

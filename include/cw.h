@@ -135,6 +135,40 @@ cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const vo
                                       cw_kv_dtype_t kv_dtype, void* out, float* lse,
                                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Page swaps between the device page pool and a host block pool (CacheWise
+ * Sec. 6.4: in the offloading configuration, evicted KV blocks move to CPU DRAM
+ * and are swapped back when their session resumes).  The host pools have the
+ * device pools' layout with their own block count: k_host, v_host
+ * [num_host_blocks, Hkv, P, D] of the pool dtype and, for fp8 pools,
+ * k_scale_host, v_scale_host fp32 [num_host_blocks, Hkv]; they must be
+ * device-accessible host memory (hipHostMalloc / pinned) or device memory, and
+ * 16-byte aligned.  Entry i of cw_kv_swap_out copies pool page pages_h[i]
+ * (every kv head, K and V, and for fp8 its scales) to host block
+ * host_blocks_h[i]; cw_kv_swap_in copies host block host_blocks_h[i] to pool
+ * page pages_h[i].  Bytes are copied unchanged.  The two lists are *host*
+ * int32 arrays of n entries, read during the call; ids must be in range and
+ * destinations distinct (sources may repeat), else CW_ERR_BAD_LENS before
+ * anything is enqueued; a pool pointer that is neither device memory nor
+ * device-mapped host memory gives CW_ERR_UNSUPPORTED.  The copy runs on `stream`; the host side is read or
+ * written by the kernel over the host link, so the host buffers must stay
+ * valid and untouched until the stream passes the call.  Workspace:
+ * cw_swap_workspace_bytes(n) bytes of device memory (the lists). */
+size_t cw_swap_workspace_bytes(int32_t n);
+cw_status_t cw_kv_swap_out(const void* k_pool, const void* v_pool, const float* k_scale,
+                           const float* v_scale, int32_t num_pages, void* k_host, void* v_host,
+                           float* k_scale_host, float* v_scale_host, int32_t num_host_blocks,
+                           const int32_t* pages_h, const int32_t* host_blocks_h, int32_t n,
+                           int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                           cw_kv_dtype_t kv_dtype, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+cw_status_t cw_kv_swap_in(const void* k_host, const void* v_host, const float* k_scale_host,
+                          const float* v_scale_host, int32_t num_host_blocks, void* k_pool,
+                          void* v_pool, float* k_scale, float* v_scale, int32_t num_pages,
+                          const int32_t* host_blocks_h, const int32_t* pages_h, int32_t n,
+                          int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                          cw_kv_dtype_t kv_dtype, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
 /* Decode: every sequence has exactly one new token (CacheWise Sec. 2:
  * continuous batching of decode steps).  Same as cw_extend_attention with all
  * suffix lengths 1: q/out are [num_seqs, Hq, D], k_new/v_new [num_seqs, Hkv, D],

@@ -28,7 +28,7 @@ from . import _lib as L
 
 __all__ = ["CWError", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
-           "set_tuning", "plan_items", "library"]
+           "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes"]
 
 
 class CWError(RuntimeError):
@@ -177,6 +177,52 @@ def write_extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_
         len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),
         _dptr(lse), _dptr(workspace), workspace.numel(), _stream()))
     return out
+
+
+def swap_workspace_bytes(n: int) -> int:
+    return int(library().cw_swap_workspace_bytes(n))
+
+
+def _hptr(t: Optional[torch.Tensor]):
+    """Pointer to a host-pool tensor: device memory or pinned (device-mapped) host memory."""
+    if t is None:
+        return None
+    if not (t.is_cuda or t.is_pinned()):
+        raise ValueError("host pools must be pinned host tensors (pin_memory=True) or on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _swap_dims(k_pool, k_host):
+    num_pages, hkv, page, d = k_pool.shape
+    if tuple(k_host.shape[1:]) != (hkv, page, d):
+        raise ValueError(f"host pool blocks {tuple(k_host.shape[1:])} differ from pool blocks {(hkv, page, d)}")
+    return num_pages, k_host.shape[0], hkv, page, d
+
+
+def kv_swap_out(k_pool, v_pool, k_host, v_host, pages, host_blocks, k_scale=None, v_scale=None,
+                k_scale_host=None, v_scale_host=None, workspace=None):
+    """Pool page pages[i] -> host block host_blocks[i] (K, V and fp8 scales)."""
+    pg, hb = _lens(pages), _lens(host_blocks)
+    num_pages, n_host, hkv, page, d = _swap_dims(k_pool, k_host)
+    ws = _workspace(swap_workspace_bytes(len(pg)), k_pool.device, workspace)
+    _check(library().cw_kv_swap_out(
+        _dptr(k_pool), _dptr(v_pool), _dptr(k_scale), _dptr(v_scale), num_pages, _hptr(k_host),
+        _hptr(v_host), _hptr(k_scale_host), _hptr(v_scale_host), n_host, _ptr(pg), _ptr(hb), len(pg),
+        hkv, d, page, _kv_dtype(k_pool), _dptr(ws), ws.numel(), _stream()))
+
+
+def kv_swap_in(k_host, v_host, k_pool, v_pool, host_blocks, pages, k_scale_host=None,
+               v_scale_host=None, k_scale=None, v_scale=None, workspace=None):
+    """Host block host_blocks[i] -> pool page pages[i] (K, V and fp8 scales)."""
+    pg, hb = _lens(pages), _lens(host_blocks)
+    num_pages, n_host, hkv, page, d = _swap_dims(k_pool, k_host)
+    ws = _workspace(swap_workspace_bytes(len(pg)), k_pool.device, workspace)
+    _check(library().cw_kv_swap_in(
+        _hptr(k_host), _hptr(v_host), _hptr(k_scale_host), _hptr(v_scale_host), n_host,
+        _dptr(k_pool), _dptr(v_pool), _dptr(k_scale), _dptr(v_scale), num_pages, _ptr(hb), _ptr(pg),
+        len(pg), hkv, d, page, _kv_dtype(k_pool), _dptr(ws), ws.numel(), _stream()))
 
 
 def decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, gqa_group,

@@ -322,12 +322,117 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   return CW_OK;
 }
 
+// Shared by both swap directions: validates and enqueues block src_ids[i] of
+// the source pools -> block dst_ids[i] of the destination pools.
+cw_status_t swap_impl(const void* src_k, const void* src_v, const float* src_ks,
+                      const float* src_vs, int32_t n_src_blocks, void* dst_k, void* dst_v,
+                      float* dst_ks, float* dst_vs, int32_t n_dst_blocks, const int32_t* src_ids,
+                      const int32_t* dst_ids, int32_t n, int32_t num_kv_heads, int32_t head_dim,
+                      int32_t page_size, cw_kv_dtype_t kv_dtype, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream) {
+  cw_status_t s = check_shape(0, num_kv_heads, 1, head_dim, page_size);
+  if (s != CW_OK) return s;
+  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN)
+    return fail(CW_ERR_UNSUPPORTED, "kv_dtype = %d", int(kv_dtype));
+  const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  if (n < 0 || n_src_blocks < 0 || n_dst_blocks < 0)
+    return fail(CW_ERR_BAD_LENS, "negative count (n = %d, pools of %d and %d blocks)", n, n_src_blocks,
+                n_dst_blocks);
+  if (n == 0) return CW_OK;
+  if (!src_ids || !dst_ids) return fail(CW_ERR_NULL, "the block lists are required");
+  if (!src_k || !src_v || !dst_k || !dst_v) return fail(CW_ERR_NULL, "K and V pools of both sides are required");
+  if (fp8 && (!src_ks || !src_vs || !dst_ks || !dst_vs))
+    return fail(CW_ERR_NULL, "fp8 pools need the scales of both sides");
+  if (!aligned16(src_k) || !aligned16(src_v) || !aligned16(dst_k) || !aligned16(dst_v) || !aligned16(workspace))
+    return fail(CW_ERR_ALIGN, "pool and workspace pointers must be 16-byte aligned");
+  std::vector<uint8_t> seen(size_t(n_dst_blocks), 0);
+  for (int32_t i = 0; i < n; ++i) {
+    if (src_ids[i] < 0 || src_ids[i] >= n_src_blocks || dst_ids[i] < 0 || dst_ids[i] >= n_dst_blocks)
+      return fail(CW_ERR_BAD_LENS, "entry %d: block %d -> %d out of range (%d, %d blocks)", i, src_ids[i],
+                  dst_ids[i], n_src_blocks, n_dst_blocks);
+    if (seen[dst_ids[i]]++)
+      return fail(CW_ERR_BAD_LENS, "entry %d: destination block %d appears twice", i, dst_ids[i]);
+  }
+  const size_t need = cw_swap_workspace_bytes(n);
+  if (workspace == nullptr || workspace_bytes < need)
+    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  // the kernel dereferences both sides: each pool pointer must be device memory
+  // or host memory mapped into the device at the same address (pinned)
+  const void* sides[] = {src_k, src_v, dst_k, dst_v, src_ks, src_vs, dst_ks, dst_vs};
+  for (const void* ptr : sides) {
+    if (ptr == nullptr) continue;
+    hipPointerAttribute_t attr{};
+    const hipError_t pe = hipPointerGetAttributes(&attr, ptr);
+    const bool ok = pe == hipSuccess &&
+                    (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged ||
+                     attr.type == hipMemoryTypeUnified ||
+                     (attr.type == hipMemoryTypeHost && attr.devicePointer == ptr));
+    if (!ok) {
+      (void)hipGetLastError();  // the query's error is ours, not a later call's
+      return fail(CW_ERR_UNSUPPORTED, "pool pointer %p is not device-accessible (pageable host memory?)", ptr);
+    }
+  }
+  std::vector<int32_t> lists(size_t(2) * n);
+  std::copy(src_ids, src_ids + n, lists.begin());
+  std::copy(dst_ids, dst_ids + n, lists.begin() + n);
+  s = upload(lists.data(), lists.size() * sizeof(int32_t), workspace, stream);
+  if (s != CW_OK) return s;
+  SwapParams p{};
+  p.src_k = static_cast<const uint8_t*>(src_k);
+  p.src_v = static_cast<const uint8_t*>(src_v);
+  p.dst_k = static_cast<uint8_t*>(dst_k);
+  p.dst_v = static_cast<uint8_t*>(dst_v);
+  if (fp8) {
+    p.src_ks = src_ks;
+    p.src_vs = src_vs;
+    p.dst_ks = dst_ks;
+    p.dst_vs = dst_vs;
+  }
+  p.src_ids = static_cast<const int32_t*>(workspace);
+  p.dst_ids = static_cast<const int32_t*>(workspace) + n;
+  p.n = n;
+  p.block_bytes = num_kv_heads * page_size * head_dim * (fp8 ? 1 : 2);
+  p.scales_per_block = num_kv_heads;
+  const hipError_t e = launch_swap(p, stream);
+  if (e != hipSuccess) return hip_fail(e, "swap kernel launch");
+  return CW_OK;
+}
+
 }  // namespace
 }  // namespace cw
 
 using namespace cw;
 
 extern "C" {
+
+size_t cw_swap_workspace_bytes(int32_t n) {
+  if (n < 0) return 0;
+  return std::max<size_t>(256, (size_t(n) * 2 * sizeof(int32_t) + 255) & ~size_t(255));
+}
+
+cw_status_t cw_kv_swap_out(const void* k_pool, const void* v_pool, const float* k_scale,
+                           const float* v_scale, int32_t num_pages, void* k_host, void* v_host,
+                           float* k_scale_host, float* v_scale_host, int32_t num_host_blocks,
+                           const int32_t* pages_h, const int32_t* host_blocks_h, int32_t n,
+                           int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                           cw_kv_dtype_t kv_dtype, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+  return swap_impl(k_pool, v_pool, k_scale, v_scale, num_pages, k_host, v_host, k_scale_host,
+                   v_scale_host, num_host_blocks, pages_h, host_blocks_h, n, num_kv_heads, head_dim,
+                   page_size, kv_dtype, workspace, workspace_bytes, stream);
+}
+
+cw_status_t cw_kv_swap_in(const void* k_host, const void* v_host, const float* k_scale_host,
+                          const float* v_scale_host, int32_t num_host_blocks, void* k_pool,
+                          void* v_pool, float* k_scale, float* v_scale, int32_t num_pages,
+                          const int32_t* host_blocks_h, const int32_t* pages_h, int32_t n,
+                          int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                          cw_kv_dtype_t kv_dtype, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  return swap_impl(k_host, v_host, k_scale_host, v_scale_host, num_host_blocks, k_pool, v_pool,
+                   k_scale, v_scale, num_pages, host_blocks_h, pages_h, n, num_kv_heads, head_dim,
+                   page_size, kv_dtype, workspace, workspace_bytes, stream);
+}
 
 size_t cw_write_pages_workspace_bytes(int32_t num_seqs) {
   if (num_seqs < 0) return 0;

@@ -95,6 +95,25 @@ struct ExtendParams {
 };
 
 
+// Whole-block copies between two block pools (device page pool <-> host block
+// pool): block src_ids[i] of (src_k, src_v) goes to block dst_ids[i] of
+// (dst_k, dst_v); scales (fp8 pools) likewise, `scales_per_block` floats each.
+struct SwapParams {
+  const uint8_t* src_k;
+  const uint8_t* src_v;
+  uint8_t* dst_k;
+  uint8_t* dst_v;
+  const float* src_ks;  // nullptr: no scales to copy
+  const float* src_vs;
+  float* dst_ks;
+  float* dst_vs;
+  const int32_t* src_ids;  // [n], device-visible
+  const int32_t* dst_ids;  // [n]
+  int32_t n;
+  int32_t block_bytes;  // Hkv * P * D * element bytes, a multiple of 16
+  int32_t scales_per_block;  // Hkv
+};
+
 // Kernel launchers (each defined in the translation unit of its kernel).
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                              hipStream_t stream);
@@ -105,5 +124,6 @@ int decode_keys_per_tile(int head_dim, bool fp8);
 int decode_waves_per_cu(bool fp8);  // resident decode waves per CU (LDS-bound)
 hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size, bool fp8,
                               hipStream_t stream);
+hipError_t launch_swap(const SwapParams& p, hipStream_t stream);
 
 }  // namespace cw

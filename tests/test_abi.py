@@ -138,3 +138,58 @@ def test_tuning_keys():
     assert lib().cw_set_tuning(9, 1) == L.CW_ERR_UNSUPPORTED
     assert lib().cw_set_tuning(0, 0) == L.CW_OK
     assert lib().cw_set_tuning(1, 0) == L.CW_OK
+
+
+def _swap(out=True, **over):
+    pages = np.array(over.pop("pages", [3, 7, 1]), dtype=np.int32)
+    host = np.array(over.pop("host", [0, 2, 1]), dtype=np.int32)
+    a = dict(pool_k=FAKE, pool_v=FAKE, ks=None, vs=None, num_pages=10, host_k=FAKE, host_v=FAKE,
+             hks=None, hvs=None, num_host=4, n=len(pages), num_kv_heads=2, head_dim=128,
+             page_size=16, kv_dtype=0, workspace=FAKE, workspace_bytes=1 << 20)
+    a.update(over)
+    if out:
+        return lib().cw_kv_swap_out(a["pool_k"], a["pool_v"], a["ks"], a["vs"], a["num_pages"],
+                                    a["host_k"], a["host_v"], a["hks"], a["hvs"], a["num_host"],
+                                    pages.ctypes.data, host.ctypes.data, a["n"], a["num_kv_heads"],
+                                    a["head_dim"], a["page_size"], a["kv_dtype"], a["workspace"],
+                                    a["workspace_bytes"], None)
+    return lib().cw_kv_swap_in(a["host_k"], a["host_v"], a["hks"], a["hvs"], a["num_host"],
+                               a["pool_k"], a["pool_v"], a["ks"], a["vs"], a["num_pages"],
+                               host.ctypes.data, pages.ctypes.data, a["n"], a["num_kv_heads"],
+                               a["head_dim"], a["page_size"], a["kv_dtype"], a["workspace"],
+                               a["workspace_bytes"], None)
+
+
+@pytest.mark.parametrize("over,status", [
+    (dict(pool_k=None), L.CW_ERR_NULL),
+    (dict(host_v=None), L.CW_ERR_NULL),
+    (dict(kv_dtype=1), L.CW_ERR_NULL),  # fp8 without scales
+    (dict(kv_dtype=5), L.CW_ERR_UNSUPPORTED),
+    (dict(head_dim=96), L.CW_ERR_UNSUPPORTED),
+    (dict(page_size=8), L.CW_ERR_UNSUPPORTED),
+    (dict(pages=[3, 10, 1]), L.CW_ERR_BAD_LENS),   # page id past the pool
+    (dict(host=[0, 4, 1]), L.CW_ERR_BAD_LENS),     # host block past the host pool
+    (dict(pages=[-1, 7, 1]), L.CW_ERR_BAD_LENS),
+    (dict(n=-1), L.CW_ERR_BAD_LENS),
+    (dict(host_k=FAKE + 4), L.CW_ERR_ALIGN),
+    (dict(workspace_bytes=8), L.CW_ERR_WORKSPACE),
+    (dict(workspace=None), L.CW_ERR_WORKSPACE),
+])
+@pytest.mark.parametrize("out", [True, False])
+def test_swap_rejects_before_any_gpu_work(over, status, out):
+    assert _swap(out, **over) == status
+    assert lib().cw_last_error_message().decode()
+
+
+def test_swap_destinations_must_be_distinct():
+    # swap-out writes host blocks, swap-in writes pool pages
+    assert _swap(True, host=[0, 2, 0]) == L.CW_ERR_BAD_LENS
+    assert _swap(False, pages=[3, 3, 1]) == L.CW_ERR_BAD_LENS
+    # repeated sources are allowed; these calls fail only at the workspace check
+    assert _swap(True, pages=[3, 3, 1], workspace_bytes=8) == L.CW_ERR_WORKSPACE
+    assert _swap(False, host=[0, 0, 1], workspace_bytes=8) == L.CW_ERR_WORKSPACE
+
+
+def test_empty_swap_is_a_no_op():
+    assert _swap(True, pages=[], host=[], pool_k=None, workspace=None) == L.CW_OK
+    assert lib().cw_swap_workspace_bytes(0) >= 256 and lib().cw_swap_workspace_bytes(-1) == 0
