@@ -25,6 +25,8 @@ Modules
   paged_attention  page gather/scatter, row-wise and blocked attention
   page_swap        whole-page copies between the page pool and a host block pool
                    (the offloading configuration of Sec. 6.4)
+  cachewise_policy the KV-block policy (prefix-aware dispatch, predictive / LRU /
+                   Belady eviction) simulated plainly over agent sessions
 """
 from .codecs import bf16_bits_to_f64, e4m3fn_decode, e4m3fn_encode_rne  # noqa: F401
 from .paged_attention import (  # noqa: F401
@@ -37,5 +39,6 @@ from .paged_attention import (  # noqa: F401
     write_pages,
 )
 from .page_swap import swap_in, swap_out  # noqa: F401
+from . import cachewise_policy  # noqa: F401
 
 PARITY_UNPINNED = ()  # every function above has at least one independent pin

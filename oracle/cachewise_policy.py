@@ -1,0 +1,182 @@
+"""CacheWise KV-block policy, simulated plainly -- oracle (test infrastructure).
+
+Written from the paper's model and design: Sec. 4 (a node holds M KV blocks;
+session S_i's context needs d_i blocks, k_i of which are resident, so a new
+request allocates a_i = d_i - k_i blocks, evicting other sessions' blocks
+when the working set would exceed M; the ideal victim is the session whose
+next reuse time tau is largest), Sec. 5.1 (dispatch the queued request with
+the fewest a_i), Sec. 5.2 (evict in decreasing order of the predicted
+E[tau | tau > elapsed], estimated from historical tool durations), Sec. 5.3
+(one priority per session, set when its blocks become unreferenced and
+recomputed for all unreferenced sessions every N_rebuild engine iterations).
+The baselines are FCFS dispatch and LRU eviction; Belady's rule uses the true
+tau.  The readings the paper leaves open (one request at a time, eviction
+from the tail of a context, service time linear in prefilled and generated
+tokens, the predictor's fallback) are the ones the library states.
+
+Plain Python with one pass over sessions per decision, no data structures
+beyond lists: slow and easy to check.
+"""
+import math
+from dataclasses import dataclass, field
+from typing import List, Sequence
+
+INF = math.inf
+
+
+@dataclass
+class Turn:
+    in_tokens: int
+    out_tokens: int
+    tool: int = 0          # type of the tool call after this turn
+    tool_s: float = 0.0    # its true duration
+
+
+@dataclass
+class SessionSpec:
+    start: float
+    turns: List[Turn]
+
+
+@dataclass
+class Config:
+    M: int                     # capacity in blocks
+    block_tokens: int
+    prefill_s_per_token: float = 0.0
+    decode_s_per_token: float = 0.0
+    sched: str = "prefix"      # "fcfs" | "prefix"
+    evict: str = "predictive"  # "lru" | "predictive" | "belady"
+    n_rebuild: int = 3
+
+
+@dataclass
+class Result:
+    makespan_s: float = 0.0
+    mean_session_s: float = 0.0
+    goodput_tok_s: float = 0.0
+    requests: int = 0
+    faults: int = 0
+    evicted_blocks: int = 0
+    recomputed_tokens: int = 0
+    prefilled_tokens: int = 0
+    heap_rebuilds: int = 0
+    dispatch: List[int] = field(default_factory=list)
+
+
+def predict_remaining(history: Sequence[float], elapsed: float) -> float:
+    """E[tau - elapsed | tau > elapsed] from samples; `elapsed` if no sample exceeds it."""
+    rest = [x - elapsed for x in history if x > elapsed]
+    return sum(rest) / len(rest) if rest else elapsed
+
+
+def _blocks(tokens: int, block_tokens: int) -> int:
+    return -(-tokens // block_tokens)
+
+
+def simulate(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Sequence[float]]) -> Result:
+    B = cfg.block_tokens
+    n = len(sessions)
+    nxt = [0] * n                 # next turn of each session
+    ctx = [0] * n                 # context tokens
+    k = [0] * n                   # resident leading blocks (k_i)
+    state = ["wait"] * n          # wait | queued | running | done
+    arrival = [s.start for s in sessions]
+    last_use = [0.0] * n
+    tool_start = [0.0] * n
+    tool = [0] * n
+    prio = [0.0] * n
+    done_at = [0.0] * n
+    for i, s in enumerate(sessions):
+        if not s.turns:
+            state[i], done_at[i], prio[i] = "done", s.start, INF
+    r = Result()
+    t = 0.0
+    running, run_end = -1, 0.0
+
+    def need(i):  # d_i of session i's pending turn
+        tr = sessions[i].turns[nxt[i]]
+        return _blocks(ctx[i] + tr.in_tokens + tr.out_tokens, B)
+
+    def tau_true(j):
+        if state[j] == "done":
+            return INF
+        if state[j] == "queued":
+            return 0.0
+        return max(0.0, arrival[j] - t)
+
+    while True:
+        for i in range(n):
+            if state[i] == "wait" and arrival[i] <= t:
+                state[i] = "queued"
+        if running < 0:
+            queued = [i for i in range(n) if state[i] == "queued"]
+            if queued:
+                if cfg.sched == "prefix":   # fewest new blocks a_i, then earliest arrival
+                    i = min(queued, key=lambda q: (need(q) - k[q], arrival[q], q))
+                else:                       # first come, first served
+                    i = min(queued, key=lambda q: (arrival[q], q))
+                # engine iteration: the eviction heap is rebuilt every N_rebuild of them
+                r.requests += 1
+                if cfg.evict == "predictive" and r.requests % cfg.n_rebuild == 0:
+                    for j in range(n):
+                        if state[j] == "done":
+                            prio[j] = INF
+                        elif state[j] == "queued":
+                            prio[j] = 0.0
+                        elif state[j] == "wait":
+                            prio[j] = predict_remaining(history[tool[j]], t - tool_start[j])
+                    r.heap_rebuilds += 1
+                tr = sessions[i].turns[nxt[i]]
+                d = need(i)
+                a = d - k[i]
+                if k[i] < _blocks(ctx[i], B):
+                    r.faults += 1
+                free = cfg.M - sum(k)
+                while free < a:
+                    cands = [j for j in range(n) if j != i and k[j] > 0]
+                    if cfg.evict == "lru":
+                        v = min(cands, key=lambda j: (last_use[j], j))
+                    elif cfg.evict == "predictive":
+                        v = min(cands, key=lambda j: (-prio[j], j))
+                    else:
+                        v = min(cands, key=lambda j: (-tau_true(j), j))
+                    take = min(k[v], a - free)   # from the tail of its context
+                    k[v] -= take
+                    free += take
+                    r.evicted_blocks += take
+                recompute = max(0, ctx[i] - k[i] * B)
+                r.recomputed_tokens += recompute
+                r.prefilled_tokens += recompute + tr.in_tokens
+                k[i] = d
+                state[i] = "running"
+                running = i
+                run_end = t + (cfg.prefill_s_per_token * (recompute + tr.in_tokens)
+                               + cfg.decode_s_per_token * tr.out_tokens)
+                r.dispatch.append(i)
+                continue
+        nexts = [arrival[i] for i in range(n) if state[i] == "wait"]
+        if running >= 0:
+            nexts.append(run_end)
+        if not nexts:
+            break
+        t = max(t, min(nexts))
+        if running >= 0 and run_end <= t:
+            i = running
+            tr = sessions[i].turns[nxt[i]]
+            ctx[i] += tr.in_tokens + tr.out_tokens
+            last_use[i] = t
+            nxt[i] += 1
+            if nxt[i] == len(sessions[i].turns):
+                state[i], done_at[i], prio[i] = "done", t, INF
+            else:
+                state[i] = "wait"
+                tool[i], tool_start[i] = tr.tool, t
+                arrival[i] = t + tr.tool_s
+                prio[i] = predict_remaining(history[tr.tool], 0.0)
+            running = -1
+    r.makespan_s = max(done_at) if n else 0.0
+    spans = [done_at[i] - sessions[i].start for i in range(n) if sessions[i].turns]
+    r.mean_session_s = sum(spans) / len(spans) if spans else 0.0
+    total = sum(tr.in_tokens + tr.out_tokens for s in sessions for tr in s.turns)
+    r.goodput_tok_s = total / r.makespan_s if r.makespan_s > 0 else 0.0
+    return r

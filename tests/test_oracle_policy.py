@@ -1,0 +1,152 @@
+"""Pins of the CacheWise policy oracle (CPU): the predictor's closed forms,
+Belady's rule against an exhaustive search and LRU against a textbook cache on
+classic paging traces, a hand-worked prefix-aware dispatch, and the equality of
+predictive eviction with a perfect predictor and Belady's rule."""
+import itertools
+import random
+from collections import OrderedDict
+
+import numpy as np
+import pytest
+
+from oracle import cachewise_policy as cp
+
+
+def test_predictor_closed_forms():
+    h = [1.0, 2.0, 3.0, 4.0]
+    assert cp.predict_remaining(h, 0.0) == 2.5
+    assert cp.predict_remaining(h, 2.5) == pytest.approx(1.0)   # (0.5 + 1.5) / 2
+    assert cp.predict_remaining(h, 5.0) == 5.0                  # no sample left: elapsed
+    # memoryless exponential: the expected remaining time does not depend on elapsed
+    x = np.random.default_rng(0).exponential(10.0, size=200_000).tolist()
+    for e in (0.0, 5.0, 20.0):
+        assert cp.predict_remaining(x, e) == pytest.approx(10.0, rel=0.03)
+    # uniform on [0, 10]: E[remaining | elapsed e] = (10 - e) / 2
+    u = np.linspace(0.0, 10.0, 100_001).tolist()
+    for e in (0.0, 4.0, 9.0):
+        assert cp.predict_remaining(u, e) == pytest.approx((10.0 - e) / 2, rel=1e-3)
+
+
+def _paging_sessions(seq):
+    """Classic paging as sessions of one block each: access number n of page p
+    arrives at time n + 1 and is served in zero time."""
+    times = {}
+    for n, p in enumerate(seq):
+        times.setdefault(p, []).append(float(n + 1))
+    sessions = []
+    for p in sorted(times):
+        ts = times[p]
+        turns = [cp.Turn(1, 0, 0, ts[m + 1] - ts[m] if m + 1 < len(ts) else 0.0) for m in range(len(ts))]
+        sessions.append(cp.SessionSpec(ts[0], turns))
+    return sessions, sorted(times)
+
+
+def _min_misses(seq, cap):
+    best = [None]
+
+    def go(i, cache, misses):
+        if best[0] is not None and misses >= best[0]:
+            return
+        if i == len(seq):
+            best[0] = misses
+            return
+        p = seq[i]
+        if p in cache:
+            go(i + 1, cache, misses)
+        elif len(cache) < cap:
+            go(i + 1, cache | {p}, misses + 1)
+        else:
+            for v in cache:
+                go(i + 1, (cache - {v}) | {p}, misses + 1)
+    go(0, frozenset(), 0)
+    return best[0]
+
+
+def _lru_misses(seq, cap):
+    c, m = OrderedDict(), 0
+    for p in seq:
+        if p in c:
+            c.move_to_end(p)
+        else:
+            m += 1
+            if len(c) == cap:
+                c.popitem(last=False)
+            c[p] = True
+    return m
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_belady_is_optimal_and_lru_is_lru_on_paging_traces(seed):
+    rng = random.Random(seed)
+    pages = rng.randint(3, 4)
+    cap = rng.randint(2, pages - 1)
+    seq = [rng.randrange(pages) for _ in range(rng.randint(4, 11))]
+    sessions, ids = _paging_sessions(seq)
+    hist = [[1.0]]
+    compulsory = len(ids)
+    for evict, want in (("belady", _min_misses(seq, cap)), ("lru", _lru_misses(seq, cap))):
+        r = cp.simulate(cp.Config(M=cap, block_tokens=1000, sched="fcfs", evict=evict), sessions, hist)
+        assert r.faults + compulsory == want, (seq, cap, evict)
+        # dispatch order is the access order
+        assert [ids[i] for i in r.dispatch] == seq
+
+
+def test_prefix_aware_dispatch_hand_worked():
+    # session 3 occupies the engine from 9.9 to 11.9; sessions 0, 1, 2 queue meanwhile
+    # with a_i = 4, 1, 3 new blocks (block = 1 token): prefix-aware serves 1, 2, 0,
+    # FCFS serves them in arrival order 0, 2, 1
+    S = cp.SessionSpec
+    T = cp.Turn
+    sessions = [
+        S(0.0, [T(5, 0, 0, 10.0), T(4, 0)]),    # resident 5 after turn 1, then needs 4 more (at t=10.0)
+        S(0.1, [T(2, 0, 0, 10.1), T(1, 0)]),    # resident 2, needs 1 more (at t=10.2)
+        S(10.1, [T(3, 0)]),                     # first turn: 3 blocks
+        S(9.9, [T(2000, 0)]),                   # long: 2000 tokens at 1 ms each
+    ]
+    hist = [[1.0]]
+    base = dict(M=10_000, block_tokens=1, prefill_s_per_token=1e-3)
+    r = cp.simulate(cp.Config(sched="prefix", evict="lru", **base), sessions, hist)
+    assert r.dispatch == [0, 1, 3, 1, 2, 0]
+    r = cp.simulate(cp.Config(sched="fcfs", evict="lru", **base), sessions, hist)
+    assert r.dispatch == [0, 1, 3, 0, 2, 1]
+
+
+def _random_sessions(rng, n_sessions, n_tools, fixed_tool_s=None):
+    sessions = []
+    for s in range(n_sessions):
+        turns = []
+        for _ in range(rng.randint(1, 6)):
+            y = rng.randrange(n_tools)
+            dur = fixed_tool_s[y] if fixed_tool_s else rng.uniform(0.0, 30.0)
+            turns.append(cp.Turn(rng.randint(1, 400), rng.randint(0, 60), y, dur))
+        sessions.append(cp.SessionSpec(rng.uniform(0.0, 20.0), turns))
+    return sessions
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_predictive_with_a_perfect_predictor_is_belady(seed):
+    # every call of tool type y takes exactly x_y and the history is [x_y]: the
+    # predictor returns the true remaining time, and with a rebuild at every
+    # dispatch the predictive policy makes Belady's choices
+    rng = random.Random(100 + seed)
+    x = [rng.uniform(0.5, 40.0) for _ in range(3)]
+    sessions = _random_sessions(rng, rng.randint(3, 8), 3, fixed_tool_s=x)
+    cfg = dict(M=rng.randint(30, 60), block_tokens=16, prefill_s_per_token=2e-3, decode_s_per_token=2e-2)
+    need = max(-(-sum(t.in_tokens + t.out_tokens for t in s.turns) // 16) for s in sessions)
+    cfg["M"] = max(cfg["M"], need)
+    a = cp.simulate(cp.Config(sched="prefix", evict="predictive", n_rebuild=1, **cfg), sessions, [[v] for v in x])
+    b = cp.simulate(cp.Config(sched="prefix", evict="belady", **cfg), sessions, [[v] for v in x])
+    assert a.dispatch == b.dispatch
+    assert (a.evicted_blocks, a.faults, a.recomputed_tokens) == (b.evicted_blocks, b.faults, b.recomputed_tokens)
+    assert a.makespan_s == b.makespan_s
+
+
+def test_unbounded_capacity_never_evicts():
+    rng = random.Random(7)
+    sessions = _random_sessions(rng, 6, 2)
+    for sched, evict in itertools.product(("fcfs", "prefix"), ("lru", "predictive", "belady")):
+        r = cp.simulate(cp.Config(M=10**9, block_tokens=16, prefill_s_per_token=1e-3, sched=sched,
+                                  evict=evict), sessions, [[1.0, 2.0], [3.0]])
+        assert r.evicted_blocks == 0 and r.faults == 0 and r.recomputed_tokens == 0
+        assert r.prefilled_tokens == sum(t.in_tokens for s in sessions for t in s.turns)
+        assert r.requests == sum(len(s.turns) for s in sessions)
