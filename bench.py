@@ -52,6 +52,8 @@ def parse():
                     help="steps of the decode measurement added to an extend run (0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables)")
+    ap.add_argument("--no-policy", dest="policy", action="store_false",
+                    help="skip the host KV-block policy comparison added to an extend run")
     ap.add_argument("--no-swap", dest="swap", action="store_false",
                     help="skip the page swap measurement added to an extend run")
     ap.add_argument("--separate-calls", action="store_true",
@@ -328,6 +330,10 @@ def main():
             "kernel": d["kernel"]}
         print(f"[bench] decode step {d['ms']:.4f} ms, kernel {d['kern_ms']:.4f} ms", file=sys.stderr,
               flush=True)
+    if not decode and args.policy:
+        from paper_2606_16824_amd import policy_bench
+        result["policy"] = policy_bench.run()
+        print("[bench] policy simulation done", file=sys.stderr, flush=True)
     if not decode and args.swap:
         result["swap"] = run_swap()
         print(f"[bench] swap {result['swap']}", file=sys.stderr, flush=True)

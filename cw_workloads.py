@@ -349,3 +349,57 @@ def materialize(spec: WorkloadSpec, threads: int = 8) -> Workload:
 
 def make(name: str, seed: Optional[int] = None, threads: int = 8) -> Workload:
     return materialize(spec_for(name, seed), threads=threads)
+
+
+# ----------------------------------------------------------------------------
+# agent sessions for the KV-block policy (stand-ins for the paper's traces)
+
+# tool types: (median seconds, lognormal sigma), spanning the orders of magnitude
+# of tool execution times the paper reports (sub-second one-liners to builds)
+AGENT_TOOLS = ((0.1, 0.8), (1.0, 0.7), (3.0, 1.0), (10.0, 1.2), (22.0, 0.9))
+
+
+@dataclasses.dataclass
+class AgentTrace:
+    """Closed-loop agent sessions: sessions[s] = (start_s, [(in_tokens, out_tokens,
+    tool_type, tool_s), ...]); history[y] = past durations of tool type y; a node of
+    capacity_blocks blocks of block_tokens tokens and a linear service-time model."""
+
+    sessions: list
+    history: list
+    capacity_blocks: int
+    block_tokens: int
+    prefill_s_per_token: float
+    decode_s_per_token: float
+
+
+def agent_sessions(num_sessions: int = 32, seed: int = 2000, max_turns: int = 24,
+                   block_tokens: int = 16, capacity_fraction: float = 0.4,
+                   history_samples: int = 400) -> AgentTrace:
+    """Seeded synthetic sessions: a 2-6k-token opening prompt, then turns whose
+    inputs are tool outputs (lognormal, median 300 tokens) and outputs of 20-300
+    tokens, each followed by a tool call of one of AGENT_TOOLS; starts U[0, 30) s.
+    The node holds `capacity_fraction` of the sessions' final KV blocks (at least
+    the largest session's), so they compete for memory."""
+    ss = np.random.SeedSequence(seed)
+    c_sess, c_hist = ss.spawn(2)
+    g = np.random.default_rng(c_sess)
+    sessions = []
+    final_blocks = []
+    for _ in range(num_sessions):
+        n_turns = int(g.integers(max(1, max_turns // 2), max_turns + 1))
+        turns = []
+        ctx = 0
+        for j in range(n_turns):
+            tin = int(g.integers(2000, 6001)) if j == 0 else int(min(4000, g.lognormal(np.log(300.0), 0.8)))
+            tout = int(g.integers(20, 301))
+            y = int(g.integers(0, len(AGENT_TOOLS)))
+            med, sig = AGENT_TOOLS[y]
+            turns.append((tin, tout, y, float(g.lognormal(np.log(med), sig))))
+            ctx += tin + tout
+        sessions.append((float(g.uniform(0.0, 30.0)), turns))
+        final_blocks.append(-(-ctx // block_tokens))
+    gh = np.random.default_rng(c_hist)
+    history = [gh.lognormal(np.log(med), sig, size=history_samples).tolist() for med, sig in AGENT_TOOLS]
+    cap = max(max(final_blocks), int(capacity_fraction * sum(final_blocks)))
+    return AgentTrace(sessions, history, cap, block_tokens, 5e-5, 1e-2)

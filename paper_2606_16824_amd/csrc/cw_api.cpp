@@ -32,6 +32,12 @@ cw_status_t fail(cw_status_t s, const char* fmt, ...) {
   return s;
 }
 
+}  // namespace
+
+void set_last_error(const char* msg) { g_last_error = msg; }
+
+namespace {
+
 cw_status_t hip_fail(hipError_t e, const char* what) {
   return fail(CW_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }

@@ -114,6 +114,9 @@ struct SwapParams {
   int32_t scales_per_block;  // Hkv
 };
 
+// Sets the thread-local message returned by cw_last_error_message.
+void set_last_error(const char* msg);
+
 // Kernel launchers (each defined in the translation unit of its kernel).
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                              hipStream_t stream);

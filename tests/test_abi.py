@@ -13,7 +13,8 @@ import pytest
 import paper_2606_16824_amd as cwlib
 from paper_2606_16824_amd import _lib as L
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "cw.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = [os.path.join(INCLUDE, h) for h in ("cw.h", "cw_policy.h")]
 
 
 def lib():
@@ -21,7 +22,7 @@ def lib():
 
 
 def test_exports_every_declared_symbol():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     names = set(re.findall(r"\b(cw_[a-z0-9_]+)\s*\(", text))
     assert {"cw_kv_write_pages", "cw_extend_attention", "cw_decode_attention"} <= names
     for n in sorted(names):
