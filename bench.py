@@ -58,7 +58,7 @@ def parse():
                     help="skip the page swap measurement added to an extend run")
     ap.add_argument("--separate-calls", action="store_true",
                     help="time an extend step as cw_kv_write_pages + cw_extend_attention instead of "
-                         "the one-launch cw_write_extend_attention")
+                         "cw_step_attention")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (for "
                          "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -142,7 +142,8 @@ def cpu_baseline(w, target_s: float):
 
 def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
     """Times `steps` hot-path steps (page write + attention) of a named workload: one
-    cw_write_extend_attention per extend step (two calls with `separate`), and
+    cw_step_attention per extend step (its decodes on the decode kernel, the page
+    write fused into the extend launch; two calls with `separate`), and
     cw_kv_write_pages + cw_decode_attention per decode step."""
     import torch
     import cw_workloads as cw
@@ -162,18 +163,21 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
     if decode:
         nb = cwlib.decode_workspace_bytes(s.prefix_lens, s.num_kv_heads, s.gqa_group, s.head_dim,
                                           s.page_size, s.kv_dtype)
-    else:
+    elif separate:
         nb = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
                                           s.gqa_group, s.head_dim, s.page_size, s.kv_dtype)
+    else:
+        nb = cwlib.step_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
+                                        s.gqa_group, s.head_dim, s.page_size, s.kv_dtype)
     ws_att = torch.empty(nb, dtype=torch.uint8, device=dev)
     ws_wr = torch.empty(cwlib.write_pages_workspace_bytes(s.num_seqs), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
         if not decode and not separate:
-            cwlib.write_extend_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
-                                         s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs,
-                                         out=out, lse=lse, workspace=ws_att)
+            cwlib.step_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
+                                 s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs,
+                                 out=out, lse=lse, workspace=ws_att)
             return
         cwlib.kv_write_pages(kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens, k_scale=ks,
                              v_scale=vs, workspace=ws_wr)
@@ -312,7 +316,7 @@ def main():
         "config": {"workload": WORKLOAD_DESC[args.workload], "new_tokens": s.total_new_tokens,
                    "calls": ("cw_decode_attention" if decode else
                              "cw_kv_write_pages + cw_extend_attention" if args.separate_calls else
-                             "cw_write_extend_attention"),
+                             "cw_step_attention"),
                    "tflop_per_step": round(s.flops() / 1e12, 5), "seed": s.seed},
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
         "roofline": roof,

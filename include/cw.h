@@ -135,6 +135,33 @@ cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const vo
                                       cw_kv_dtype_t kv_dtype, void* out, float* lse,
                                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* One serving step (a chunked-prefill batch: sequences extending their
+ * cached prefix by a chunk of new tokens, mixed with decodes of one token;
+ * CacheWise Sec. 6.1 serves with chunked prefill): writes every sequence's
+ * new K/V into the pools and computes the attention of every new token, like
+ * cw_kv_write_pages + cw_extend_attention over the whole batch.  Sequences
+ * with exactly one new token run on the HBM-streaming decode kernel, the
+ * others on the extend kernel (which also performs the batch's page write),
+ * each sub-batch with the plan it would get alone: the rows of the decode
+ * sequences are bit-identical to cw_decode_attention of those sequences, the
+ * other rows to cw_extend_attention of the others, and the pools to
+ * cw_kv_write_pages.  Arguments, layouts and errors as for
+ * cw_write_extend_attention; the workspace is cw_step_workspace_bytes.  With
+ * timing events set, `start` is recorded before the step's first attention
+ * kernel and `stop` after its extend kernel (after the decode part and the
+ * page write when no sequence extends by more than one token). */
+size_t cw_step_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                               int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                               int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype);
+cw_status_t cw_step_attention(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                              void* v_pool, const float* k_scale, const float* v_scale,
+                              const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                              const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                              int32_t head_dim, int32_t page_size, float softmax_scale,
+                              cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
 /* Page swaps between the device page pool and a host block pool (CacheWise
  * Sec. 6.4: in the offloading configuration, evicted KV blocks move to CPU DRAM
  * and are swapped back when their session resumes).  The host pools have the

@@ -28,7 +28,8 @@ from . import _lib as L
 
 __all__ = ["CWError", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
-           "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes"]
+           "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
+           "step_attention", "step_workspace_bytes"]
 
 
 class CWError(RuntimeError):
@@ -172,6 +173,32 @@ def write_extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_
         workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
                                q.device, None)
     _check(library().cw_write_extend_attention(
+        _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
+        _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
+        len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),
+        _dptr(lse), _dptr(workspace), workspace.numel(), _stream()))
+    return out
+
+
+def step_workspace_bytes(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page_size,
+                         kv_dtype="bf16") -> int:
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    return int(library().cw_step_workspace_bytes(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group,
+                                                 head_dim, page_size, _dtype_code(kv_dtype)))
+
+
+def step_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
+                   gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None, lse=None,
+                   workspace=None):
+    """One serving step: page write + attention, decodes on the decode kernel."""
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    num_pages, hkv, page, d = k_pool.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = _workspace(step_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
+                               q.device, None)
+    _check(library().cw_step_attention(
         _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
         _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
         len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),

@@ -31,6 +31,10 @@ SIGNATURES = {
                                             _vp, _vp, _vp, _sz, _vp]),
     "cw_decode_workspace_bytes": (_sz, [_vp, _i32, _i32, _i32, _i32, _i32, _i32]),
     "cw_swap_workspace_bytes": (_sz, [_i32]),
+    "cw_step_workspace_bytes": (_sz, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32]),
+    "cw_step_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                    _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
+                                    _vp, _sz, _vp]),
     "cw_kv_swap_out": (C.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
                                  _i32, _i32, _i32, C.c_int, _vp, _sz, _vp]),
     "cw_kv_swap_in": (C.c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32,

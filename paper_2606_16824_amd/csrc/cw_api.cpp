@@ -206,25 +206,89 @@ int64_t sum_suffix(const int32_t* ls, int32_t num_seqs) {
 // Both pool dtypes run the LDS-staged kernel: LDS_BLOCK_M rows per work item,
 // one workgroup per CU.
 ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t num_kv_heads,
-                     int32_t gqa_group, int32_t head_dim, cw_kv_dtype_t kv_dtype) {
+                     int32_t gqa_group, int32_t head_dim, cw_kv_dtype_t kv_dtype,
+                     const int32_t* cu_rows = nullptr, const int32_t* bt_rows = nullptr) {
   (void)kv_dtype;
   int32_t cus = 256, xcds = 8;
   device_shape(&cus, &xcds);
   return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, LDS_BLOCK_M, 1,
-                           cus, xcds, current_tuning());
+                           cus, xcds, current_tuning(), cu_rows, bt_rows);
 }
 
 // Decode plans follow the pool dtype's tile length and residency (three
 // 16 KB-tile waves per CU for bf16, six 8 KB-tile waves for fp8).
 ExtendPlan make_decode_plan(const int32_t* lp, int32_t num_seqs, int32_t num_kv_heads,
                             int32_t gqa_group, int32_t head_dim, int32_t page_size,
-                            cw_kv_dtype_t kv_dtype) {
+                            cw_kv_dtype_t kv_dtype, const int32_t* cu_rows = nullptr,
+                            const int32_t* bt_rows = nullptr) {
   int32_t cus = 256, xcds = 8;
   device_shape(&cus, &xcds);
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
   return build_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size,
                            decode_keys_per_tile(head_dim, fp8), decode_waves_per_cu(fp8), cus,
-                           current_tuning());
+                           current_tuning(), cu_rows, bt_rows);
+}
+
+// A step of a serving engine: the sequences with one new token go to the decode
+// kernel, the others to the extend kernel, as sub-batches whose plans keep the
+// step's packed rows and block-table rows.
+struct StepPlan {
+  std::vector<int32_t> ext, dec;  // step sequence indices of each sub-batch
+  ExtendPlan ext_plan, dec_plan;
+  std::vector<SeqInfo> seqs;      // every sequence of the step (for the page write)
+  // workspace: [step seqs | extend meta | decode meta | extend partials | decode partials]
+  size_t off_ext_meta = 0, off_dec_meta = 0, off_ext_part = 0, off_dec_part = 0, meta_bytes = 0,
+         total_bytes = 0;
+};
+
+size_t align256h(size_t x) { return (x + 255) & ~size_t(255); }
+
+StepPlan make_step_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t num_kv_heads,
+                        int32_t gqa_group, int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype) {
+  StepPlan sp;
+  std::vector<int32_t> lp_e, ls_e, cu_e, lp_d, cu_d;
+  int32_t cu = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    sp.seqs.push_back(SeqInfo{lp[b], ls[b], cu, b});
+    if (ls[b] == 1) {
+      sp.dec.push_back(b);
+      lp_d.push_back(lp[b]);
+      cu_d.push_back(cu);
+    } else if (ls[b] > 1) {
+      sp.ext.push_back(b);
+      lp_e.push_back(lp[b]);
+      ls_e.push_back(ls[b]);
+      cu_e.push_back(cu);
+    }
+    cu += ls[b];
+  }
+  if (!sp.ext.empty())
+    sp.ext_plan = make_plan(lp_e.data(), ls_e.data(), static_cast<int32_t>(sp.ext.size()), num_kv_heads,
+                            gqa_group, head_dim, kv_dtype, cu_e.data(), sp.ext.data());
+  if (!sp.dec.empty())
+    sp.dec_plan = make_decode_plan(lp_d.data(), static_cast<int32_t>(sp.dec.size()), num_kv_heads,
+                                   gqa_group, head_dim, page_size, kv_dtype, cu_d.data(), sp.dec.data());
+  sp.off_ext_meta = align256h(sp.seqs.size() * sizeof(SeqInfo));
+  sp.off_dec_meta = sp.off_ext_meta + sp.ext_plan.meta_bytes;
+  sp.meta_bytes = sp.off_dec_meta + sp.dec_plan.meta_bytes;
+  sp.off_ext_part = sp.meta_bytes;
+  sp.off_dec_part = sp.off_ext_part + (sp.ext_plan.total_bytes - sp.ext_plan.meta_bytes);
+  sp.total_bytes = std::max<size_t>(256, sp.off_dec_part + (sp.dec_plan.total_bytes - sp.dec_plan.meta_bytes));
+  return sp;
+}
+
+// Kernel arguments of a plan whose meta sits at ws + meta and partials at ws + part.
+ExtendParams plan_params(const ExtendPlan& plan, uint8_t* ws, size_t meta, size_t part) {
+  ExtendParams p{};
+  p.seqs = reinterpret_cast<const SeqInfo*>(ws + meta + plan.off_seqs);
+  p.items = reinterpret_cast<const WorkItem*>(ws + meta + plan.off_items);
+  p.groups = reinterpret_cast<const CombineGroup*>(ws + meta + plan.off_groups);
+  p.part_o = reinterpret_cast<float*>(ws + part + (plan.off_part_o - plan.meta_bytes));
+  p.part_ml = reinterpret_cast<float*>(ws + part + (plan.off_part_ml - plan.meta_bytes));
+  p.n_items = static_cast<int32_t>(plan.items.size());
+  p.n_groups = static_cast<int32_t>(plan.groups.size());
+  p.part_rows = plan.part_rows;
+  return p;
 }
 
 cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, void* k_pool,
@@ -404,6 +468,117 @@ cw_status_t swap_impl(const void* src_k, const void* src_v, const float* src_ks,
   return CW_OK;
 }
 
+cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                      const float* k_scale, const float* v_scale, const int32_t* block_table,
+                      int32_t bt_stride, int32_t num_pages, const int32_t* lp, const int32_t* ls,
+                      int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                      int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype, void* out,
+                      float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  cw_status_t s = check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size);
+  if (s != CW_OK) return s;
+  s = check_dtype(kv_dtype, k_scale, v_scale);
+  if (s != CW_OK) return s;
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(CW_ERR_UNSUPPORTED, "softmax_scale = %g (must be finite and > 0)", double(softmax_scale));
+  if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
+  s = check_lens(lp, ls, num_seqs, bt_stride, page_size, num_kv_heads, gqa_group, head_dim, true);
+  if (s != CW_OK) return s;
+  const int64_t total = sum_suffix(ls, num_seqs);
+  if (total == 0) return CW_OK;
+  if (!q || !k_new || !v_new || !out || !block_table)
+    return fail(CW_ERR_NULL, "q, k_new, v_new, out and block_table are required");
+  if (!k_pool || !v_pool) return fail(CW_ERR_NULL, "k_pool / v_pool is NULL");
+  if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(out) ||
+      !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(workspace))
+    return fail(CW_ERR_ALIGN, "tensor and workspace pointers must be 16-byte aligned");
+  if (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)) return fail(CW_ERR_ALIGN, "lse not 4-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(block_table) & 3u)) return fail(CW_ERR_ALIGN, "block_table not 4-byte aligned");
+
+  const StepPlan sp = make_step_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype);
+  if (workspace == nullptr || workspace_bytes < sp.total_bytes)
+    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, sp.total_bytes);
+  std::vector<uint8_t> meta(sp.meta_bytes, 0);
+  std::copy(reinterpret_cast<const uint8_t*>(sp.seqs.data()),
+            reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), meta.data());
+  if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, meta.data() + sp.off_ext_meta);
+  if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, meta.data() + sp.off_dec_meta);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  s = upload(meta.data(), meta.size(), ws, stream);
+  if (s != CW_OK) return s;
+
+  auto common = [&](ExtendParams& p) {
+    p.q = q;
+    p.k_new = k_new;
+    p.v_new = v_new;
+    p.k_pool = k_pool;
+    p.v_pool = v_pool;
+    p.k_scale = k_scale;
+    p.v_scale = v_scale;
+    p.block_table = block_table;
+    p.out = out;
+    p.lse = lse;
+    p.bt_stride = bt_stride;
+    p.num_kv_heads = num_kv_heads;
+    p.gqa_group = gqa_group;
+    p.num_seqs = num_seqs;
+    p.scale_log2 = softmax_scale * 1.4426950408889634f;
+  };
+  WriteParams w{};
+  w.k_new = k_new;
+  w.v_new = v_new;
+  w.k_pool = k_pool;
+  w.v_pool = v_pool;
+  w.k_scale = k_scale;
+  w.v_scale = v_scale;
+  w.block_table = block_table;
+  w.seqs = reinterpret_cast<const SeqInfo*>(ws);
+  w.bt_stride = bt_stride;
+  w.num_seqs = num_seqs;
+  w.num_kv_heads = num_kv_heads;
+  w.total_tokens = static_cast<int32_t>(total);
+
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  {
+    std::lock_guard<std::mutex> g(g_tuning_mu);
+    ev0 = g_ev_start;
+    ev1 = g_ev_stop;
+  }
+  const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  hipError_t e = hipSuccess;
+  if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if (!sp.dec.empty()) {
+    ExtendParams pd = plan_params(sp.dec_plan, ws, sp.off_dec_meta, sp.off_dec_part);
+    common(pd);
+    if ((e = launch_decode(pd, head_dim, page_size, fp8, stream)) != hipSuccess)
+      return hip_fail(e, "decode kernel launch");
+    if (pd.n_groups > 0) {
+      int max_parts = 0;
+      for (const CombineGroup& g : sp.dec_plan.groups) max_parts = std::max(max_parts, g.n_parts);
+      if ((e = launch_combine(pd, head_dim, max_parts, stream)) != hipSuccess)
+        return hip_fail(e, "combine kernel launch");
+    }
+  }
+  if (!sp.ext.empty()) {
+    ExtendParams pe = plan_params(sp.ext_plan, ws, sp.off_ext_meta, sp.off_ext_part);
+    common(pe);
+    pe.w = w;  // every sequence's new K/V, written under the extend's first tiles
+    if ((e = launch_extend_lds(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
+      return hip_fail(e, "extend kernel launch");
+    if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (pe.n_groups > 0) {
+      int max_parts = 0;
+      for (const CombineGroup& g : sp.ext_plan.groups) max_parts = std::max(max_parts, g.n_parts);
+      if ((e = launch_combine(pe, head_dim, max_parts, stream)) != hipSuccess)
+        return hip_fail(e, "combine kernel launch");
+    }
+  } else {
+    if ((e = launch_write_pages(w, head_dim, page_size, fp8, stream)) != hipSuccess)
+      return hip_fail(e, "write_pages kernel launch");
+    if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  return CW_OK;
+}
+
 }  // namespace
 }  // namespace cw
 
@@ -473,7 +648,7 @@ cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool
   std::vector<SeqInfo> seqs(num_seqs);
   int64_t cu = 0;
   for (int32_t b = 0; b < num_seqs; ++b) {
-    seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), 0};
+    seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), b};
     cu += suffix_lens_h[b];
   }
   s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
@@ -537,6 +712,34 @@ cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const vo
                      num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
                      head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
                      workspace_bytes, stream, false, true);
+}
+
+size_t cw_step_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                               int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                               int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype) {
+  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
+  if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                 head_dim, false) != CW_OK)
+    return 0;
+  if (num_seqs == 0) return 256;
+  return make_step_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim,
+                        page_size, kv_dtype)
+      .total_bytes;
+}
+
+cw_status_t cw_step_attention(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                              void* v_pool, const float* k_scale, const float* v_scale,
+                              const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                              const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
+                              int32_t head_dim, int32_t page_size, float softmax_scale,
+                              cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+  return step_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
+                   num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
+                   head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
+                   workspace_bytes, stream);
 }
 
 size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,

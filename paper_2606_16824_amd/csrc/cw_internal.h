@@ -19,10 +19,10 @@ constexpr int LDS_BLOCK_M = LDS_WAVES * 32;
 
 // Per-sequence metadata on the device.
 struct SeqInfo {
-  int32_t lp;  // cached prefix length
-  int32_t ls;  // suffix length
-  int32_t cu;  // first packed token row of the sequence
-  int32_t pad;
+  int32_t lp;      // cached prefix length
+  int32_t ls;      // suffix length
+  int32_t cu;      // first packed token row of the sequence
+  int32_t bt_row;  // its row of the block table
 };
 
 // One workgroup's share of the extend: packed query rows

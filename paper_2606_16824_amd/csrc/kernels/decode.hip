@@ -144,7 +144,7 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   const int kvh = it.kvh;
   const int lp = sq.lp;
   const int tok = sq.cu;  // the sequence's single new token
-  const int32_t* bt = p.block_table + size_t(it.seq) * p.bt_stride;
+  const int32_t* bt = p.block_table + size_t(sq.bt_row) * p.bt_stride;
   const uint8_t* k_pool = static_cast<const uint8_t*>(p.k_pool);
   const uint8_t* v_pool = static_cast<const uint8_t*>(p.v_pool);
   const bool row_ok = col < G;

@@ -182,7 +182,7 @@ void extend_lds_kernel(ExtendParams p) {
   const int G = p.gqa_group, hkv = p.num_kv_heads, hq = hkv * G;
   const int kvh = it.kvh;
   const int lp = sq.lp, total_len = sq.lp + sq.ls;
-  const int32_t* bt = p.block_table + size_t(it.seq) * p.bt_stride;
+  const int32_t* bt = p.block_table + size_t(sq.bt_row) * p.bt_stride;
   const uint8_t* k_pool = static_cast<const uint8_t*>(p.k_pool);
   const uint8_t* v_pool = static_cast<const uint8_t*>(p.v_pool);
   const uint8_t* k_new = static_cast<const uint8_t*>(p.k_new);

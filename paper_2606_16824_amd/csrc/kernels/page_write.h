@@ -53,7 +53,7 @@ __device__ __forceinline__ void write_piece(const WriteParams& p, int64_t idx) {
   }
   const SeqInfo sq = p.seqs[lo];
   const int pos = sq.lp + (tok - sq.cu);
-  const int pg = p.block_table[size_t(lo) * p.bt_stride + pos / P];
+  const int pg = p.block_table[size_t(sq.bt_row) * p.bt_stride + pos / P];
   const int slot = pos % P;
   const size_t src = (size_t(tok) * hkv + h) * D + c8 * 8;
   const size_t dst = ((size_t(pg) * hkv + h) * P + slot) * D + c8 * 8;

@@ -43,12 +43,14 @@ void layout_workspace(ExtendPlan& plan, int32_t head_dim);
 ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
                              int32_t head_dim, int32_t block_m, int32_t wgs_per_cu,
-                             int32_t num_cus, int32_t num_xcds, const Tuning& tuning) {
+                             int32_t num_cus, int32_t num_xcds, const Tuning& tuning,
+                             const int32_t* cu_rows, const int32_t* bt_rows) {
   ExtendPlan plan;
   plan.seqs.resize(num_seqs);
   int64_t cu = 0;
   for (int32_t b = 0; b < num_seqs; ++b) {
-    plan.seqs[b] = SeqInfo{prefix_lens[b], suffix_lens[b], static_cast<int32_t>(cu), 0};
+    plan.seqs[b] = SeqInfo{prefix_lens[b], suffix_lens[b],
+                           cu_rows ? cu_rows[b] : static_cast<int32_t>(cu), bt_rows ? bt_rows[b] : b};
     cu += suffix_lens[b];
   }
 
@@ -205,13 +207,13 @@ void layout_workspace(ExtendPlan& plan, int32_t head_dim) {
 ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32_t num_kv_heads,
                              int32_t gqa_group, int32_t head_dim, int32_t page_size,
                              int32_t keys_per_tile, int32_t waves_per_cu, int32_t num_cus,
-                             const Tuning& tuning) {
+                             const Tuning& tuning, const int32_t* cu_rows, const int32_t* bt_rows) {
   ExtendPlan plan;
   plan.part_rows = gqa_group;
   plan.seqs.resize(num_seqs);
   int64_t total_tiles = 0;
   for (int32_t b = 0; b < num_seqs; ++b) {
-    plan.seqs[b] = SeqInfo{prefix_lens[b], 1, b, 0};
+    plan.seqs[b] = SeqInfo{prefix_lens[b], 1, cu_rows ? cu_rows[b] : b, bt_rows ? bt_rows[b] : b};
     total_tiles += (int64_t(prefix_lens[b]) + keys_per_tile) / keys_per_tile * num_kv_heads;
   }
   const int64_t unit = std::max<int64_t>(keys_per_tile, page_size);  // chunk granule

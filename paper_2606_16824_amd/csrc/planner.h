@@ -29,18 +29,22 @@ struct ExtendPlan {
 
 // Builds the plan for a kernel whose workgroups own `block_m` rows and of
 // which `wgs_per_cu` are resident per CU.  `num_cus` and `num_xcds` describe
-// the device.  Lengths must already be validated.
+// the device.  Lengths must already be validated.  Sequence b's first packed
+// row is cu_rows[b] and its block-table row bt_rows[b] when given (a sub-batch
+// of a larger step), else the prefix sum of the suffix lengths and b.
 ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_lens,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
                              int32_t head_dim, int32_t block_m, int32_t wgs_per_cu,
-                             int32_t num_cus, int32_t num_xcds, const Tuning& tuning);
+                             int32_t num_cus, int32_t num_xcds, const Tuning& tuning,
+                             const int32_t* cu_rows = nullptr, const int32_t* bt_rows = nullptr);
 
 // Decode plan (every suffix length 1): one item per (sequence, kv head, key
 // chunk) with `gqa_group` rows; `keys_per_tile` is the decode kernel's tile.
 ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32_t num_kv_heads,
                              int32_t gqa_group, int32_t head_dim, int32_t page_size,
                              int32_t keys_per_tile, int32_t waves_per_cu, int32_t num_cus,
-                             const Tuning& tuning);
+                             const Tuning& tuning, const int32_t* cu_rows = nullptr,
+                             const int32_t* bt_rows = nullptr);
 
 // Serialises seqs, items and groups into `dst` (meta_bytes long) at their offsets.
 void pack_plan_meta(const ExtendPlan& plan, uint8_t* dst);

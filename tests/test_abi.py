@@ -39,7 +39,24 @@ def test_status_strings():
 FAKE = 0x100000  # a 16-byte-aligned address that is never dereferenced
 
 
+def _step(**over):
+    lp = np.array(over.pop("lp", [10, 20]), dtype=np.int32)
+    ls = np.array(over.pop("ls", [5, 6]), dtype=np.int32)
+    a = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k_pool=FAKE, v_pool=FAKE, k_scale=None, v_scale=None,
+             block_table=FAKE, bt_stride=4, num_pages=100, num_kv_heads=2, gqa_group=4,
+             head_dim=128, page_size=16, scale=0.088, kv_dtype=0, out=FAKE, lse=None,
+             workspace=FAKE, workspace_bytes=1 << 40)
+    a.update(over)
+    return lib().cw_step_attention(
+        a["q"], a["k_new"], a["v_new"], a["k_pool"], a["v_pool"], a["k_scale"], a["v_scale"],
+        a["block_table"], a["bt_stride"], a["num_pages"], lp.ctypes.data, ls.ctypes.data, len(lp),
+        a["num_kv_heads"], a["gqa_group"], a["head_dim"], a["page_size"], a["scale"],
+        a["kv_dtype"], a["out"], a["lse"], a["workspace"], a["workspace_bytes"], None)
+
+
 def _extend(fused=False, **over):
+    if fused == "step":
+        return _step(**over)
     lp = np.array(over.pop("lp", [10, 20]), dtype=np.int32)
     ls = np.array(over.pop("ls", [5, 6]), dtype=np.int32)
     a = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k_pool=FAKE, v_pool=FAKE, k_scale=None, v_scale=None,
@@ -78,7 +95,7 @@ def _extend(fused=False, **over):
     (dict(workspace_bytes=16), L.CW_ERR_WORKSPACE),
     (dict(workspace=None), L.CW_ERR_WORKSPACE),
 ])
-@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("fused", [False, True, "step"])
 def test_extend_rejects_before_any_gpu_work(over, status, fused):
     assert _extend(fused=fused, **over) == status
     assert lib().cw_last_error_message().decode()
