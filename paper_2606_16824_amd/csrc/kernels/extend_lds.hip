@@ -418,7 +418,7 @@ void extend_lds_kernel(ExtendParams p) {
   };
   // fp8: log2 units relative to the running max, times the page's K scale,
   // plus log2 of its V scale (bf16 scores leave the MFMAs in these units)
-  auto to_log2 = [&](int j0, int slot, f32x16(&s)[2]) __attribute__((always_inline)) {
+  auto to_log2 = [&](int j0, int slot, f32x16(&s)[2], bool edge) __attribute__((always_inline)) {
     if constexpr (FP8) {
       uint32_t cgv[4], lvv[4];
 #pragma unroll
@@ -426,7 +426,7 @@ void extend_lds_kernel(ExtendParams p) {
         cgv[gi] = prm[slot][gi];
         lvv[gi] = prm[slot][4 + gi];
       }
-      if (!straddles(j0)) {
+      if (!(edge && straddles(j0))) {
 #pragma unroll
         for (int gi = 0; gi < 4; ++gi) {
           const float cg = __uint_as_float(cgv[gi]), lo = __uint_as_float(lvv[gi]) - m_run;
@@ -452,8 +452,8 @@ void extend_lds_kernel(ExtendParams p) {
   // weight carries its page's V scale, which the sum divides back out: per
   // 16-key group the rounded weights are summed, then scaled by 1 / V scale in
   // fp32 (key by key in a tile straddling the prefix end).
-  auto weights = [&](int j0, int slot, const f32x16(&x)[2], bf16x8(&pf)[4],
-                     float& lsum) __attribute__((always_inline)) {
+  auto weights = [&](int j0, int slot, const f32x16(&x)[2], bf16x8(&pf)[4], float& lsum,
+                     bool edge) __attribute__((always_inline)) {
     const bf16x2 one = __builtin_bit_cast(bf16x2, kOnePair);
 #pragma unroll
     for (int gi = 0; gi < 4; ++gi)
@@ -475,7 +475,7 @@ void extend_lds_kernel(ExtendParams p) {
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) iv[gi] = __uint_as_float(prm[slot][8 + gi]);
       float acc = 0.f;
-      if (!straddles(j0)) {
+      if (!(edge && straddles(j0))) {
 #pragma unroll
         for (int gi = 0; gi < 4; ++gi) {
           float la = 0.f, lb = 0.f;
@@ -602,7 +602,7 @@ void extend_lds_kernel(ExtendParams p) {
     if (visible(0)) {
       scores(lds_k0, xa);
       mask(tile0(0), xa);
-      to_log2(tile0(0), 0, xa);  // m_run = 0 here
+      to_log2(tile0(0), 0, xa, true);  // m_run = 0 here
       const float mx = row_max(xa);
       // a row with no visible key in the first tile sees none in the item
       const float d = mx == -INFINITY ? 0.f : mx;
@@ -618,13 +618,14 @@ void extend_lds_kernel(ExtendParams p) {
   // the work of iteration j after its staging is issued: tile j+1's scores
   // (discarded after the last visible tile: the stage then holds finite stale
   // data) while tile j's weights are formed, then tile j's P V while tile j+1's
-  // scores are scaled
-  auto compute = [&](int j, const uint8_t* k_nxt, const uint8_t* v_cur, bool may_mask,
+  // scores are scaled.  `edge` false: tiles j and j+1 lie wholly in the prefix
+  // (no mask, no tile straddling the prefix end).
+  auto compute = [&](int j, const uint8_t* k_nxt, const uint8_t* v_cur, bool edge,
                      f32x16(&x)[2], f32x16(&s)[2]) __attribute__((always_inline)) {
     bf16x8 pf[4];
     float lsum;
     scores(k_nxt, s);
-    weights(tile0(j), j & 3, x, pf, lsum);
+    weights(tile0(j), j & 3, x, pf, lsum, edge);
     interleave_scores_weights();
     if (__any(!(lsum <= kSumLimit))) {
       // raise the running max to this tile's row max and redo its weights
@@ -636,7 +637,7 @@ void extend_lds_kernel(ExtendParams p) {
       for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
-      weights(tile0(j), j & 3, x, pf, lsum);
+      weights(tile0(j), j & 3, x, pf, lsum, edge);
       if constexpr (!FP8) {
         // tile j+1's scores were started from the old -m_run
 #pragma unroll
@@ -645,9 +646,9 @@ void extend_lds_kernel(ExtendParams p) {
       }
     }
     l_run += lsum;
-    if (may_mask) mask(tile0(j + 1), s);
+    if (edge) mask(tile0(j + 1), s);
     accumulate(v_cur, pf);
-    to_log2(tile0(j + 1), (j + 1) & 3, s);
+    to_log2(tile0(j + 1), (j + 1) & 3, s, edge);
     interleave_pv_scale();
   };
 
