@@ -59,6 +59,12 @@ def parse():
     ap.add_argument("--separate-calls", action="store_true",
                     help="time an extend step as cw_kv_write_pages + cw_extend_attention instead of "
                          "cw_step_attention")
+    ap.add_argument("--cold-steps", type=int, default=20,
+                    help="extra steps, each after reading 1 GiB of another buffer so that the "
+                         "memory-side cache holds none of its inputs (kernel time reported "
+                         "separately; 0 disables)")
+    ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
+                    help="skip the measured MFMA and HBM ceilings")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (for "
                          "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -140,7 +146,7 @@ def cpu_baseline(w, target_s: float):
             "tok_s": n / dt}
 
 
-def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
+def run_workload(name: str, steps: int, warmup: int, separate: bool = False, cold_steps: int = 0):
     """Times `steps` hot-path steps (page write + attention) of a named workload: one
     cw_step_attention per extend step (its decodes on the decode kernel, the page
     write fused into the extend launch; two calls with `separate`), and
@@ -195,8 +201,9 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
     torch.cuda.synchronize()
     # timed region: exactly `steps` steps; the library records kernel-only events
     lib = cwlib.library()
-    k_starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    k_stops = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    n_ev = max(steps, cold_steps)
+    k_starts = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+    k_stops = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_stop = torch.cuda.Event(enable_timing=True)
     for e in k_starts + k_stops:  # torch creates the HIP event on first record
@@ -210,9 +217,67 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False):
     torch.cuda.synchronize()
     lib.cw_set_timing_events(None, None)
     ms = t_start.elapsed_time(t_stop) / steps
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)]))
+    kern = np.array([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)])
     kernel = "decode_kernel" if decode else KERNEL_SOURCES[s.kv_dtype][0]
-    return {"spec": s, "workload": w, "ms": ms, "kern_ms": kern_ms, "kernel": kernel}
+    res = {"spec": s, "workload": w, "ms": ms, "kern_ms": float(kern.mean()),
+           "kern_ms_median": float(np.median(kern)), "kern_ms_min": float(kern.min()),
+           "kernel": kernel}
+    if cold_steps > 0:
+        # outside the kernel's events: before each step, 1 GiB of another buffer is
+        # read so that the 256 MB memory-side cache (and every L2) holds none of the
+        # step's inputs.  Reads leave clean lines: a flush by writing would leave
+        # dirty lines whose write-back then competes with the measured kernel.
+        flush = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        for i in range(cold_steps):
+            flush.max()
+            lib.cw_set_timing_events(k_starts[i].cuda_event, k_stops[i].cuda_event)
+            step()
+        torch.cuda.synchronize()
+        lib.cw_set_timing_events(None, None)
+        cold = np.array([k_starts[i].elapsed_time(k_stops[i]) for i in range(cold_steps)])
+        res["cold_kern_ms_median"] = float(np.median(cold))
+        res["cold_kern_ms_min"] = float(cold.min())
+        del flush
+    return res
+
+
+def measure_ceilings(reps: int = 5):
+    """What the chip sustains on each roofline's unit of work with nothing else in
+    the way: a matrix-core loop (bf16 MFMA, no memory traffic), a streaming read and
+    a streaming copy of 4 GiB (each launch median over `reps`)."""
+    import torch
+    import paper_2606_16824_amd as cwlib
+
+    def med(fn):
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            t.append(a.elapsed_time(b))
+        return float(np.median(t))
+
+    wgs, iters = 512, 40000  # two workgroups per CU, all resident at once: no tail
+    sink = torch.empty(wgs * 8, dtype=torch.float32, device="cuda")
+    flops = float(wgs) * 8 * iters * 131072
+    mfma_ms = med(lambda: cwlib.ceiling_mfma_bf16(wgs, iters, sink))
+    buf = torch.empty(4 << 30, dtype=torch.uint8, device="cuda").fill_(3)
+    dst = torch.empty_like(buf)
+    rsink = torch.empty(16384, dtype=torch.int32, device="cuda")
+    read_ms = med(lambda: cwlib.ceiling_stream_read(buf, rsink))
+    copy_ms = med(lambda: cwlib.ceiling_stream_copy(buf, dst))
+    n = buf.numel()
+    del buf, dst
+    return {"mfma_bf16_TFLOP_s": round(flops / (mfma_ms * 1e-3) / 1e12, 1),
+            "hbm_read_GB_s": round(n / (read_ms * 1e-3) / 1e9, 1),
+            "hbm_copy_GB_s": round(2 * n / (copy_ms * 1e-3) / 1e9, 1),
+            "kernels": "mfma_loop_kernel (512 workgroups of 8 waves, 4 independent 32x32x16 bf16 "
+                       "chains per wave), stream_read_kernel / stream_copy_kernel (4 GiB, 16 B "
+                       "nontemporal loads, 4 in flight per lane, 16384 workgroups)"}
 
 
 def run_swap(reps: int = 10):
@@ -276,7 +341,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
-    res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls)
+    res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,
+                       cold_steps=args.cold_steps)
+    ceil = measure_ceilings() if args.ceilings else None
     s, w = res["spec"], res["workload"]
     ms, kern_ms = res["ms"], res["kern_ms"]
     decode = s.suffix_lens.max() == 1 and args.workload.startswith("decode")
@@ -287,6 +354,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode", args.workload),
                 "kernel": res["kernel"], "kernel_ms": round(kern_ms, 5)}
+        rate = lambda t: nbytes / (t * 1e-3) / 1e9
+        ceil_key = "hbm_read_GB_s"
         unit = "GB/s"
     else:
         flops = s.flops()
@@ -296,7 +365,19 @@ def main():
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": measured_traffic(s.kv_dtype, args.workload),
                 "kernel": res["kernel"], "kernel_ms": round(kern_ms, 5)}
+        rate = lambda t: flops / (t * 1e-3) / 1e12
+        ceil_key = "mfma_bf16_TFLOP_s"
         unit = "TFLOP/s"
+    roof["kernel_ms_median"] = round(res["kern_ms_median"], 5)
+    roof["kernel_ms_min"] = round(res["kern_ms_min"], 5)
+    if "cold_kern_ms_median" in res:
+        roof["cold"] = {"steps": args.cold_steps, "kernel_ms_median": round(res["cold_kern_ms_median"], 5),
+                        "kernel_ms_min": round(res["cold_kern_ms_min"], 5),
+                        "achieved": round(rate(res["cold_kern_ms_median"]), 2),
+                        "note": "1 GiB of another buffer read before each step, outside the kernel's events"}
+    if ceil is not None:
+        roof["measured_ceiling"] = ceil[ceil_key]
+        roof["frac_of_measured_ceiling"] = round(roof["achieved"] / ceil[ceil_key], 4)
     print(f"[bench] step {ms:.4f} ms, main kernel {kern_ms:.4f} ms, {achieved:.1f} {unit} kernel",
           file=sys.stderr, flush=True)
 
@@ -321,9 +402,11 @@ def main():
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
         "roofline": roof,
     }
+    if ceil is not None:
+        result["ceilings"] = ceil
     if not decode and args.decode_steps > 0:
         # the decode side of the metric: the mixed step's 48 decodes, fp8 pool
-        d = run_workload("decode", args.decode_steps, 10)
+        d = run_workload("decode", args.decode_steps, 10, cold_steps=args.cold_steps)
         nbytes = cw.decode_bytes(d["spec"])
         result["decode"] = {
             "workload": WORKLOAD_DESC["decode"], "ms_per_step": round(d["ms"], 5),
@@ -331,7 +414,14 @@ def main():
             "kernel_GB_s": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9, 1),
             "frac_hbm_peak": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "algorithmic_bytes": nbytes, "traffic": measured_traffic("decode", "decode"),
-            "kernel": d["kernel"]}
+            "kernel": d["kernel"], "kernel_ms": round(d["kern_ms"], 5),
+            "kernel_ms_median": round(d["kern_ms_median"], 5)}
+        if "cold_kern_ms_median" in d:
+            result["decode"]["cold_kernel_GB_s"] = round(
+                nbytes / (d["cold_kern_ms_median"] * 1e-3) / 1e9, 1)
+        if ceil is not None:
+            result["decode"]["frac_of_measured_read_ceiling"] = round(
+                nbytes / (d["kern_ms"] * 1e-3) / 1e9 / ceil["hbm_read_GB_s"], 4)
         print(f"[bench] decode step {d['ms']:.4f} ms, kernel {d['kern_ms']:.4f} ms", file=sys.stderr,
               flush=True)
     if not decode and args.policy:

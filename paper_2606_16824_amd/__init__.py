@@ -29,7 +29,8 @@ from . import _lib as L
 __all__ = ["CWError", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
            "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
-           "step_attention", "step_workspace_bytes"]
+           "step_attention", "step_workspace_bytes", "ceiling_mfma_bf16", "ceiling_stream_read",
+           "ceiling_stream_copy"]
 
 
 class CWError(RuntimeError):
@@ -267,3 +268,27 @@ def decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, 
         hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out), _dptr(lse),
         _dptr(workspace), workspace.numel(), _stream()))
     return out
+
+
+# measured ceilings (include/cw_ceiling.h): not part of the attention path
+
+def ceiling_mfma_bf16(workgroups: int, iters: int, sink: torch.Tensor) -> float:
+    """Enqueues the matrix-core loop; returns the FLOPs it performs."""
+    _check(library().cw_ceiling_mfma_bf16(int(workgroups), int(iters), _dptr(sink), _stream()))
+    return float(workgroups) * 8 * iters * 131072
+
+
+def ceiling_stream_read(src: torch.Tensor, sink: torch.Tensor) -> int:
+    """Enqueues a streaming read of `src`; returns the bytes it moves."""
+    n = src.numel() * src.element_size()
+    _check(library().cw_ceiling_stream_read(_dptr(src), n, _dptr(sink), _stream()))
+    return n
+
+
+def ceiling_stream_copy(src: torch.Tensor, dst: torch.Tensor) -> int:
+    """Enqueues a streaming copy of `src` into `dst`; returns the bytes it moves."""
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < n:
+        raise ValueError("dst is smaller than src")
+    _check(library().cw_ceiling_stream_copy(_dptr(src), _dptr(dst), n, _stream()))
+    return 2 * n

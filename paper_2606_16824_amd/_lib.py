@@ -1,5 +1,5 @@
-"""ctypes declarations of libcw.so (the C ABI declared in include/cw.h and
-include/cw_policy.h)."""
+"""ctypes declarations of libcw.so (the C ABI declared in include/cw.h,
+include/cw_ceiling.h and include/cw_policy.h)."""
 from __future__ import annotations
 
 import ctypes as C
@@ -48,6 +48,10 @@ SIGNATURES = {
     "cw_status_string": (C.c_char_p, [C.c_int]),
     "cw_last_error_message": (C.c_char_p, []),
     "cw_version": (_i32, []),
+    # include/cw_ceiling.h (measurement kernels)
+    "cw_ceiling_mfma_bf16": (C.c_int, [_i32, _i32, _vp, _vp]),
+    "cw_ceiling_stream_read": (C.c_int, [_vp, _sz, _vp, _vp]),
+    "cw_ceiling_stream_copy": (C.c_int, [_vp, _vp, _sz, _vp]),
     # include/cw_policy.h (host-only)
     "cw_policy_simulate": (C.c_int, [_vp, _vp, _vp, _vp, C.c_int64]),
     "cw_policy_predict": (C.c_int, [_vp, _i32, C.c_double, _vp]),

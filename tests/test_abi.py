@@ -14,7 +14,7 @@ import paper_2606_16824_amd as cwlib
 from paper_2606_16824_amd import _lib as L
 
 INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
-HEADERS = [os.path.join(INCLUDE, h) for h in ("cw.h", "cw_policy.h")]
+HEADERS = sorted(os.path.join(INCLUDE, h) for h in os.listdir(INCLUDE) if h.endswith(".h"))
 
 
 def lib():
@@ -211,3 +211,18 @@ def test_swap_destinations_must_be_distinct():
 def test_empty_swap_is_a_no_op():
     assert _swap(True, pages=[], host=[], pool_k=None, workspace=None) == L.CW_OK
     assert lib().cw_swap_workspace_bytes(0) >= 256 and lib().cw_swap_workspace_bytes(-1) == 0
+
+
+def test_ceiling_calls_reject_before_any_gpu_work():
+    L_ = lib()
+    assert L_.cw_ceiling_mfma_bf16(256, 10, None, None) == L.CW_ERR_NULL
+    assert L_.cw_ceiling_mfma_bf16(0, 10, 16, None) == L.CW_ERR_UNSUPPORTED
+    assert L_.cw_ceiling_mfma_bf16(256, 0, 16, None) == L.CW_ERR_UNSUPPORTED
+    assert L_.cw_ceiling_mfma_bf16(65537, 10, 16, None) == L.CW_ERR_UNSUPPORTED
+    assert L_.cw_ceiling_stream_read(None, 1024, 16, None) == L.CW_ERR_NULL
+    assert L_.cw_ceiling_stream_read(16, 0, 16, None) == L.CW_ERR_UNSUPPORTED
+    assert L_.cw_ceiling_stream_read(24, 1024, 16, None) == L.CW_ERR_ALIGN
+    assert L_.cw_ceiling_stream_read(16, 1000, 16, None) == L.CW_ERR_ALIGN
+    assert L_.cw_ceiling_stream_copy(16, None, 1024, None) == L.CW_ERR_NULL
+    assert L_.cw_ceiling_stream_copy(4096, 4096 + 512, 1024, None) == L.CW_ERR_UNSUPPORTED
+    assert b"overlap" in L_.cw_last_error_message()
