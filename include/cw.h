@@ -70,10 +70,21 @@ typedef enum {
   CW_ERR_BAD_LENS = 3,    /* negative length, Lp+Ls > bt_stride*P, or sizes overflow */
   CW_ERR_ALIGN = 4,       /* a tensor or workspace pointer not 16-byte aligned */
   CW_ERR_WORKSPACE = 5,   /* workspace_bytes smaller than the matching *_workspace_bytes() */
-  CW_ERR_HIP = 6          /* a HIP runtime call failed while enqueuing */
+  CW_ERR_HIP = 6,         /* a HIP runtime call failed while enqueuing */
+  CW_STATUS_RANGE_MIN_ = -2147483647 - 1,
+  CW_STATUS_RANGE_MAX_ = 2147483647
 } cw_status_t;
 
-typedef enum { CW_KV_BF16 = 0, CW_KV_FP8_E4M3FN = 1 } cw_kv_dtype_t;
+/* Every enum of this ABI carries two range markers (never valid arguments):
+ * they make every int32 value a value of the type, so an out-of-range argument
+ * reaches the library's checks as a plain integer and is rejected with
+ * CW_ERR_UNSUPPORTED instead of being undefined in the C++ implementation. */
+typedef enum {
+  CW_KV_BF16 = 0,
+  CW_KV_FP8_E4M3FN = 1,
+  CW_KV_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+  CW_KV_DTYPE_RANGE_MAX_ = 2147483647
+} cw_kv_dtype_t;
 
 /* Scatter the new K/V rows into their pool slots (CacheWise Sec. 2: the KV of a
  * request is kept in fixed-size blocks so a later turn can reuse it).
@@ -221,7 +232,12 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
  *   CW_TUNE_TARGET_WGS      0 = automatic; n > 0 = split-K until at least n
  *                           workgroups are launched.
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
-typedef enum { CW_TUNE_KV_CHUNK_TILES = 0, CW_TUNE_TARGET_WGS = 1 } cw_tune_key_t;
+typedef enum {
+  CW_TUNE_KV_CHUNK_TILES = 0,
+  CW_TUNE_TARGET_WGS = 1,
+  CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
+  CW_TUNE_RANGE_MAX_ = 2147483647
+} cw_tune_key_t;
 cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value);
 
 /* Benchmark hook: when `start` and `stop` are non-NULL, every later

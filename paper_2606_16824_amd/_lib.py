@@ -5,7 +5,10 @@ from __future__ import annotations
 import ctypes as C
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcw.so")
+# CW_LIBRARY names another build of the same library (the sanitizer build of
+# the host code, for the CPU tests); by default the in-tree libcw.so
+LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libcw.so")
 
 CW_OK, CW_ERR_NULL, CW_ERR_UNSUPPORTED, CW_ERR_BAD_LENS, CW_ERR_ALIGN, CW_ERR_WORKSPACE, CW_ERR_HIP = range(7)
 CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1

@@ -1,8 +1,18 @@
 """Builds libcw.so (the C-ABI library) in-tree with hipcc for gfx950.
 
-Usage: python -m paper_2606_16824_amd.build [--jobs N]
+Usage: python -m paper_2606_16824_amd.build [--jobs N] [--sanitize]
 Every .hip / .cpp under csrc/ is compiled to an object in _build/ (in
 parallel), then linked into paper_2606_16824_amd/libcw.so.
+
+--sanitize builds the host side of every source with AddressSanitizer and
+UndefinedBehaviorSanitizer (device code is built as usual) into
+_build/sanitize/libcw.so, for running the CPU tests (argument validation,
+planner, host policy simulator) under the sanitizers:
+
+    python -m paper_2606_16824_amd.build --sanitize
+    LD_PRELOAD=$(hipcc -print-file-name=libclang_rt.asan-x86_64.so) \
+    ASAN_OPTIONS=detect_leaks=0 CW_LIBRARY=_build/sanitize/libcw.so \
+    python -m pytest tests -m "not gpu"
 """
 from __future__ import annotations
 
@@ -41,25 +51,33 @@ def sources():
     return sorted(out)
 
 
-def _obj(src):
+# host-side sanitizers only: each -fsanitize= applies to the host pass
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+
+
+def _obj(src, build_dir=BUILD):
     rel = os.path.relpath(src, CSRC).replace(os.sep, "__")
-    return os.path.join(BUILD, rel + ".o")
+    return os.path.join(build_dir, rel + ".o")
 
 
-def _compile(src):
-    obj = _obj(src)
-    lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
-    cmd = [HIPCC, *COMMON, *lang, "-c", src, "-o", obj]
+def _compile(src, extra=(), build_dir=BUILD):
+    obj = _obj(src, build_dir)
+    lang = ["-x", "hip"]
+    cmd = [HIPCC, *COMMON, *extra, *lang, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     return src, r.returncode, r.stdout + r.stderr, cmd
 
 
-def build(jobs: int = 8, verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(jobs: int = 8, verbose: bool = False, sanitize: bool = False) -> str:
+    build_dir = os.path.join(BUILD, "sanitize") if sanitize else BUILD
+    lib_path = os.path.join(build_dir, "libcw.so") if sanitize else LIB
+    extra = SANITIZE if sanitize else []
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sources()
     errors = []
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
-        for src, rc, log, cmd in ex.map(_compile, srcs):
+        for src, rc, log, cmd in ex.map(lambda s_: _compile(s_, extra, build_dir), srcs):
             if verbose or rc != 0:
                 print(" ".join(cmd), file=sys.stderr)
             # the host pass does not know the packed-fp32 feature; drop that warning
@@ -70,20 +88,23 @@ def build(jobs: int = 8, verbose: bool = False) -> str:
                 errors.append(src)
     if errors:
         raise RuntimeError("hipcc failed for: " + ", ".join(errors))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp,
-           *[_obj(s) for s in srcs]]
+    tmp = lib_path + ".tmp"
+    link_extra = ["-fsanitize=address,undefined", "-shared-libsan"] if sanitize else []
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *link_extra, "-o", tmp,
+           *[_obj(s, build_dir) for s in srcs]]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         print(" ".join(cmd), "\n", r.stdout, r.stderr, file=sys.stderr)
         raise RuntimeError("link of libcw.so failed")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=8)
     ap.add_argument("-v", "--verbose", action="store_true")
+    ap.add_argument("--sanitize", action="store_true",
+                    help="host-side ASan + UBSan build into _build/sanitize/libcw.so")
     a = ap.parse_args()
-    print(build(a.jobs, a.verbose))
+    print(build(a.jobs, a.verbose, a.sanitize))

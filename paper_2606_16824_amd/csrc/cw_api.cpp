@@ -780,6 +780,7 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
   switch (key) {
     case CW_TUNE_KV_CHUNK_TILES: g_tuning.kv_chunk_tiles = value; return CW_OK;
     case CW_TUNE_TARGET_WGS: g_tuning.target_wgs = value; return CW_OK;
+    default: break;
   }
   return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));
 }
@@ -823,6 +824,7 @@ const char* cw_status_string(cw_status_t status) {
     case CW_ERR_ALIGN: return "CW_ERR_ALIGN: misaligned pointer";
     case CW_ERR_WORKSPACE: return "CW_ERR_WORKSPACE: workspace too small";
     case CW_ERR_HIP: return "CW_ERR_HIP: HIP runtime error";
+    default: break;
   }
   return "unknown cw_status_t";
 }
