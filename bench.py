@@ -57,8 +57,8 @@ def parse():
     ap.add_argument("--no-swap", dest="swap", action="store_false",
                     help="skip the page swap measurement added to an extend run")
     ap.add_argument("--separate-calls", action="store_true",
-                    help="time an extend step as cw_kv_write_pages + cw_extend_attention instead of "
-                         "cw_step_attention")
+                    help="time a step as cw_kv_write_pages + cw_extend_attention (or "
+                         "cw_decode_attention) instead of cw_step_attention")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps, each after reading 1 GiB of another buffer so that the "
                          "memory-side cache holds none of its inputs (kernel time reported "
@@ -148,9 +148,10 @@ def cpu_baseline(w, target_s: float):
 
 def run_workload(name: str, steps: int, warmup: int, separate: bool = False, cold_steps: int = 0):
     """Times `steps` hot-path steps (page write + attention) of a named workload: one
-    cw_step_attention per extend step (its decodes on the decode kernel, the page
-    write fused into the extend launch; two calls with `separate`), and
-    cw_kv_write_pages + cw_decode_attention per decode step."""
+    cw_step_attention per step (decodes on the decode kernel, extends on the extend
+    kernel, the page write fused into the extend launch, or into the decode launch
+    when there are no extends); with `separate`, cw_kv_write_pages followed by
+    cw_extend_attention or cw_decode_attention."""
     import torch
     import cw_workloads as cw
     import paper_2606_16824_amd as cwlib
@@ -166,7 +167,7 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
     ks, vs, bt = mv(w.k_scale), mv(w.v_scale), mv(w.block_table)
     out = torch.empty_like(q)
     lse = torch.empty(q.shape[0], q.shape[1], device=dev, dtype=torch.float32)
-    if decode:
+    if decode and separate:
         nb = cwlib.decode_workspace_bytes(s.prefix_lens, s.num_kv_heads, s.gqa_group, s.head_dim,
                                           s.page_size, s.kv_dtype)
     elif separate:
@@ -180,7 +181,7 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
     stream = torch.cuda.current_stream()
 
     def step():
-        if not decode and not separate:
+        if not separate:
             cwlib.step_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
                                  s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs,
                                  out=out, lse=lse, workspace=ws_att)
@@ -395,9 +396,9 @@ def main():
         "dtype": "bf16" if s.kv_dtype == "bf16" else "bf16+fp8kv",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_DESC[args.workload], "new_tokens": s.total_new_tokens,
-                   "calls": ("cw_decode_attention" if decode else
-                             "cw_kv_write_pages + cw_extend_attention" if args.separate_calls else
-                             "cw_step_attention"),
+                   "calls": (("cw_kv_write_pages + cw_decode_attention" if decode else
+                              "cw_kv_write_pages + cw_extend_attention") if args.separate_calls
+                             else "cw_step_attention"),
                    "tflop_per_step": round(s.flops() / 1e12, 5), "seed": s.seed},
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
         "roofline": roof,

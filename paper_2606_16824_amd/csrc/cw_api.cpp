@@ -549,8 +549,13 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   if (!sp.dec.empty()) {
     ExtendParams pd = plan_params(sp.dec_plan, ws, sp.off_dec_meta, sp.off_dec_part);
     common(pd);
+    // without extends, the decode launch performs the page write (each
+    // sequence's one new token, stored by the work item holding its key)
+    if (sp.ext.empty()) pd.w = w;
     if ((e = launch_decode(pd, head_dim, page_size, fp8, stream)) != hipSuccess)
       return hip_fail(e, "decode kernel launch");
+    if (sp.ext.empty() && ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess)
+      return hip_fail(e, "hipEventRecord");
     if (pd.n_groups > 0) {
       int max_parts = 0;
       for (const CombineGroup& g : sp.dec_plan.groups) max_parts = std::max(max_parts, g.n_parts);
@@ -571,10 +576,6 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
       if ((e = launch_combine(pe, head_dim, max_parts, stream)) != hipSuccess)
         return hip_fail(e, "combine kernel launch");
     }
-  } else {
-    if ((e = launch_write_pages(w, head_dim, page_size, fp8, stream)) != hipSuccess)
-      return hip_fail(e, "write_pages kernel launch");
-    if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
   return CW_OK;
 }

@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include "../cw_internal.h"
+#include "page_write.h"
 
 namespace cw {
 namespace {
@@ -180,6 +181,22 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   }
   // per page: log2 and reciprocal of the V scale (read back per key group)
   float my_lvs = 0.f, my_ivs = 1.f;
+  // Fused page write (a step of decodes only): the item holding the new key
+  // also stores the new token's K/V into slot lp of its page, after its own
+  // DMA has drained.  The attention reads no pool slot at or past lp, so the
+  // two are independent.  The page and its scales land with the page ids, so
+  // no load of this is outstanding in the counted DMA pipeline.
+  const bool writer = has_new && p.w.total_tokens > 0;
+  int pg_new = 0;
+  float ks_new = 1.f, vs_new = 1.f;
+  if (writer) {
+    pg_new = bt[lp / P];
+    if constexpr (FP8) {
+      const size_t si = size_t(pg_new) * hkv + kvh;
+      ks_new = p.k_scale[si];
+      vs_new = p.v_scale[si];
+    }
+  }
 
   // Q^T (B operand).  bf16 pools: k-step kk holds dims 16 kk + 8 h + e.  fp8
   // pools read 16 fp8 dims per fragment, so k-steps 2t and 2t+1 hold dims
@@ -381,6 +398,8 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
     step(t + 2, lds_s2);
   }
   wait_vmcnt<0>();  // no DMA may land in LDS after the wave has ended
+  if (writer && lane < D / 8)
+    pw::store_piece<D, P, FP8>(p.w, tok, kvh, lane, pg_new, lp % P, ks_new, vs_new);
 
   // the new token's own key and value (bf16, from k_new / v_new)
   if (has_new) {

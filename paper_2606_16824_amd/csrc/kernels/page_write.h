@@ -1,6 +1,7 @@
 // Scatter of one 16-byte piece of a new K/V row into its page-pool slot (bf16
 // copy, or fp8 quantise-on-write with the page's scale), shared by the
-// stand-alone page-write kernel and the extend kernel's fused write.
+// stand-alone page-write kernel and the fused writes of the extend and decode
+// kernels.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -33,6 +34,25 @@ __device__ __forceinline__ u32x2 quantise8(u32x4 x, float s) {
   return out;
 }
 
+// Elements c8 * 8 .. c8 * 8 + 7 of K and V of new row (tok, kv head h) into slot
+// `slot` of physical page `pg`; fp8 pools quantise with the page's scales ks, vs.
+template <int D, int P, bool FP8>
+__device__ __forceinline__ void store_piece(const WriteParams& p, int tok, int h, int c8, int pg,
+                                            int slot, float ks, float vs) {
+  const int hkv = p.num_kv_heads;
+  const size_t src = (size_t(tok) * hkv + h) * D + c8 * 8;
+  const size_t dst = ((size_t(pg) * hkv + h) * P + slot) * D + c8 * 8;
+  const u32x4 kx = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.k_new) + src);
+  const u32x4 vx = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.v_new) + src);
+  if constexpr (FP8) {
+    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(p.k_pool) + dst) = quantise8(kx, ks);
+    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(p.v_pool) + dst) = quantise8(vx, vs);
+  } else {
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.k_pool) + dst) = kx;
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.v_pool) + dst) = vx;
+  }
+}
+
 // Piece `idx` of the flat [token, kv head, D / 8] order: the 8 elements
 // c8 * 8 .. c8 * 8 + 7 of K and of V for (token, kv head) go to slot
 // (Lp + i) % P of page block_table[b][(Lp + i) / P], where token = cu_b + i.
@@ -54,18 +74,11 @@ __device__ __forceinline__ void write_piece(const WriteParams& p, int64_t idx) {
   const SeqInfo sq = p.seqs[lo];
   const int pos = sq.lp + (tok - sq.cu);
   const int pg = p.block_table[size_t(sq.bt_row) * p.bt_stride + pos / P];
-  const int slot = pos % P;
-  const size_t src = (size_t(tok) * hkv + h) * D + c8 * 8;
-  const size_t dst = ((size_t(pg) * hkv + h) * P + slot) * D + c8 * 8;
-  const u32x4 kx = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.k_new) + src);
-  const u32x4 vx = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.v_new) + src);
   if constexpr (FP8) {
     const size_t si = size_t(pg) * hkv + h;
-    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(p.k_pool) + dst) = quantise8(kx, p.k_scale[si]);
-    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(p.v_pool) + dst) = quantise8(vx, p.v_scale[si]);
+    store_piece<D, P, FP8>(p, tok, h, c8, pg, pos % P, p.k_scale[si], p.v_scale[si]);
   } else {
-    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.k_pool) + dst) = kx;
-    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.v_pool) + dst) = vx;
+    store_piece<D, P, FP8>(p, tok, h, c8, pg, pos % P, 1.f, 1.f);
   }
 }
 

@@ -20,6 +20,10 @@ CASES = {
     "bf16_mixed": ([40, 0, 300, 17, 128, 999, 64], [1, 5, 1, 0, 70, 1, 33], 2, 4, 128, 16, "bf16"),
     "fp8_mixed_p64": ([65, 3, 500, 130], [1, 61, 1, 200], 2, 3, 64, 64, "fp8"),
     "decodes_only": ([100, 7, 250], [1, 1, 1], 1, 8, 128, 16, "bf16"),
+    # the decode launch performs the page write; new tokens at page starts (Lp = 0, 16, 160, 64)
+    "decodes_only_fp8": ([0, 16, 33, 160, 1023], [1, 1, 1, 1, 1], 2, 4, 128, 16, "fp8"),
+    "decodes_only_fp8_p64_d64": ([64, 5, 700], [1, 1, 1], 3, 2, 64, 64, "fp8"),
+    "decodes_only_bf16_p64": ([0, 64, 4100], [1, 1, 1], 2, 8, 128, 64, "bf16"),
     "extends_only": ([31, 200], [9, 40], 2, 2, 128, 16, "fp8"),
 }
 
@@ -95,3 +99,7 @@ def test_step_matches_single_kernel_calls_and_oracle(name):
 
 def test_step_mixed_full_size():
     _check(cw.spec_for("mixed"), "mixed", with_oracle=False)
+
+
+def test_step_decodes_full_size():
+    _check(cw.spec_for("decode"), "decode", with_oracle=False)
