@@ -46,10 +46,10 @@
  * later synchronisation.  cw_last_error_message() returns a thread-local
  * description of the last error.  No call throws or aborts.
  *
- * Preconditions the library does not check (checking would need device reads):
- * page ids < num_pages; write slots of different sequences are disjoint;
- * pages shared between sequences lie inside every sharer's prefix; out and
- * lse alias no input.
+ * Preconditions the library does not check (checking would need device reads;
+ * cw_check_block_table checks the first on request): page ids < num_pages;
+ * write slots of different sequences are disjoint; pages shared between
+ * sequences lie inside every sharer's prefix; out and lse alias no input.
  */
 #ifndef CW_H_
 #define CW_H_
@@ -223,6 +223,22 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
                                 int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype,
                                 void* out, float* lse, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
+
+/* Debug check of the block-table precondition (page ids < num_pages), which the
+ * attention and page-write calls cannot check without reading device memory.
+ * For each sequence b, counts the entries block_table[b][j], j <
+ * ceil((Lp_b + Ls_b) / page_size) (exactly the entries those calls read), that
+ * lie outside [0, num_pages), and writes the count to bad_per_seq[b] (device
+ * int32 [num_seqs], overwritten; no atomics, so the counts are exact and
+ * repeatable).  Entries past a sequence's length are not read.  Lens and
+ * block_table as for cw_kv_write_pages; workspace: cw_write_pages_workspace_bytes
+ * (num_seqs) bytes, 16-byte aligned.  Errors: CW_ERR_NULL, CW_ERR_UNSUPPORTED
+ * (page_size), CW_ERR_BAD_LENS (as cw_kv_write_pages), CW_ERR_ALIGN,
+ * CW_ERR_WORKSPACE; all checked before anything is enqueued. */
+cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                                 const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                 int32_t num_seqs, int32_t page_size, int32_t* bad_per_seq,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Tuning knobs for tests and benchmarks; every value gives the same results
  * within floating-point tolerance.  Process-wide; set them before querying a

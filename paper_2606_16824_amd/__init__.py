@@ -29,7 +29,7 @@ from . import _lib as L
 __all__ = ["CWError", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
            "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
-           "step_attention", "step_workspace_bytes", "ceiling_mfma_bf16", "ceiling_stream_read",
+           "step_attention", "step_workspace_bytes", "check_block_table", "ceiling_mfma_bf16", "ceiling_stream_read",
            "ceiling_stream_copy"]
 
 
@@ -268,6 +268,20 @@ def decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, 
         hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out), _dptr(lse),
         _dptr(workspace), workspace.numel(), _stream()))
     return out
+
+
+def check_block_table(block_table, prefix_lens, suffix_lens, num_pages: int, page_size: int,
+                      workspace=None) -> np.ndarray:
+    """Per sequence, the number of block-table entries a call with these lengths
+    would read that lie outside [0, num_pages) (waits for the result)."""
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    bad = torch.empty(max(len(lp), 1), dtype=torch.int32, device=block_table.device)
+    if workspace is None:
+        workspace = _workspace(write_pages_workspace_bytes(len(lp)), block_table.device, None)
+    _check(library().cw_check_block_table(
+        _dptr(block_table), block_table.shape[1], int(num_pages), _ptr(lp), _ptr(ls), len(lp),
+        int(page_size), _dptr(bad), _dptr(workspace), workspace.numel(), _stream()))
+    return bad[:len(lp)].cpu().numpy()
 
 
 # measured ceilings (include/cw_ceiling.h): not part of the attention path

@@ -45,6 +45,7 @@ SIGNATURES = {
     "cw_decode_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
                                       _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
                                       _vp, _sz, _vp]),
+    "cw_check_block_table": (C.c_int, [_vp, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _sz, _vp]),
     "cw_set_tuning": (C.c_int, [C.c_int, _i32]),
     "cw_set_timing_events": (C.c_int, [_vp, _vp]),
     "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),

@@ -621,6 +621,37 @@ size_t cw_write_pages_workspace_bytes(int32_t num_seqs) {
   return std::max<size_t>(256, (size_t(num_seqs) * sizeof(SeqInfo) + 255) & ~size_t(255));
 }
 
+cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, int32_t num_pages,
+                                 const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
+                                 int32_t num_seqs, int32_t page_size, int32_t* bad_per_seq,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  cw_status_t s = check_shape(num_seqs, 1, 1, 64, page_size);
+  if (s != CW_OK) return s;
+  if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
+  s = check_lens(prefix_lens_h, suffix_lens_h, num_seqs, bt_stride, page_size, 1, 1, 64, true);
+  if (s != CW_OK) return s;
+  if (num_seqs == 0) return CW_OK;
+  if (!block_table || !bad_per_seq) return fail(CW_ERR_NULL, "block_table and bad_per_seq are required");
+  if ((reinterpret_cast<uintptr_t>(block_table) & 3u) || (reinterpret_cast<uintptr_t>(bad_per_seq) & 3u))
+    return fail(CW_ERR_ALIGN, "block_table and bad_per_seq must be 4-byte aligned");
+  if (!aligned16(workspace)) return fail(CW_ERR_ALIGN, "workspace must be 16-byte aligned");
+  const size_t need = cw_write_pages_workspace_bytes(num_seqs);
+  if (workspace == nullptr || workspace_bytes < need)
+    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  std::vector<SeqInfo> seqs(num_seqs);
+  int64_t cu = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), b};
+    cu += suffix_lens_h[b];
+  }
+  s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
+  if (s != CW_OK) return s;
+  const hipError_t e = launch_check_table(block_table, bt_stride, num_pages,
+                                          static_cast<const SeqInfo*>(workspace), num_seqs,
+                                          page_size, bad_per_seq, stream);
+  return e == hipSuccess ? CW_OK : hip_fail(e, "check_table kernel launch");
+}
+
 cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                               const float* k_scale, const float* v_scale,
                               const int32_t* block_table, int32_t bt_stride, int32_t num_pages,

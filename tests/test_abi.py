@@ -226,3 +226,26 @@ def test_ceiling_calls_reject_before_any_gpu_work():
     assert L_.cw_ceiling_stream_copy(16, None, 1024, None) == L.CW_ERR_NULL
     assert L_.cw_ceiling_stream_copy(4096, 4096 + 512, 1024, None) == L.CW_ERR_UNSUPPORTED
     assert b"overlap" in L_.cw_last_error_message()
+
+
+def test_check_block_table_rejects_before_any_gpu_work():
+    L_ = lib()
+    lp = np.array([10, 20], dtype=np.int32)
+    ls = np.array([5, 6], dtype=np.int32)
+
+    def call(bt=FAKE, stride=4, num_pages=100, lp=lp, ls=ls, page=16, bad=FAKE, ws=FAKE,
+             ws_bytes=1 << 20):
+        return L_.cw_check_block_table(bt, stride, num_pages, lp.ctypes.data, ls.ctypes.data,
+                                       len(lp), page, bad, ws, ws_bytes, None)
+
+    assert call(bt=None) == L.CW_ERR_NULL
+    assert call(bad=None) == L.CW_ERR_NULL
+    assert call(page=32) == L.CW_ERR_UNSUPPORTED
+    assert call(num_pages=-1) == L.CW_ERR_BAD_LENS
+    assert call(lp=np.array([60, 0], dtype=np.int32)) == L.CW_ERR_BAD_LENS  # 65 > 4 * 16
+    assert call(ls=np.array([-1, 0], dtype=np.int32)) == L.CW_ERR_BAD_LENS
+    assert call(bt=FAKE + 2) == L.CW_ERR_ALIGN
+    assert call(ws=FAKE + 4) == L.CW_ERR_ALIGN
+    assert call(ws_bytes=16) == L.CW_ERR_WORKSPACE
+    assert call(ws=None) == L.CW_ERR_WORKSPACE
+    assert L_.cw_last_error_message()
