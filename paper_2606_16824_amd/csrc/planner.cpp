@@ -227,6 +227,15 @@ ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32
     chunk = tiles * keys_per_tile;
   }
   chunk = std::min(max_chunk, std::max(unit, (chunk + unit - 1) / unit * unit));
+  // Longest chunks first so that short tails fill in at the end: every chunk but
+  // the last of a (sequence, kv head) has the full length, so the order is the
+  // full-length chunks in build order, then the shorter last chunks by length
+  // (stable), the same as a stable sort of all items by length.
+  int64_t n_items = 0;
+  for (int32_t b = 0; b < num_seqs; ++b) n_items += (int64_t(prefix_lens[b]) + chunk) / chunk;
+  plan.items.reserve(size_t(n_items * num_kv_heads));
+  std::vector<WorkItem> tails;
+  tails.reserve(size_t(num_seqs) * num_kv_heads);
   for (int32_t b = 0; b < num_seqs; ++b) {
     const int64_t n = int64_t(prefix_lens[b]) + 1;  // keys including the new one
     const int64_t n_c = (n + chunk - 1) / chunk;
@@ -237,16 +246,18 @@ ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32
         plan.groups.push_back(CombineGroup{b, h, 0, gqa_group, part0, static_cast<int32_t>(n_c), 0, 0});
         plan.n_parts += n_c;
       }
-      for (int64_t c = 0; c < n_c; ++c)
-        plan.items.push_back(WorkItem{b, h, 0, static_cast<int32_t>(c * chunk),
-                                      static_cast<int32_t>(std::min(n, (c + 1) * chunk)),
-                                      n_c > 1 ? static_cast<int32_t>(part0 + c) : -1, gqa_group, 0});
+      for (int64_t c = 0; c < n_c; ++c) {
+        const WorkItem it{b, h, 0, static_cast<int32_t>(c * chunk),
+                          static_cast<int32_t>(std::min(n, (c + 1) * chunk)),
+                          n_c > 1 ? static_cast<int32_t>(part0 + c) : -1, gqa_group, 0};
+        (it.kv_end - it.kv_begin == chunk ? plan.items : tails).push_back(it);
+      }
     }
   }
-  // longest chunks first so that short tails fill in at the end
-  std::stable_sort(plan.items.begin(), plan.items.end(), [](const WorkItem& a, const WorkItem& c) {
+  std::stable_sort(tails.begin(), tails.end(), [](const WorkItem& a, const WorkItem& c) {
     return (a.kv_end - a.kv_begin) > (c.kv_end - c.kv_begin);
   });
+  plan.items.insert(plan.items.end(), tails.begin(), tails.end());
   layout_workspace(plan, head_dim);
   return plan;
 }
