@@ -219,10 +219,19 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
     lib.cw_set_timing_events(None, None)
     ms = t_start.elapsed_time(t_stop) / steps
     kern = np.array([a.elapsed_time(b) for a, b in zip(k_starts, k_stops)])
+    # host cost of issuing one step (validation, planning, plan upload, launches)
+    # with an idle queue, so that nothing waits on the GPU
+    host = []
+    for _ in range(20):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        step()
+        host.append(time.perf_counter() - t0)
+    torch.cuda.synchronize()
     kernel = "decode_kernel" if decode else KERNEL_SOURCES[s.kv_dtype][0]
     res = {"spec": s, "workload": w, "ms": ms, "kern_ms": float(kern.mean()),
            "kern_ms_median": float(np.median(kern)), "kern_ms_min": float(kern.min()),
-           "kernel": kernel}
+           "host_us": float(np.median(host)) * 1e6, "kernel": kernel}
     if cold_steps > 0:
         # outside the kernel's events: before each step, 1 GiB of another buffer is
         # read so that the 256 MB memory-side cache (and every L2) holds none of the
@@ -401,6 +410,7 @@ def main():
                              else "cw_step_attention"),
                    "tflop_per_step": round(s.flops() / 1e12, 5), "seed": s.seed},
         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
+        "host_us_per_step": round(res["host_us"], 1),
         "roofline": roof,
     }
     if ceil is not None:
@@ -416,7 +426,8 @@ def main():
             "frac_hbm_peak": round(nbytes / (d["kern_ms"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "algorithmic_bytes": nbytes, "traffic": measured_traffic("decode", "decode"),
             "kernel": d["kernel"], "kernel_ms": round(d["kern_ms"], 5),
-            "kernel_ms_median": round(d["kern_ms_median"], 5)}
+            "kernel_ms_median": round(d["kern_ms_median"], 5),
+            "host_us_per_step": round(d["host_us"], 1)}
         if "cold_kern_ms_median" in d:
             result["decode"]["cold_kernel_GB_s"] = round(
                 nbytes / (d["cold_kern_ms_median"] * 1e-3) / 1e9, 1)
