@@ -107,7 +107,10 @@ void device_shape(int32_t* cus, int32_t* xcds) {
 // Copies `bytes` of host data to `dst` on `stream` through a pinned staging
 // slot, so that the copy is asynchronous and the caller's host buffer can be
 // reused at once.  A slot is reused only after its previous copy completed.
-cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
+// `fill(host)` writes the `bytes` bytes into the slot (the plan is packed there
+// directly, without an intermediate buffer).
+template <class Fill>
+cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill) {
   if (bytes == 0) return CW_OK;
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
@@ -135,13 +138,17 @@ cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream)
     if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
     s.cap = cap;
   }
-  std::memcpy(s.host, src, bytes);
+  fill(static_cast<uint8_t*>(s.host));
   e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
   e = hipEventRecord(s.ev, stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   s.pending = true;
   return CW_OK;
+}
+
+cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
+  return upload_fill(bytes, dst, stream, [&](uint8_t* h) { std::memcpy(h, src, bytes); });
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -326,10 +333,8 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
 
-  std::vector<uint8_t> meta(plan.meta_bytes);
-  pack_plan_meta(plan, meta.data());
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  s = upload(meta.data(), meta.size(), ws, stream);
+  s = upload_fill(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); });
   if (s != CW_OK) return s;
 
   ExtendParams p{};
@@ -497,13 +502,14 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   const StepPlan sp = make_step_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype);
   if (workspace == nullptr || workspace_bytes < sp.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, sp.total_bytes);
-  std::vector<uint8_t> meta(sp.meta_bytes, 0);
-  std::copy(reinterpret_cast<const uint8_t*>(sp.seqs.data()),
-            reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), meta.data());
-  if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, meta.data() + sp.off_ext_meta);
-  if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, meta.data() + sp.off_dec_meta);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  s = upload(meta.data(), meta.size(), ws, stream);
+  s = upload_fill(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
+    std::fill(h, h + sp.off_ext_meta, uint8_t(0));
+    std::copy(reinterpret_cast<const uint8_t*>(sp.seqs.data()),
+              reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), h);
+    if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, h + sp.off_ext_meta);
+    if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, h + sp.off_dec_meta);
+  });
   if (s != CW_OK) return s;
 
   auto common = [&](ExtendParams& p) {
