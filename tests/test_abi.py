@@ -249,3 +249,21 @@ def test_check_block_table_rejects_before_any_gpu_work():
     assert call(ws_bytes=16) == L.CW_ERR_WORKSPACE
     assert call(ws=None) == L.CW_ERR_WORKSPACE
     assert L_.cw_last_error_message()
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    # no fallback path: with the library absent, the first call raises
+    import subprocess
+    import sys
+    code = ("import paper_2606_16824_amd as cw\n"
+            "try:\n"
+            "    cw.write_pages_workspace_bytes(1)\n"
+            "except RuntimeError as e:\n"
+            "    print('raised:', e)\n"
+            "else:\n"
+            "    print('no error')\n")
+    env = dict(os.environ, CW_LIBRARY=str(tmp_path / "absent" / "libcw.so"))
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], env=env, cwd=root, capture_output=True,
+                       text=True, timeout=300)
+    assert "raised:" in r.stdout and "not found" in r.stdout, r.stdout + r.stderr
