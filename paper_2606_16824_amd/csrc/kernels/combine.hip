@@ -7,6 +7,7 @@ namespace cw {
 namespace {
 
 constexpr float kLn2 = 0.69314718055994531f;
+constexpr int kFewParts = 4;  // the one-slice merge loads up to this many partials at once
 
 // Merges the split-K partials of query rows: weights 2^(m_c - max m),
 // O = sum w_c O_c / sum w_c l_c.  A workgroup of 256 lanes covers ROWS rows;
@@ -30,16 +31,47 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
   float m = -INFINITY, L = 0.f, acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  for (int c = slice; active && c < cg.n_parts; c += SLICES) {
-    const size_t pr = size_t(cg.part0 + c) * p.part_rows + lr;
-    const float mc = p.part_ml[pr * 2], lc = p.part_ml[pr * 2 + 1];
-    const float m_new = fmaxf(m, mc);
-    const float a = exp2f(m - m_new), w = exp2f(mc - m_new);
-    const float* po = p.part_o + pr * D + d0;
-    L = L * a + w * lc;
+  if (SLICES == 1 && active && cg.n_parts <= kFewParts) {
+    // few partials (at most kFewParts): every load is issued before the first
+    // use, so a row waits for one memory latency instead of one per partial
+    float mc[kFewParts], lc[kFewParts], oc[kFewParts][PER];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] = acc[e] * a + w * po[e];
-    m = m_new;
+    for (int c = 0; c < kFewParts; ++c) {
+      mc[c] = -INFINITY;
+      lc[c] = 0.f;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) oc[c][e] = 0.f;
+      if (c < cg.n_parts) {
+        const size_t pr = size_t(cg.part0 + c) * p.part_rows + lr;
+        const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + pr * 2);
+        mc[c] = ml.x;
+        lc[c] = ml.y;
+        const float* po = p.part_o + pr * D + d0;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) oc[c][e] = po[e];
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < kFewParts; ++c) m = fmaxf(m, mc[c]);
+#pragma unroll
+    for (int c = 0; c < kFewParts; ++c) {
+      const float w = c < cg.n_parts ? exp2f(mc[c] - m) : 0.f;
+      L += w * lc[c];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += w * oc[c][e];
+    }
+  } else {
+    for (int c = slice; active && c < cg.n_parts; c += SLICES) {
+      const size_t pr = size_t(cg.part0 + c) * p.part_rows + lr;
+      const float mc = p.part_ml[pr * 2], lc = p.part_ml[pr * 2 + 1];
+      const float m_new = fmaxf(m, mc);
+      const float a = exp2f(m - m_new), w = exp2f(mc - m_new);
+      const float* po = p.part_o + pr * D + d0;
+      L = L * a + w * lc;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] = acc[e] * a + w * po[e];
+      m = m_new;
+    }
   }
   if (SLICES > 1) {
 #pragma unroll
