@@ -55,6 +55,7 @@ constexpr int kStagingSlots = 8;
 
 struct StagingSlot {
   void* host = nullptr;
+  void* dev = nullptr;  // the same pinned memory as the device addresses it
   size_t cap = 0;
   hipEvent_t ev = nullptr;
   bool pending = false;
@@ -136,11 +137,17 @@ cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill
     const size_t cap = std::max<size_t>(bytes, size_t(1) << 20);
     e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
     if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
+    e = hipHostGetDevicePointer(&s.dev, s.host, 0);
+    if (e != hipSuccess) {
+      (void)hipHostFree(s.host);
+      s.host = nullptr;
+      return hip_fail(e, "hipHostGetDevicePointer");
+    }
     s.cap = cap;
   }
   fill(static_cast<uint8_t*>(s.host));
-  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  e = launch_stage_copy(s.dev, dst, bytes, stream);
+  if (e != hipSuccess) return hip_fail(e, "plan upload kernel launch");
   e = hipEventRecord(s.ev, stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   s.pending = true;

@@ -61,15 +61,41 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
       for (int e = 0; e < PER; ++e) acc[e] += w * oc[c][e];
     }
   } else {
-    for (int c = slice; active && c < cg.n_parts; c += SLICES) {
-      const size_t pr = size_t(cg.part0 + c) * p.part_rows + lr;
-      const float mc = p.part_ml[pr * 2], lc = p.part_ml[pr * 2 + 1];
-      const float m_new = fmaxf(m, mc);
-      const float a = exp2f(m - m_new), w = exp2f(mc - m_new);
-      const float* po = p.part_o + pr * D + d0;
-      L = L * a + w * lc;
+    // many partials: each slice takes its partials kFewParts at a time, all of
+    // a group's loads issued before the group is merged into the running state
+    for (int c0 = slice; active && c0 < cg.n_parts; c0 += kFewParts * SLICES) {
+      float mc[kFewParts], lc[kFewParts], oc[kFewParts][PER];
 #pragma unroll
-      for (int e = 0; e < PER; ++e) acc[e] = acc[e] * a + w * po[e];
+      for (int k = 0; k < kFewParts; ++k) {
+        const int c = c0 + k * SLICES;
+        mc[k] = -INFINITY;
+        lc[k] = 0.f;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) oc[k][e] = 0.f;
+        if (c < cg.n_parts) {
+          const size_t pr = size_t(cg.part0 + c) * p.part_rows + lr;
+          const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + pr * 2);
+          mc[k] = ml.x;
+          lc[k] = ml.y;
+          const float* po = p.part_o + pr * D + d0;
+#pragma unroll
+          for (int e = 0; e < PER; ++e) oc[k][e] = po[e];
+        }
+      }
+      float m_new = m;
+#pragma unroll
+      for (int k = 0; k < kFewParts; ++k) m_new = fmaxf(m_new, mc[k]);
+      const float a = exp2f(m - m_new);
+      L *= a;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] *= a;
+#pragma unroll
+      for (int k = 0; k < kFewParts; ++k) {
+        const float w = c0 + k * SLICES < cg.n_parts ? exp2f(mc[k] - m_new) : 0.f;
+        L += w * lc[k];
+#pragma unroll
+        for (int e = 0; e < PER; ++e) acc[e] += w * oc[k][e];
+      }
       m = m_new;
     }
   }

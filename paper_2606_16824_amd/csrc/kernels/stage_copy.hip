@@ -1,0 +1,38 @@
+// Plan upload: copies a call's plan (per-sequence info, work items, merge
+// groups) from the library's pinned staging slot to the caller's workspace.
+// The device reads the pinned host memory directly over the host link, on the
+// call's stream, so the upload is one small kernel in the same queue as the
+// attention kernels (a copy engine would cost a hand-off between queues).
+#include <hip/hip_runtime.h>
+
+#include "../cw_internal.h"
+
+namespace cw {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void stage_copy_kernel(const uint8_t* src, uint8_t* dst,
+                                                              int64_t bytes) {
+  const int64_t n16 = bytes / 16;
+  const int64_t stride = int64_t(gridDim.x) * kThreads;
+  const int64_t first = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  for (int64_t i = first; i < n16; i += stride)
+    reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
+  if (first < bytes - n16 * 16) dst[n16 * 16 + first] = src[n16 * 16 + first];
+}
+
+}  // namespace
+
+hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  const int64_t n16 = int64_t(bytes / 16);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n16 + kThreads - 1) / kThreads, 1024));
+  hipLaunchKernelGGL(stage_copy_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream,
+                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), int64_t(bytes));
+  return hipGetLastError();
+}
+
+}  // namespace cw
