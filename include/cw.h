@@ -46,10 +46,14 @@
  * later synchronisation.  cw_last_error_message() returns a thread-local
  * description of the last error.  No call throws or aborts.
  *
+ * Aliasing: the attention calls reject (CW_ERR_ALIAS) an out or lse range that
+ * overlaps q, k_new, v_new, the pools, the fp8 scales, the block table, the
+ * workspace or each other (ranges from the shapes and lengths of the call).
+ *
  * Preconditions the library does not check (checking would need device reads;
  * cw_check_block_table checks the first on request): page ids < num_pages;
  * write slots of different sequences are disjoint; pages shared between
- * sequences lie inside every sharer's prefix; out and lse alias no input.
+ * sequences lie inside every sharer's prefix.
  */
 #ifndef CW_H_
 #define CW_H_
@@ -71,6 +75,7 @@ typedef enum {
   CW_ERR_ALIGN = 4,       /* a tensor or workspace pointer not 16-byte aligned */
   CW_ERR_WORKSPACE = 5,   /* workspace_bytes smaller than the matching *_workspace_bytes() */
   CW_ERR_HIP = 6,         /* a HIP runtime call failed while enqueuing */
+  CW_ERR_ALIAS = 7,       /* out or lse overlaps an input, the workspace or each other */
   CW_STATUS_RANGE_MIN_ = -2147483647 - 1,
   CW_STATUS_RANGE_MAX_ = 2147483647
 } cw_status_t;

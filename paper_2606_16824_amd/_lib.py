@@ -10,7 +10,8 @@ import os
 LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(
     os.path.dirname(os.path.abspath(__file__)), "libcw.so")
 
-CW_OK, CW_ERR_NULL, CW_ERR_UNSUPPORTED, CW_ERR_BAD_LENS, CW_ERR_ALIGN, CW_ERR_WORKSPACE, CW_ERR_HIP = range(7)
+(CW_OK, CW_ERR_NULL, CW_ERR_UNSUPPORTED, CW_ERR_BAD_LENS, CW_ERR_ALIGN, CW_ERR_WORKSPACE, CW_ERR_HIP,
+ CW_ERR_ALIAS) = range(8)
 CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1
 CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS = 0, 1
 

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -156,6 +157,53 @@ cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill
 
 cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
   return upload_fill(bytes, dst, stream, [&](uint8_t* h) { std::memcpy(h, src, bytes); });
+}
+
+// A byte range of one argument, for the aliasing check.
+struct Span {
+  const void* p;
+  size_t bytes;
+  const char* name;
+};
+
+bool overlap(const Span& a, const Span& b) {
+  if (a.p == nullptr || b.p == nullptr || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// out / lse must not overlap any input, the workspace or each other.
+cw_status_t check_no_alias(std::initializer_list<Span> outputs, std::initializer_list<Span> inputs) {
+  for (const Span* o = outputs.begin(); o != outputs.end(); ++o) {
+    for (const Span& i : inputs)
+      if (overlap(*o, i)) return fail(CW_ERR_ALIAS, "%s overlaps %s", o->name, i.name);
+    for (const Span* o2 = o + 1; o2 != outputs.end(); ++o2)
+      if (overlap(*o, *o2)) return fail(CW_ERR_ALIAS, "%s overlaps %s", o->name, o2->name);
+  }
+  return CW_OK;
+}
+
+// The aliasing check of an attention call (extend, decode or step).
+cw_status_t check_attention_alias(const void* q, const void* k_new, const void* v_new,
+                                  const void* k_pool, const void* v_pool, const float* k_scale,
+                                  const float* v_scale, const int32_t* block_table,
+                                  int32_t bt_stride, int32_t num_pages, int32_t num_seqs,
+                                  int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                  int32_t page_size, cw_kv_dtype_t kv_dtype, int64_t total,
+                                  const void* out, const float* lse, const void* workspace,
+                                  size_t workspace_bytes) {
+  const size_t hq = size_t(num_kv_heads) * gqa_group;
+  const size_t rows_q = size_t(total) * hq * head_dim * 2;
+  const size_t rows_kv = size_t(total) * num_kv_heads * head_dim * 2;
+  const size_t elem = kv_dtype == CW_KV_FP8_E4M3FN ? 1 : 2;
+  const size_t pool = size_t(num_pages) * num_kv_heads * page_size * head_dim * elem;
+  const size_t scales = kv_dtype == CW_KV_FP8_E4M3FN ? size_t(num_pages) * num_kv_heads * 4 : 0;
+  return check_no_alias({{out, rows_q, "out"}, {lse, size_t(total) * hq * 4, "lse"}},
+                        {{q, rows_q, "q"}, {k_new, rows_kv, "k_new"}, {v_new, rows_kv, "v_new"},
+                         {k_pool, pool, "k_pool"}, {v_pool, pool, "v_pool"},
+                         {k_scale, scales, "k_scale"}, {v_scale, scales, "v_scale"},
+                         {block_table, size_t(num_seqs) * bt_stride * 4, "block_table"},
+                         {workspace, workspace_bytes, "workspace"}});
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -339,6 +387,10 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
                            : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype);
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
+  s = check_attention_alias(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table,
+                            bt_stride, num_pages, num_seqs, num_kv_heads, gqa_group, head_dim,
+                            page_size, kv_dtype, total, out, lse, workspace, workspace_bytes);
+  if (s != CW_OK) return s;
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   s = upload_fill(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); });
@@ -509,6 +561,10 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   const StepPlan sp = make_step_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype);
   if (workspace == nullptr || workspace_bytes < sp.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, sp.total_bytes);
+  s = check_attention_alias(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table,
+                            bt_stride, num_pages, num_seqs, num_kv_heads, gqa_group, head_dim,
+                            page_size, kv_dtype, total, out, lse, workspace, workspace_bytes);
+  if (s != CW_OK) return s;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   s = upload_fill(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
     std::fill(h, h + sp.off_ext_meta, uint8_t(0));
@@ -869,6 +925,7 @@ const char* cw_status_string(cw_status_t status) {
     case CW_ERR_ALIGN: return "CW_ERR_ALIGN: misaligned pointer";
     case CW_ERR_WORKSPACE: return "CW_ERR_WORKSPACE: workspace too small";
     case CW_ERR_HIP: return "CW_ERR_HIP: HIP runtime error";
+    case CW_ERR_ALIAS: return "CW_ERR_ALIAS: an output overlaps an input or the workspace";
     default: break;
   }
   return "unknown cw_status_t";

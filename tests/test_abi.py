@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in range(7):
+    for s in range(8):
         assert lib().cw_status_string(s).decode().startswith("CW_")
 
 
@@ -267,3 +267,36 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
     r = subprocess.run([sys.executable, "-c", code], env=env, cwd=root, capture_output=True,
                        text=True, timeout=300)
     assert "raised:" in r.stdout and "not found" in r.stdout, r.stdout + r.stderr
+
+
+# distinct, far-apart fake ranges; sizes for the default call: 11 rows x 8 heads x 128 x 2 B
+_BASES = dict(q=0x10000000, k_new=0x20000000, v_new=0x30000000, k_pool=0x40000000,
+              v_pool=0x50000000, block_table=0x60000000, out=0x70000000, workspace=0x80000000)
+_ROWS_Q = 11 * 8 * 128 * 2
+
+
+@pytest.mark.parametrize("fused", [False, True, "step"])
+@pytest.mark.parametrize("over,culprit", [
+    (dict(out=_BASES["q"] + 16), "q"),
+    (dict(out=_BASES["q"] - _ROWS_Q + 16), "q"),                 # tail of out over the head of q
+    (dict(out=_BASES["k_pool"] + 4096), "k_pool"),
+    (dict(out=_BASES["block_table"] - 64), "block_table"),
+    (dict(out=_BASES["workspace"] + (1 << 20)), "workspace"),
+    (dict(lse=_BASES["v_new"] + 4), "v_new"),
+    (dict(lse=_BASES["out"] + 512), "lse"),                       # out and lse overlap
+])
+def test_outputs_that_alias_inputs_are_rejected(fused, over, culprit):
+    args = dict(_BASES, workspace_bytes=1 << 24)
+    args.update(over)
+    assert _extend(fused=fused, **args) == L.CW_ERR_ALIAS
+    msg = lib().cw_last_error_message().decode()
+    assert culprit in msg and "overlaps" in msg, msg
+
+
+def test_decode_output_alias_is_rejected():
+    lp = np.array([10, 20], dtype=np.int32)
+    r = lib().cw_decode_attention(
+        _BASES["q"], _BASES["k_new"], _BASES["v_new"], _BASES["k_pool"], _BASES["v_pool"], None,
+        None, _BASES["block_table"], 4, 100, lp.ctypes.data, 2, 2, 4, 128, 16, 0.088, 0,
+        _BASES["k_new"] + 128, None, _BASES["workspace"], 1 << 24, None)
+    assert r == L.CW_ERR_ALIAS and b"k_new" in lib().cw_last_error_message()
