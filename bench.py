@@ -65,6 +65,9 @@ def parse():
                          "separately; 0 disables)")
     ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
                     help="skip the measured MFMA and HBM ceilings")
+    ap.add_argument("--ceilings-only", action="store_true",
+                    help="only measure the MFMA and HBM ceilings, print them as one JSON line "
+                         "and exit")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (for "
                          "scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -258,8 +261,11 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
 
 def measure_ceilings(reps: int = 5):
     """What the chip sustains on each roofline's unit of work with nothing else in
-    the way: a matrix-core loop (bf16 MFMA, no memory traffic), a streaming read and
-    a streaming copy of 4 GiB (each launch median over `reps`)."""
+    the way: a matrix-core loop (bf16 MFMA, no memory traffic) with operand bits like
+    real data (the ceiling attention is priced against) and with a few repeated bit
+    patterns (less power per MFMA, so a higher clock), a streaming read and a streaming
+    copy of 4 GiB (each launch median over `reps`).  For context also the vendor
+    library's bf16 GEMM (torch.matmul, 8192^3, N(0,1) operands)."""
     import torch
     import paper_2606_16824_amd as cwlib
 
@@ -279,20 +285,30 @@ def measure_ceilings(reps: int = 5):
     wgs, iters = 512, 40000  # two workgroups per CU, all resident at once: no tail
     sink = torch.empty(wgs * 8, dtype=torch.float32, device="cuda")
     flops = float(wgs) * 8 * iters * 131072
-    mfma_ms = med(lambda: cwlib.ceiling_mfma_bf16(wgs, iters, sink))
+    mfma_ms = med(lambda: cwlib.ceiling_mfma_bf16(wgs, iters, sink, random=True))
+    mfma_low_ms = med(lambda: cwlib.ceiling_mfma_bf16(wgs, iters, sink, random=False))
+    n = 8192
+    g = torch.Generator(device="cuda").manual_seed(7)
+    a = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", generator=g).to(torch.bfloat16)
+    gemm_ms = med(lambda: torch.matmul(a, b))
+    del a, b
     buf = torch.empty(4 << 30, dtype=torch.uint8, device="cuda").fill_(3)
     dst = torch.empty_like(buf)
     rsink = torch.empty(16384, dtype=torch.int32, device="cuda")
     read_ms = med(lambda: cwlib.ceiling_stream_read(buf, rsink))
     copy_ms = med(lambda: cwlib.ceiling_stream_copy(buf, dst))
-    n = buf.numel()
+    nb = buf.numel()
     del buf, dst
     return {"mfma_bf16_TFLOP_s": round(flops / (mfma_ms * 1e-3) / 1e12, 1),
-            "hbm_read_GB_s": round(n / (read_ms * 1e-3) / 1e9, 1),
-            "hbm_copy_GB_s": round(2 * n / (copy_ms * 1e-3) / 1e9, 1),
+            "mfma_bf16_low_entropy_TFLOP_s": round(flops / (mfma_low_ms * 1e-3) / 1e12, 1),
+            "vendor_gemm_bf16_TFLOP_s": round(2.0 * n ** 3 / (gemm_ms * 1e-3) / 1e12, 1),
+            "hbm_read_GB_s": round(nb / (read_ms * 1e-3) / 1e9, 1),
+            "hbm_copy_GB_s": round(2 * nb / (copy_ms * 1e-3) / 1e9, 1),
             "kernels": "mfma_loop_kernel (512 workgroups of 8 waves, 4 independent 32x32x16 bf16 "
-                       "chains per wave), stream_read_kernel / stream_copy_kernel (4 GiB, 16 B "
-                       "nontemporal loads, 4 in flight per lane, 16384 workgroups)"}
+                       "chains per wave; random operand bits, and low-entropy patterns), torch.matmul "
+                       "bf16 8192^3 on N(0,1) data, stream_read_kernel / stream_copy_kernel (4 GiB, "
+                       "16 B nontemporal loads, 4 in flight per lane, 16384 workgroups)"}
 
 
 def run_swap(reps: int = 10):
@@ -345,6 +361,9 @@ def main():
     args = parse()
     if args.calibrate_copy_mib:
         calibrate_copy(args.calibrate_copy_mib)
+        return
+    if args.ceilings_only:
+        print(json.dumps({"ceilings": measure_ceilings()}), flush=True)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))

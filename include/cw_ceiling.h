@@ -9,7 +9,9 @@
  * ceiling:
  *   - a matrix-core loop: every wave issues independent
  *     v_mfma_f32_32x32x16_bf16 chains and touches no memory (the shader clock
- *     under sustained MFMA load sets the result);
+ *     under sustained MFMA load sets the result, and that clock depends on the
+ *     operand bits: the chip is power-limited, and operands whose bits toggle
+ *     like real data draw more power per MFMA than a few repeated patterns);
  *   - a streaming read and a streaming copy of a device buffer in 16-byte
  *     pieces by every lane, grid-stride, many loads in flight per lane.
  * They are not part of the attention path.
@@ -33,16 +35,36 @@
 extern "C" {
 #endif
 
+/* Operand bits of the matrix-core loop. */
+typedef enum {
+  /* a = ((lane + e) & 7) / 1024, b = ((3 lane + e) & 7) / 1024 for element e
+   * of a lane's eight: eight bit patterns in all, the same for every chain. */
+  CW_CEILING_LOW_ENTROPY = 0,
+  /* Every element of every chain's A and B is a bf16 with a random sign, a
+   * random 7-bit mantissa and a magnitude in [2^-4, 4) (the bit statistics of
+   * N(0,1) data), drawn from a 32-bit integer hash of its global lane and
+   * index: h(x) = x ^ x>>16, * 0x7feb352d, ^ >>15, * 0x846ca68b, ^ >>16 (all
+   * mod 2^32).  For chain c and element e of global lane g = 512 workgroup +
+   * thread, A's bits come from ha = h(64 g + 8 c + e), B's from
+   * h(ha ^ 0x9e3779b9); bits(u) = (u >> 31) << 15 | (123 + (u >> 8) % 6) << 7
+   * | (u & 127). */
+  CW_CEILING_RANDOM = 1,
+  CW_CEILING_RANGE_MIN_ = -2147483647 - 1, /* int32-sized enum (ABI) */
+  CW_CEILING_RANGE_MAX_ = 2147483647
+} cw_ceiling_operands_t;
+
 /* Matrix-core loop.  `workgroups` workgroups of eight wave64s, each wave
  * running `iters` rounds of four independent 32x32x16 bf16 MFMAs (4 x 32768
- * FLOPs per round).  Total FLOPs = workgroups * 8 * iters * 131072.  A grid
- * that the CUs hold at once (one or two workgroups per CU) measures the matrix
- * pipes; a larger one adds a tail.  `sink` (device, fp32 [workgroups * 8])
- * receives one accumulator element per wave so the loop cannot be removed.
- * CW_ERR_NULL for a NULL sink; CW_ERR_UNSUPPORTED unless 1 <= workgroups
- * <= 65536 and 1 <= iters <= 2^24. */
-cw_status_t cw_ceiling_mfma_bf16(int32_t workgroups, int32_t iters, float* sink,
-                                 hipStream_t stream);
+ * FLOPs per round), chain c accumulating A_c B_c every round.  Total FLOPs =
+ * workgroups * 8 * iters * 131072.  A grid that the CUs hold at once (one or
+ * two workgroups per CU) measures the matrix pipes; a larger one adds a tail.
+ * `sink` (device, fp32 [workgroups * 8]) receives, per wave, the sum over
+ * chains c = 0..3 of element (row c, column 0) of chain c's accumulator, so the
+ * loop cannot be removed.  CW_ERR_NULL for a NULL sink; CW_ERR_UNSUPPORTED
+ * unless 1 <= workgroups <= 65536, 1 <= iters <= 2^24 and `operands` is one of
+ * the values above. */
+cw_status_t cw_ceiling_mfma_bf16(int32_t workgroups, int32_t iters, cw_ceiling_operands_t operands,
+                                 float* sink, hipStream_t stream);
 
 /* Streaming read of `bytes` (a multiple of 16, > 0) from device buffer `src`
  * (16-byte aligned).  `sink` (device, uint32 [16384]) receives one XOR of

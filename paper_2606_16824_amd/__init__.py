@@ -286,9 +286,11 @@ def check_block_table(block_table, prefix_lens, suffix_lens, num_pages: int, pag
 
 # measured ceilings (include/cw_ceiling.h): not part of the attention path
 
-def ceiling_mfma_bf16(workgroups: int, iters: int, sink: torch.Tensor) -> float:
-    """Enqueues the matrix-core loop; returns the FLOPs it performs."""
-    _check(library().cw_ceiling_mfma_bf16(int(workgroups), int(iters), _dptr(sink), _stream()))
+def ceiling_mfma_bf16(workgroups: int, iters: int, sink: torch.Tensor, random: bool = True) -> float:
+    """Enqueues the matrix-core loop (random operand bits, or the low-entropy
+    patterns with `random=False`); returns the FLOPs it performs."""
+    kind = L.CW_CEILING_RANDOM if random else L.CW_CEILING_LOW_ENTROPY
+    _check(library().cw_ceiling_mfma_bf16(int(workgroups), int(iters), kind, _dptr(sink), _stream()))
     return float(workgroups) * 8 * iters * 131072
 
 

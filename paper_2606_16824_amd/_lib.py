@@ -14,6 +14,7 @@ LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(
  CW_ERR_ALIAS) = range(8)
 CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1
 CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS = 0, 1
+CW_CEILING_LOW_ENTROPY, CW_CEILING_RANDOM = 0, 1
 
 _i32p = C.POINTER(C.c_int32)
 _fp = C.POINTER(C.c_float)
@@ -54,7 +55,7 @@ SIGNATURES = {
     "cw_last_error_message": (C.c_char_p, []),
     "cw_version": (_i32, []),
     # include/cw_ceiling.h (measurement kernels)
-    "cw_ceiling_mfma_bf16": (C.c_int, [_i32, _i32, _vp, _vp]),
+    "cw_ceiling_mfma_bf16": (C.c_int, [_i32, _i32, _i32, _vp, _vp]),
     "cw_ceiling_stream_read": (C.c_int, [_vp, _sz, _vp, _vp]),
     "cw_ceiling_stream_copy": (C.c_int, [_vp, _vp, _sz, _vp]),
     # include/cw_policy.h (host-only)

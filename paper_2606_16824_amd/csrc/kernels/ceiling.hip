@@ -20,24 +20,51 @@ constexpr int kStreamGrid = 16384;
 constexpr int kStreamThreads = 256;
 constexpr int kUnroll = 4;  // 16-byte loads in flight per lane per round
 
+// 32-bit integer hash (the two-multiply avalanche mix); all arithmetic mod 2^32.
+__device__ inline uint32_t mix32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+// A bf16 with a random sign and mantissa and a magnitude in [2^-4, 4).
+__device__ inline __bf16 random_bf16(uint32_t u) {
+  const uint32_t bits = ((u >> 31) << 15) | ((123u + (u >> 8) % 6u) << 7) | (u & 127u);
+  return __builtin_bit_cast(__bf16, static_cast<uint16_t>(bits));
+}
+
 // Eight waves (two per SIMD), four independent accumulator chains per wave:
 // an MFMA's result is needed again only four issues later, so the matrix pipe
-// never waits on a dependency.  Operands come from the lane id, so nothing is
-// known at compile time; the values stay small (no overflow over 2^24 rounds).
-__global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* sink) {
+// never waits on a dependency.  Operands come from the lane id (never known at
+// compile time), either as eight repeated small patterns or as random bits per
+// chain; the accumulators stay finite over 2^24 rounds either way.
+__global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, int random, float* sink) {
   const int lane = threadIdx.x & 63;
-  bf16x8 a, b;
+  const uint32_t g = blockIdx.x * 512u + threadIdx.x;
+  bf16x8 a[4], b[4];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    a[e] = static_cast<__bf16>(float((lane + e) & 7) * (1.f / 1024.f));
-    b[e] = static_cast<__bf16>(float((lane * 3 + e) & 7) * (1.f / 1024.f));
+  for (int c = 0; c < 4; ++c) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (random) {
+        const uint32_t ha = mix32(64u * g + 8u * c + e);
+        a[c][e] = random_bf16(ha);
+        b[c][e] = random_bf16(mix32(ha ^ 0x9e3779b9u));
+      } else {
+        a[c][e] = static_cast<__bf16>(float((lane + e) & 7) * (1.f / 1024.f));
+        b[c][e] = static_cast<__bf16>(float((lane * 3 + e) & 7) * (1.f / 1024.f));
+      }
+    }
   }
   f32x16 c0 = f32x16{}, c1 = f32x16{}, c2 = f32x16{}, c3 = f32x16{};
   for (int i = 0; i < iters; ++i) {
-    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
-    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
-    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[0], c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1], b[1], c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[2], b[2], c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[3], b[3], c3, 0, 0, 0);
   }
   if (lane == 0) sink[blockIdx.x * 8 + (threadIdx.x >> 6)] = c0[0] + c1[1] + c2[2] + c3[3];
 }
@@ -110,13 +137,19 @@ cw_status_t check_stream_args(const void* src, const void* dst, size_t bytes) {
 
 extern "C" {
 
-cw_status_t cw_ceiling_mfma_bf16(int32_t workgroups, int32_t iters, float* sink,
-                                 hipStream_t stream) {
+cw_status_t cw_ceiling_mfma_bf16(int32_t workgroups, int32_t iters, cw_ceiling_operands_t operands,
+                                 float* sink, hipStream_t stream) {
   using namespace cw;
   if (sink == nullptr) return fail_msg(CW_ERR_NULL, "sink is NULL");
   if (workgroups < 1 || workgroups > 65536 || iters < 1 || iters > (1 << 24))
     return fail_msg(CW_ERR_UNSUPPORTED, "workgroups must be in [1, 65536], iters in [1, 2^24]");
-  hipLaunchKernelGGL(mfma_loop_kernel, dim3(workgroups), dim3(512), 0, stream, iters, sink);
+  int random = 0;
+  switch (operands) {
+    case CW_CEILING_LOW_ENTROPY: random = 0; break;
+    case CW_CEILING_RANDOM: random = 1; break;
+    default: return fail_msg(CW_ERR_UNSUPPORTED, "operands must be CW_CEILING_LOW_ENTROPY or CW_CEILING_RANDOM");
+  }
+  hipLaunchKernelGGL(mfma_loop_kernel, dim3(workgroups), dim3(512), 0, stream, iters, random, sink);
   return launched("mfma_loop_kernel");
 }
 

@@ -215,10 +215,13 @@ def test_empty_swap_is_a_no_op():
 
 def test_ceiling_calls_reject_before_any_gpu_work():
     L_ = lib()
-    assert L_.cw_ceiling_mfma_bf16(256, 10, None, None) == L.CW_ERR_NULL
-    assert L_.cw_ceiling_mfma_bf16(0, 10, 16, None) == L.CW_ERR_UNSUPPORTED
-    assert L_.cw_ceiling_mfma_bf16(256, 0, 16, None) == L.CW_ERR_UNSUPPORTED
-    assert L_.cw_ceiling_mfma_bf16(65537, 10, 16, None) == L.CW_ERR_UNSUPPORTED
+    R = L.CW_CEILING_RANDOM
+    assert L_.cw_ceiling_mfma_bf16(256, 10, R, None, None) == L.CW_ERR_NULL
+    assert L_.cw_ceiling_mfma_bf16(0, 10, R, 16, None) == L.CW_ERR_UNSUPPORTED
+    assert L_.cw_ceiling_mfma_bf16(256, 0, R, 16, None) == L.CW_ERR_UNSUPPORTED
+    assert L_.cw_ceiling_mfma_bf16(65537, 10, R, 16, None) == L.CW_ERR_UNSUPPORTED
+    for bad in (2, -1, 7):
+        assert L_.cw_ceiling_mfma_bf16(256, 10, bad, 16, None) == L.CW_ERR_UNSUPPORTED
     assert L_.cw_ceiling_stream_read(None, 1024, 16, None) == L.CW_ERR_NULL
     assert L_.cw_ceiling_stream_read(16, 0, 16, None) == L.CW_ERR_UNSUPPORTED
     assert L_.cw_ceiling_stream_read(24, 1024, 16, None) == L.CW_ERR_ALIGN
