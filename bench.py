@@ -65,6 +65,9 @@ def parse():
                          "separately; 0 disables)")
     ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
                     help="skip the measured MFMA and HBM ceilings")
+    ap.add_argument("--power-seconds", type=float, default=3.0,
+                    help="seconds of back-to-back steps (and of each MFMA loop) during which "
+                         "amd-smi samples socket power and GFX clocks; 0 disables")
     ap.add_argument("--ceilings-only", action="store_true",
                     help="only measure the MFMA and HBM ceilings, print them as one JSON line "
                          "and exit")
@@ -149,7 +152,101 @@ def cpu_baseline(w, target_s: float):
             "tok_s": n / dt}
 
 
-def run_workload(name: str, steps: int, warmup: int, separate: bool = False, cold_steps: int = 0):
+def _smi_json(args):
+    """JSON from a ROCm SMI tool, or None when it is missing or fails."""
+    import shutil
+    import subprocess
+    tool = shutil.which(args[0])
+    if tool is None:
+        return None
+    try:
+        r = subprocess.run([tool] + args[1:], capture_output=True, text=True, timeout=20)
+        return json.loads(r.stdout)
+    except (OSError, ValueError, subprocess.SubprocessError):
+        return None
+
+
+def _find(d, pred, out):
+    """Collects (key, value) pairs anywhere in nested dicts / lists for which pred(key) holds."""
+    if isinstance(d, dict):
+        for k, v in d.items():
+            if pred(str(k)):
+                out.append((str(k), v))
+            _find(v, pred, out)
+    elif isinstance(d, list):
+        for v in d:
+            _find(v, pred, out)
+    return out
+
+
+def _num(v):
+    if isinstance(v, dict):
+        v = v.get("value")
+    try:
+        return float(v)
+    except (TypeError, ValueError):
+        return None
+
+
+def power_cap_w():
+    """The board's power cap (W) as rocm-smi reports it, or None."""
+    d = _smi_json(["rocm-smi", "--showmaxpower", "--json"])
+    vals = [_num(v) for _, v in _find(d, lambda k: "Max Graphics Package Power" in k, [])]
+    vals = [v for v in vals if v]
+    return vals[0] if vals else None
+
+
+def sample_power(enqueue, seconds: float, settle: float = 0.5):
+    """Keeps the GPU busy with `enqueue()` (one batch of work per call, two batches in
+    flight) for `seconds` while amd-smi samples socket power and the XCDs' GFX clocks
+    of GPU 0 (the only GPU of the box); samples from the first `settle` seconds are
+    dropped.  Returns medians over the samples, or None without amd-smi."""
+    import threading
+    import torch
+
+    samples = []
+    stop = threading.Event()
+    t0 = time.perf_counter()
+
+    def poll():
+        while not stop.is_set():
+            d = _smi_json(["amd-smi", "metric", "-g", "0", "-p", "-c", "--json"])
+            if d is None:
+                return
+            if time.perf_counter() - t0 < settle:
+                continue
+            pw = [_num(v) for _, v in _find(d, lambda k: k == "socket_power", [])]
+            clk = [_num(v.get("clk")) for k, v in _find(d, lambda k: k.lower().startswith("gfx_"), [])
+                   if isinstance(v, dict)]
+            clk = [c for c in clk if c]
+            if pw and pw[0]:
+                samples.append((pw[0], float(np.median(clk)) if clk else None))
+
+    th = threading.Thread(target=poll, daemon=True)
+    th.start()
+    prev = None
+    while time.perf_counter() - t0 < seconds:
+        enqueue()
+        ev = torch.cuda.Event()
+        ev.record()
+        if prev is not None:
+            prev.synchronize()
+        prev = ev
+    torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=30)
+    if not samples:
+        return None
+    pw = [a for a, _ in samples]
+    clk = [b for _, b in samples if b]
+    return {"socket_W_median": round(float(np.median(pw)), 1),
+            "socket_W_max": round(float(np.max(pw)), 1),
+            "gfx_MHz_median": round(float(np.median(clk)), 0) if clk else None,
+            "samples": len(samples)}
+
+
+def run_workload(name: str, steps: int, warmup: int, separate: bool = False, cold_steps: int = 0,
+                 power_s: float = 0.0):
     """Times `steps` hot-path steps (page write + attention) of a named workload: one
     cw_step_attention per step (decodes on the decode kernel, extends on the extend
     kernel, the page write fused into the extend launch, or into the decode launch
@@ -256,10 +353,15 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
         res["cold_kern_ms_median"] = float(np.median(cold))
         res["cold_kern_ms_min"] = float(cold.min())
         del flush
+    if power_s > 0:
+        def batch():
+            for _ in range(20):
+                step()
+        res["power"] = sample_power(batch, power_s)
     return res
 
 
-def measure_ceilings(reps: int = 5):
+def measure_ceilings(reps: int = 5, power_s: float = 0.0):
     """What the chip sustains on each roofline's unit of work with nothing else in
     the way: a matrix-core loop (bf16 MFMA, no memory traffic) with operand bits like
     real data (the ceiling attention is priced against) and with a few repeated bit
@@ -300,7 +402,13 @@ def measure_ceilings(reps: int = 5):
     copy_ms = med(lambda: cwlib.ceiling_stream_copy(buf, dst))
     nb = buf.numel()
     del buf, dst
-    return {"mfma_bf16_TFLOP_s": round(flops / (mfma_ms * 1e-3) / 1e12, 1),
+    power = None
+    if power_s > 0:
+        loop = lambda rnd: lambda: [cwlib.ceiling_mfma_bf16(wgs, iters, sink, random=rnd) for _ in range(4)]
+        power = {"mfma_loop_random": sample_power(loop(True), power_s),
+                 "mfma_loop_low_entropy": sample_power(loop(False), power_s)}
+    return {"power": power,
+            "mfma_bf16_TFLOP_s": round(flops / (mfma_ms * 1e-3) / 1e12, 1),
             "mfma_bf16_low_entropy_TFLOP_s": round(flops / (mfma_low_ms * 1e-3) / 1e12, 1),
             "vendor_gemm_bf16_TFLOP_s": round(2.0 * n ** 3 / (gemm_ms * 1e-3) / 1e12, 1),
             "hbm_read_GB_s": round(nb / (read_ms * 1e-3) / 1e9, 1),
@@ -363,7 +471,9 @@ def main():
         calibrate_copy(args.calibrate_copy_mib)
         return
     if args.ceilings_only:
-        print(json.dumps({"ceilings": measure_ceilings()}), flush=True)
+        c = measure_ceilings(power_s=args.power_seconds)
+        c["power_cap_W"] = power_cap_w()
+        print(json.dumps({"ceilings": c}), flush=True)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -376,8 +486,9 @@ def main():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
     res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,
-                       cold_steps=args.cold_steps)
-    ceil = measure_ceilings() if args.ceilings else None
+                       cold_steps=args.cold_steps, power_s=args.power_seconds)
+    ceil = measure_ceilings(power_s=args.power_seconds) if args.ceilings else None
+    ceil_power = ceil.pop("power") if ceil is not None else None
     s, w = res["spec"], res["workload"]
     ms, kern_ms = res["ms"], res["kern_ms"]
     decode = s.suffix_lens.max() == 1 and args.workload.startswith("decode")
@@ -439,9 +550,19 @@ def main():
     }
     if ceil is not None:
         result["ceilings"] = ceil
+    if args.power_seconds > 0:
+        power = {"cap_W": power_cap_w(), args.workload: res.get("power")}
+        if ceil_power is not None:
+            power.update(ceil_power)
+        power["source"] = ("amd-smi metric -p -c: socket power and the median of the XCDs' GFX "
+                           "clocks, sampled while the work runs back to back; cap from rocm-smi")
+        result["power"] = power
     if not decode and args.decode_steps > 0:
         # the decode side of the metric: the mixed step's 48 decodes, fp8 pool
-        d = run_workload("decode", args.decode_steps, 10, cold_steps=args.cold_steps)
+        d = run_workload("decode", args.decode_steps, 10, cold_steps=args.cold_steps,
+                         power_s=args.power_seconds)
+        if args.power_seconds > 0:
+            result["power"]["decode"] = d.get("power")
         nbytes = cw.decode_bytes(d["spec"])
         result["decode"] = {
             "workload": WORKLOAD_DESC["decode"], "ms_per_step": round(d["ms"], 5),
