@@ -262,9 +262,11 @@ typedef enum {
 cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value);
 
 /* Benchmark hook: when `start` and `stop` are non-NULL, every later
- * cw_extend_attention / cw_decode_attention call records `start` on its stream
- * right before the main attention kernel and `stop` right after it (before any
- * split-K merge), so hipEventElapsedTime gives that kernel's duration alone.
+ * cw_extend_attention / cw_decode_attention / cw_step_attention call records
+ * `start` on its stream right before the main attention kernel and `stop` right
+ * after it (before any split-K merge), so hipEventElapsedTime gives that
+ * kernel's duration alone.  For cw_step_attention the main kernel is the
+ * extend kernel when the step has extends, else the decode kernel.
  * Pass NULL, NULL to stop.  Process-wide; the events stay owned by the caller. */
 cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop);
 

@@ -614,7 +614,10 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   }
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
   hipError_t e = hipSuccess;
-  if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  // the timing events bracket the extend kernel, or the decode kernel of a
+  // step without extends
+  if (sp.ext.empty() && ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess)
+    return hip_fail(e, "hipEventRecord");
   if (!sp.dec.empty()) {
     ExtendParams pd = plan_params(sp.dec_plan, ws, sp.off_dec_meta, sp.off_dec_part);
     common(pd);
@@ -636,6 +639,7 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     ExtendParams pe = plan_params(sp.ext_plan, ws, sp.off_ext_meta, sp.off_ext_part);
     common(pe);
     pe.w = w;  // every sequence's new K/V, written under the extend's first tiles
+    if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     if ((e = launch_extend_lds(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
       return hip_fail(e, "extend kernel launch");
     if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
