@@ -123,7 +123,10 @@ cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill
   StagingSlot& s = st.slots[st.next_slot];
   st.next_slot = (st.next_slot + 1) % kStagingSlots;
   if (s.ev == nullptr) {
-    e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
+    // The event only tells the host that the upload kernel has finished reading
+    // the slot; it needs no system-scope fence (by default an L2 write-back and
+    // invalidate, which held the next kernel back by ~5 us and left it a cold L2).
+    e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming | hipEventDisableSystemFence);
     if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
   }
   if (s.pending) {
