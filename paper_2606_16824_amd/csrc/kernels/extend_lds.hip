@@ -248,9 +248,23 @@ void extend_lds_kernel(ExtendParams p) {
     return uint32_t((R0 * hkv - R0 % P) * T::RB);
   };
   const size_t page_bytes = size_t(P) * T::PRB;  // one (page, kv head) block
-  // fp8 rows: lane l stages bytes [B8 (l % 8), B8 (l % 8 + 1)) of row 8 w + l / 8
+  // fp8 rows.  D = 64: lane l stages the 8 bytes [8 (l % 8), 8 (l % 8) + 8) of row
+  // 8 w + l / 8 (one widened chunk, stored at its swizzled position).  D = 128:
+  // like the bf16 DMA, load u of lane l fetches what belongs at LDS position
+  // l % 16 of row 8 w + 4 u + l / 16, i.e. the 8 codes of global chunk
+  // (l % 16) ^ swz(row), so that each widened store fills 1 KiB of contiguous LDS
+  // (conflict-free) instead of scattering two chunks over a row.
   const int r8 = wrow0 + (lane >> 3), q8 = lane & 7;
   const uint32_t off8 = uint32_t((r8 % P) * D + q8 * T::B8);
+  int r8u[2];
+  uint32_t koff8[2], voff8[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int R = wrow0 + 4 * u + (lane >> 4), pos = lane & 15;
+    r8u[u] = R;
+    koff8[u] = uint32_t((R % P) * D + 8 * (pos ^ k_swz<D>(R)));
+    voff8[u] = uint32_t((R % P) * D + 8 * (pos ^ v_swz<D>(R)));
+  }
 
   const_i32* bt_s = (const_i32*)bt;
   // physical page of this wave's rows of the tile at j0 (0 if they hold no prefix key)
@@ -304,12 +318,14 @@ void extend_lds_kernel(ExtendParams p) {
   // fp8 pool rows of the tile at j0 into registers (nothing when this wave's
   // rows hold no prefix key; rows of the page past the prefix end are loaded
   // but never stored)
-  auto load8 = [&](int j0, int pg, const uint8_t* pool) __attribute__((always_inline)) -> u32x4 {
+  auto load8 = [&](int j0, int pg, const uint8_t* pool, bool is_k) __attribute__((always_inline)) -> u32x4 {
     u32x4 v = {0u, 0u, 0u, 0u};
     if (j0 + wrow0 < lp) {
       const auto rs = rsrc_at(pool + (size_t(pg) * hkv + kvh) * page_bytes);
       if constexpr (T::B8 == 16) {
-        v = __builtin_amdgcn_raw_buffer_load_b128(rs, off8, 0, 0);
+        const u32x2 a = __builtin_amdgcn_raw_buffer_load_b64(rs, is_k ? koff8[0] : voff8[0], 0, 0);
+        const u32x2 b = __builtin_amdgcn_raw_buffer_load_b64(rs, is_k ? koff8[1] : voff8[1], 0, 0);
+        v = u32x4{a.x, a.y, b.x, b.y};
       } else {
         const u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(rs, off8, 0, 0);
         v = u32x4{w.x, w.y, 0u, 0u};
@@ -319,13 +335,17 @@ void extend_lds_kernel(ExtendParams p) {
   };
   // ... widened to bf16 and stored at the swizzled positions of their rows
   auto store8 = [&](int j0, u32x4 v, uint8_t* dst, bool is_k) __attribute__((always_inline)) {
-    if (j0 + wrow0 < lp && j0 + r8 < lp) {
+    if constexpr (T::B8 == 16) {
+      if (j0 + wrow0 < lp) {
+        if (j0 + r8u[0] < lp)
+          *reinterpret_cast<u32x4*>(dst + wrow0 * T::RB + 16 * lane) = fp8x8_bf16x8(v.x, v.y);
+        if (j0 + r8u[1] < lp)
+          *reinterpret_cast<u32x4*>(dst + (wrow0 + 4) * T::RB + 16 * lane) = fp8x8_bf16x8(v.z, v.w);
+      }
+    } else if (j0 + wrow0 < lp && j0 + r8 < lp) {
       const int swz = is_k ? k_swz<D>(r8) : v_swz<D>(r8);
       uint8_t* row = dst + r8 * T::RB;
-      if constexpr (T::B8 == 16) {
-        *reinterpret_cast<u32x4*>(row + 16 * ((2 * q8) ^ swz)) = fp8x8_bf16x8(v.x, v.y);
-        *reinterpret_cast<u32x4*>(row + 16 * ((2 * q8 + 1) ^ swz)) = fp8x8_bf16x8(v.z, v.w);
-      } else {
+      {
         *reinterpret_cast<u32x4*>(row + 16 * (q8 ^ swz)) = fp8x8_bf16x8(v.x, v.y);
       }
     }
@@ -575,9 +595,9 @@ void extend_lds_kernel(ExtendParams p) {
       pg_v = pg1;
       if (n_tiles > 2) pg_raw = load_page(tile0(2));
     } else {
-      const u32x4 a = load8(tile0(0), pg0, k_pool), b = load8(tile0(0), pg0, v_pool);
+      const u32x4 a = load8(tile0(0), pg0, k_pool, true), b = load8(tile0(0), pg0, v_pool, false);
       u32x4 k1 = {0u, 0u, 0u, 0u};
-      if (n_tiles > 1) k1 = load8(tile0(1), pg1, k_pool);
+      if (n_tiles > 1) k1 = load8(tile0(1), pg1, k_pool, true);
       float ks0, vs0, ks1 = 1.f, vs1 = 1.f;
       load_scales(tile0(0), pg0, ks0, vs0);
       if (n_tiles > 1) load_scales(tile0(1), pg1, ks1, vs1);
@@ -589,10 +609,10 @@ void extend_lds_kernel(ExtendParams p) {
       write_params(tile0(0), 0, ks0, vs0);
       if (n_tiles > 1) write_params(tile0(1), 1, ks1, vs1);
       if (n_tiles > 2) {
-        k8 = load8(tile0(2), pg2, k_pool);
+        k8 = load8(tile0(2), pg2, k_pool, true);
         load_scales(tile0(2), pg2, ks_n, vs_n);
       }
-      if (n_tiles > 1) v8 = load8(tile0(1), pg1, v_pool);
+      if (n_tiles > 1) v8 = load8(tile0(1), pg1, v_pool, false);
       pg_v = pg2;
       if (n_tiles > 3) pg_raw = load_page(tile0(3));
     }
@@ -664,10 +684,10 @@ void extend_lds_kernel(ExtendParams p) {
     if (all_prefix || j + 1 < n_tiles) store8(tile0(j + 1), v8, v_nxt, false);
     const int pg3 = pg_raw;
     if (all_prefix || j + 3 < n_tiles) {
-      k8 = load8(tile0(j + 3), pg3, k_pool);
+      k8 = load8(tile0(j + 3), pg3, k_pool, true);
       load_scales(tile0(j + 3), pg3, ks_n, vs_n);
     }
-    if (all_prefix || j + 2 < n_tiles) v8 = load8(tile0(j + 2), pg_v, v_pool);
+    if (all_prefix || j + 2 < n_tiles) v8 = load8(tile0(j + 2), pg_v, v_pool, false);
     pg_v = pg3;
     pg_raw = load_page(tile0(j + 4));  // an in-range entry whenever it is a prefix page
   };
