@@ -188,6 +188,16 @@ def _num(v):
         return None
 
 
+def parse_smi_metric(d):
+    """(socket power W, median GFX clock MHz over the XCDs) from the JSON of
+    `amd-smi metric -p -c --json`; either is None when the report lacks it."""
+    pw = [_num(v) for _, v in _find(d, lambda k: k == "socket_power", [])]
+    clk = [_num(v.get("clk")) for k, v in _find(d, lambda k: k.lower().startswith("gfx_"), [])
+           if isinstance(v, dict)]
+    clk = [c for c in clk if c]
+    return (pw[0] if pw and pw[0] else None), (float(np.median(clk)) if clk else None)
+
+
 def power_cap_w():
     """The board's power cap (W) as rocm-smi reports it, or None."""
     d = _smi_json(["rocm-smi", "--showmaxpower", "--json"])
@@ -215,12 +225,9 @@ def sample_power(enqueue, seconds: float, settle: float = 0.5):
                 return
             if time.perf_counter() - t0 < settle:
                 continue
-            pw = [_num(v) for _, v in _find(d, lambda k: k == "socket_power", [])]
-            clk = [_num(v.get("clk")) for k, v in _find(d, lambda k: k.lower().startswith("gfx_"), [])
-                   if isinstance(v, dict)]
-            clk = [c for c in clk if c]
-            if pw and pw[0]:
-                samples.append((pw[0], float(np.median(clk)) if clk else None))
+            pw, clk = parse_smi_metric(d)
+            if pw:
+                samples.append((pw, clk))
 
     th = threading.Thread(target=poll, daemon=True)
     th.start()
