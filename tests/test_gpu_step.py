@@ -19,6 +19,7 @@ pytestmark = pytest.mark.gpu
 CASES = {
     "bf16_mixed": ([40, 0, 300, 17, 128, 999, 64], [1, 5, 1, 0, 70, 1, 33], 2, 4, 128, 16, "bf16"),
     "fp8_mixed_p64": ([65, 3, 500, 130], [1, 61, 1, 200], 2, 3, 64, 64, "fp8"),
+    "fp8_mixed_p64_d128": ([700, 64, 129], [1, 150, 70], 2, 4, 128, 64, "fp8"),
     "decodes_only": ([100, 7, 250], [1, 1, 1], 1, 8, 128, 16, "bf16"),
     # the decode launch performs the page write; new tokens at page starts (Lp = 0, 16, 160, 64)
     "decodes_only_fp8": ([0, 16, 33, 160, 1023], [1, 1, 1, 1, 1], 2, 4, 128, 16, "fp8"),
