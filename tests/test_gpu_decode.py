@@ -31,6 +31,8 @@ CASES = {
     "p64_g8_fp8": ([63, 64, 65, 5000], 2, 8, 128, 64, "fp8"),
     "d64_bf16": ([100, 2047, 2048, 2049], 3, 2, 64, 16, "bf16"),
     "d64_fp8_p64": ([100, 4095, 4096, 9000], 1, 16, 64, 64, "fp8"),
+    "d64_fp8_p16": ([100, 2047, 2048, 2049], 2, 4, 64, 16, "fp8"),
+    "d64_bf16_p64": ([63, 64, 65, 3000], 2, 2, 64, 64, "bf16"),
     "mqa_g1": ([300, 7], 1, 1, 128, 16, "bf16"),
 }
 

@@ -40,6 +40,7 @@ SMALL_CASES = {
     "many_heads_mha": ([64, 130], [40, 17], 16, 1, 64, 16, "bf16"),
     "gqa16_d128_fp8": ([200, 17], [24, 3], 1, 16, 128, 16, "fp8"),
     "fp8_p64_d128": ([129, 64, 300], [33, 90, 1], 2, 4, 128, 64, "fp8"),
+    "fp8_p16_d64": ([50, 130, 17], [20, 45, 3], 2, 4, 64, 16, "fp8"),
     # 40 short ragged sequences: many bundles, idle padding in the XCD queues
     "many_seqs": ([(37 * i) % 301 for i in range(40)], [1 + (11 * i) % 40 for i in range(40)],
                   2, 4, 128, 16, "bf16"),
