@@ -35,6 +35,7 @@ from .paged_attention import (  # noqa: F401
     extend_attention_blocked,
     extend_attention_rows,
     extend_attention_rowwise,
+    extend_attention_token_blocks,
     gather_sequence_kv,
     write_pages,
 )

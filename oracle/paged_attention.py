@@ -150,41 +150,78 @@ def extend_attention_rows(inp: PagedInputs, rows: Iterable[Tuple[int, int]]):
     return out, lse
 
 
-def extend_attention_blocked(inp: PagedInputs, block_tokens: int = 64):
+def _blocked_rows(inp: PagedInputs, b: int, k: np.ndarray, v: np.ndarray, t0: int, t1: int):
+    """Suffix tokens [t0, t1) of sequence b, every query head, by implementation
+    (ii): per kv head, S = Q K^T over the visible keys with one matrix product
+    (row = token * G + group member), keys past each row's causal limit set to
+    -inf, row softmax, then P V.  k, v: the sequence's gathered keys/values; the
+    arithmetic runs in their dtype (float64, or float32 for the timed CPU
+    baseline).  Returns (out [t1-t0, Hq, D], lse [t1-t0, Hq]) in that dtype."""
+    _, hq, d = inp.q.shape
+    g = inp.gqa_group
+    lp = int(inp.prefix_lens[b])
+    c0 = int(inp.cu()[b])
+    dt = k.dtype
+    out = np.zeros((t1 - t0, hq, d), dtype=dt)
+    lse = np.zeros((t1 - t0, hq), dtype=dt)
+    n_max = lp + t1
+    limit = lp + np.repeat(np.arange(t0, t1), g) + 1  # visible keys per row
+    for kvh in range(inp.num_kv_heads):
+        kh, vh = k[:, kvh], v[:, kvh]
+        qb = bf16_bits_to_f64(inp.q[c0 + t0:c0 + t1, kvh * g:(kvh + 1) * g]).astype(dt)
+        qb = qb.reshape((t1 - t0) * g, d)
+        s = dt.type(inp.softmax_scale) * (qb @ kh[:n_max].T)
+        s[np.arange(n_max)[None, :] >= limit[:, None]] = -np.inf
+        m = s.max(axis=1, keepdims=True)
+        p = np.exp(s - m)
+        l = p.sum(axis=1, keepdims=True)
+        o = (p @ vh[:n_max]) / l
+        out[:, kvh * g:(kvh + 1) * g] = o.reshape(t1 - t0, g, d)
+        lse[:, kvh * g:(kvh + 1) * g] = (m + np.log(l)).reshape(t1 - t0, g)
+    return out, lse
+
+
+def extend_attention_blocked(inp: PagedInputs, block_tokens: int = 64, dtype=np.float64):
     """Implementation (ii): per (sequence, kv head), blocks of query tokens x G heads.
 
     S = Q K^T over all visible keys with a matrix product, keys past each
-    row's causal limit set to -inf, row softmax, then P V.
+    row's causal limit set to -inf, row softmax, then P V.  `dtype` float32
+    runs the same steps in single precision (the CPU baseline the benchmark
+    times); the parity checks use the float64 default.
     """
     t_total, hq, d = inp.q.shape
-    g = inp.gqa_group
-    hkv = inp.num_kv_heads
-    out = np.zeros((t_total, hq, d), dtype=np.float64)
-    lse = np.zeros((t_total, hq), dtype=np.float64)
+    out = np.zeros((t_total, hq, d), dtype=dtype)
+    lse = np.zeros((t_total, hq), dtype=dtype)
     cu = inp.cu()
     for b in range(len(inp.suffix_lens)):
-        lp, ls = int(inp.prefix_lens[b]), int(inp.suffix_lens[b])
+        ls = int(inp.suffix_lens[b])
         if ls == 0:
             continue
         k, v = gather_sequence_kv(inp, b)
+        if dtype != np.float64:
+            k, v = k.astype(dtype), v.astype(dtype)
         c0 = int(cu[b])
-        for kvh in range(hkv):
-            kh, vh = k[:, kvh], v[:, kvh]
-            for t0 in range(0, ls, block_tokens):
-                t1 = min(ls, t0 + block_tokens)
-                n_max = lp + t1
-                qb = bf16_bits_to_f64(inp.q[c0 + t0:c0 + t1, kvh * g:(kvh + 1) * g])
-                qb = qb.reshape((t1 - t0) * g, d)  # row = token * G + group member
-                s = inp.softmax_scale * (qb @ kh[:n_max].T)
-                limit = lp + np.repeat(np.arange(t0, t1), g) + 1  # visible keys per row
-                s[np.arange(n_max)[None, :] >= limit[:, None]] = -np.inf
-                m = s.max(axis=1, keepdims=True)
-                p = np.exp(s - m)
-                l = p.sum(axis=1, keepdims=True)
-                o = (p @ vh[:n_max]) / l
-                out[c0 + t0:c0 + t1, kvh * g:(kvh + 1) * g] = o.reshape(t1 - t0, g, d)
-                lse[c0 + t0:c0 + t1, kvh * g:(kvh + 1) * g] = (m + np.log(l)).reshape(t1 - t0, g)
+        for t0 in range(0, ls, block_tokens):
+            t1 = min(ls, t0 + block_tokens)
+            out[c0 + t0:c0 + t1], lse[c0 + t0:c0 + t1] = _blocked_rows(inp, b, k, v, t0, t1)
     return out, lse
+
+
+def extend_attention_token_blocks(inp: PagedInputs, blocks: Sequence[Tuple[int, int, int]]):
+    """Implementation (ii) on chosen blocks only: `blocks` lists (sequence b,
+    first suffix token t0, end t1).  Returns a list of (out float64
+    [t1-t0, Hq, D], lse float64 [t1-t0, Hq]) in the order given; each
+    sequence's keys are gathered once."""
+    res = [None] * len(blocks)
+    by_seq = {}
+    for i, (b, t0, t1) in enumerate(blocks):
+        by_seq.setdefault(int(b), []).append(i)
+    for b, idx in by_seq.items():
+        k, v = gather_sequence_kv(inp, b)
+        for i in idx:
+            _, t0, t1 = blocks[i]
+            res[i] = _blocked_rows(inp, b, k, v, int(t0), int(t1))
+    return res
 
 
 def decode_attention(q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray, k_pool: np.ndarray,

@@ -14,7 +14,8 @@ import torch
 
 import cw_workloads as cw
 from oracle import (PagedInputs, decode_attention, extend_attention_blocked,
-                    extend_attention_rows, extend_attention_rowwise, gather_sequence_kv)
+                    extend_attention_rows, extend_attention_rowwise, extend_attention_token_blocks,
+                    gather_sequence_kv)
 from conftest import paged_inputs
 
 
@@ -242,6 +243,31 @@ def test_rows_and_decode_agree_with_full():
     for k, (t, h) in enumerate(rows):
         np.testing.assert_allclose(o3[k], out[t, h], rtol=1e-12)
         assert l3[k] == pytest.approx(lse[t, h], rel=1e-12)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_token_blocks_against_brute_force(kv_dtype):
+    # chosen suffix-token blocks (first, middle, ragged last, a whole short sequence)
+    inp = small([7, 0, 12], [9, 5, 3], 3, 8, p=4, kv_dtype=kv_dtype, seed=57)
+    ref, ref_lse = brute_force(inp)
+    cu = inp.cu()
+    blocks = [(0, 0, 4), (0, 4, 8), (0, 8, 9), (1, 0, 5), (2, 1, 3)]
+    for (b, t0, t1), (out, lse) in zip(blocks, extend_attention_token_blocks(inp, blocks)):
+        r0, r1 = int(cu[b]) + t0, int(cu[b]) + t1
+        np.testing.assert_allclose(out, ref[r0:r1], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(lse, ref_lse[r0:r1], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_float32_blocked_matches_float64(kv_dtype):
+    # the single-precision variant (timed as the CPU baseline) runs the same steps:
+    # it agrees with the float64 checker to fp32 accumulation error
+    inp = small([300, 0, 77], [40, 9, 64], 4, 64, p=16, kv_dtype=kv_dtype, seed=61)
+    ref, ref_lse = extend_attention_blocked(inp)
+    out, lse = extend_attention_blocked(inp, dtype=np.float32)
+    assert out.dtype == np.float32 and lse.dtype == np.float32
+    np.testing.assert_allclose(out, ref, rtol=0, atol=2e-5)
+    np.testing.assert_allclose(lse, ref_lse, rtol=0, atol=2e-5)
 
 
 def test_fp8_gather_uses_page_scale():
