@@ -377,7 +377,10 @@ void extend_lds_kernel(ExtendParams p) {
   f32x16 o[T::DB];
 #pragma unroll
   for (int b = 0; b < T::DB; ++b) o[b] = f32x16{};
-  float m_run = 0.f, l_run = 0.f;
+  // A wave that sees no key of this item (a split-K chunk past its rows' causal
+  // limits) keeps m = kNegBig and l = 0, so its partial gets weight 0 in the
+  // merge whatever the other chunks' maxima are.
+  float m_run = kNegBig, l_run = 0.f;
   f32x16 negm = f32x16{};  // bf16: -m_run in every element (the score MFMAs' start)
 
   const int n_tiles = (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
@@ -620,9 +623,10 @@ void extend_lds_kernel(ExtendParams p) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (visible(0)) {
+      m_run = 0.f;  // the scores below are taken relative to 0 (negm is 0 too)
       scores(lds_k0, xa);
       mask(tile0(0), xa);
-      to_log2(tile0(0), 0, xa, true);  // m_run = 0 here
+      to_log2(tile0(0), 0, xa, true);
       const float mx = row_max(xa);
       // a row with no visible key in the first tile sees none in the item
       const float d = mx == -INFINITY ? 0.f : mx;

@@ -143,3 +143,30 @@ def test_closed_form_single_key_and_mean():
     out0, _ = run_extend(to_gpu(w))
     ref, _ = oracle.extend_attention_rowwise(paged_inputs(w))
     assert_close(as_f64(out0), ref, BF16_MAX_ABS, BF16_MEAN_ABS, "q=0")
+
+
+@pytest.mark.parametrize("lp", [0, 100])
+def test_forced_split_with_strongly_negative_scores(lp):
+    """G = 1 and one-tile chunks: the first wave of a 256-row item sees none of the
+    later chunks' keys; its empty partials must not outweigh real ones whose row
+    maxima lie far below zero (scores about -128, i.e. -185 in log2 units)."""
+    spec = cw.custom_spec([lp], [256], num_kv_heads=1, gqa_group=1, head_dim=64, page_size=16,
+                          seed=31)
+    _case(f"negative_split_lp{lp}", spec)
+    w = cw.materialize(spec)
+    g = torch.Generator().manual_seed(4)
+    w.q = torch.full_like(w.q, -16.0)
+    w.k_new = (1 + 0.05 * torch.randn(w.k_new.shape, generator=g)).to(torch.bfloat16)
+    w.k_pool = (1 + 0.05 * torch.randn(w.k_pool.shape, generator=g)).to(torch.bfloat16)
+    ref, ref_lse = oracle.extend_attention_blocked(paged_inputs(w))
+    assert ref_lse.max() < -100.0  # every row's scores are strongly negative
+    cwlib.set_tuning(0, 1)
+    try:
+        out, lse = run_extend(to_gpu(w))
+    finally:
+        cwlib.set_tuning(0, 0)
+    assert_close(as_f64(out), ref, BF16_MAX_ABS, BF16_MEAN_ABS, "negative split")
+    # the kernel rounds the scaled query to bf16 once (relative 2^-9); here every
+    # element of q is the same, so every score moves by the same relative amount
+    # and lse (about -128) by up to 128 * 2^-9 = 0.25
+    assert_close(lse.cpu().double().numpy(), ref_lse, 0.5, None, "negative split lse")
