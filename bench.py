@@ -116,16 +116,51 @@ def measured_traffic(kind: str, workload: str):
     return int(m.group(1))
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or the platform's processor string."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def blas_vendor() -> str:
+    """The BLAS numpy calls (runtime library as threadpoolctl sees it, and numpy's
+    build configuration)."""
+    parts = []
+    try:
+        from threadpoolctl import threadpool_info
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                parts.append(f"{i.get('internal_api')} {i.get('version')} ({os.path.basename(i.get('filepath', ''))})")
+    except Exception:
+        pass
+    try:
+        cfg = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        parts.append(f"numpy built with {cfg.get('name')} {cfg.get('version')}")
+    except Exception:
+        pass
+    return "; ".join(parts) or "unknown"
+
+
 def cpu_baseline(w, target_s: float):
-    """The oracle (float64, blocked) on the first suffix tokens of sequence 0."""
+    """The oracle's blocked implementation in float32 (NumPy sgemm for S and P V, per
+    (sequence, kv head) blocks of 64 tokens x G heads) on the first suffix tokens of
+    sequence 0, as many as fit in about `target_s` seconds (the whole suffix when it
+    is faster), with BLAS threads = the CPUs this process may run on."""
     import oracle
     from tests.conftest import paged_inputs
 
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores, user_api="blas")
     except Exception:
-        threads = os.cpu_count() or 1
+        limiter = None
     inp = paged_inputs(w)
     s = w.spec
     lp, ls = int(s.prefix_lens[0]), int(s.suffix_lens[0])
@@ -136,20 +171,27 @@ def cpu_baseline(w, target_s: float):
                                  inp.gqa_group, inp.softmax_scale, inp.kv_dtype, inp.k_scale,
                                  inp.v_scale)
         t0 = time.perf_counter()
-        oracle.extend_attention_blocked(sub, block_tokens=64)
+        oracle.extend_attention_blocked(sub, block_tokens=64, dtype=np.float32)
         return time.perf_counter() - t0
 
-    n = min(16, ls)
-    dt = run(n)
-    if dt < target_s and n < ls:
-        n = int(min(ls, max(n + 1, n * target_s / max(dt, 1e-3))))
+    try:
+        # the page gather is a fixed cost, so grow the sample by doubling until it
+        # takes at least half the target (or covers the whole suffix)
+        n = min(64, ls)
         dt = run(n)
+        while dt < 0.5 * target_s and n < ls:
+            n = min(ls, 2 * n)
+            dt = run(n)
+    finally:
+        if limiter is not None:
+            limiter.unregister()
     pairs = n * lp + n * (n + 1) // 2
     flops = 4.0 * s.head_dim * s.num_q_heads * pairs
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
             "sample": f"first {n} of {ls} suffix tokens of sequence 0, all {s.num_q_heads} query heads "
-                      f"(float64 blocked oracle), {dt:.1f} s",
-            "tok_s": n / dt}
+                      f"(float32 blocked oracle: page gather, sgemm, mask, softmax, P V), {dt:.1f} s",
+            "tok_s": n / dt, "cpu_model": cpu_model(), "blas": blas_vendor(),
+            "wall_s": round(dt, 3)}
 
 
 def _smi_json(args):
@@ -279,7 +321,7 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
                                           s.page_size, s.kv_dtype)
     elif separate:
         nb = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
-                                          s.gqa_group, s.head_dim, s.page_size, s.kv_dtype)
+                                          s.gqa_group, s.head_dim, s.page_size)
     else:
         nb = cwlib.step_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
                                         s.gqa_group, s.head_dim, s.page_size, s.kv_dtype)

@@ -34,8 +34,11 @@
  * the suffix keys/values come from the bf16 k_new / v_new.
  *
  * Ownership and ordering: the caller owns every buffer, including the
- * workspace; the library keeps only a per-device cache of device properties
- * and a small pinned host staging area it allocates on first use.  All work is
+ * workspace.  Per device the library keeps a cache of device properties, a
+ * pinned host staging ring for the per-call plan (8 slots of 4 MiB, allocated
+ * once by cw_init or by the first call that needs it, never grown or freed;
+ * a call whose plan exceeds a slot fails with CW_ERR_UNSUPPORTED).  No call
+ * allocates device or pinned memory after that one-time set-up.  All work is
  * enqueued on `stream`; returning CW_OK means enqueued, not finished; buffers
  * must stay valid until the stream has passed the work.  Calls on one stream
  * may share one workspace; calls that may run concurrently need separate ones.
@@ -108,13 +111,12 @@ cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool
                               int32_t page_size, cw_kv_dtype_t kv_dtype, void* workspace,
                               size_t workspace_bytes, hipStream_t stream);
 
-/* Workspace bytes cw_extend_attention needs for these lengths and this pool
- * dtype on the current device (work list plus split-K partials; the two pool
- * dtypes run kernels with different row blocks, so their work lists differ).
+/* Workspace bytes cw_extend_attention needs for these lengths on the current
+ * device (work list plus split-K partials; the same for both pool dtypes).
  * 0 if the arguments are invalid. */
 size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                  int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                                 int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype);
+                                 int32_t head_dim, int32_t page_size);
 
 /* Prefix-cached paged extend attention (CacheWise Sec. 2-3: a request that
  * extends a cached prefix computes attention only for its new tokens, over the
@@ -275,12 +277,21 @@ cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop);
  * {seq, kv_head, first packed row, key begin, key end, partial slot or -1,
  *  rows in tile, 0}; a seq of -1 marks an idle padding item.  Returns the
  * number of items, or -1 if the arguments are invalid.  The plan is the one
- * cw_extend_attention uses for a pool of `kv_dtype`.  Makes no HIP call
+ * cw_extend_attention uses (for either pool dtype).  Makes no HIP call
  * other than a cached device-property query, and works without a GPU. */
 int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                             int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype,
-                             int32_t* items_out, int64_t capacity);
+                             int32_t head_dim, int32_t page_size, int32_t* items_out,
+                             int64_t capacity);
+
+/* One-time set-up of the current device: allocates the pinned plan staging
+ * ring.  Idempotent; every other call does it on first use.  CW_ERR_HIP on failure
+ * (nothing stays allocated then, and the call can be repeated). */
+cw_status_t cw_init(void);
+
+/* Number of pinned host allocations the library has made in this process
+ * (kStagingSlots per initialised device; for tests that no call allocates). */
+int64_t cw_pinned_allocations(void);
 
 const char* cw_status_string(cw_status_t status);
 const char* cw_last_error_message(void);

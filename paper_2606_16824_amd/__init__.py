@@ -15,6 +15,13 @@ fallback: without the built library every call raises.
 
 Page size and head dim are read from the pool shape [num_pages, Hkv, P, D];
 an fp8 pool is a uint8 (or float8_e4m3fn) tensor of e4m3fn codes.
+
+The C side sees only pointers, so the binding checks every tensor's dtype and
+shape against the call's lengths before passing a pointer (ValueError on a
+mismatch): block_table 2-D int32 with a row per sequence; q and out bf16
+[T, Hkv*G, D]; k_new, v_new bf16 [T, Hkv, D]; lse fp32 [T, Hkv*G]; v_pool like
+k_pool; fp8 scales fp32 [num_pages, Hkv] (and absent for bf16 pools); every
+tensor on one GPU and contiguous.
 """
 from __future__ import annotations
 
@@ -26,7 +33,7 @@ import torch
 
 from . import _lib as L
 
-__all__ = ["CWError", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
+__all__ = ["CWError", "init", "pinned_allocations", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
            "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
            "step_attention", "step_workspace_bytes", "check_block_table", "ceiling_mfma_bf16", "ceiling_stream_read",
@@ -68,6 +75,83 @@ def _dptr(t: Optional[torch.Tensor]):
     return t.data_ptr()
 
 
+def _want(t, name, dtypes, shape):
+    """Marshalling check: `t` has one of `dtypes` and exactly `shape`."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {' or '.join(map(str, dtypes))}")
+    if tuple(t.shape) != tuple(int(x) for x in shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(int(x) for x in shape)}")
+
+
+_BF16 = (torch.bfloat16,)
+_FP8 = (torch.uint8, torch.float8_e4m3fn)
+
+
+def _check_pools(k_pool, v_pool, k_scale, v_scale):
+    """Pool, scale and their dtypes; returns (num_pages, Hkv, P, D)."""
+    if not isinstance(k_pool, torch.Tensor) or k_pool.dim() != 4:
+        raise ValueError("k_pool must be a 4-D tensor [num_pages, Hkv, P, D]")
+    _kv_dtype(k_pool)
+    _want(v_pool, "v_pool", (k_pool.dtype,), k_pool.shape)
+    num_pages, hkv, page, d = k_pool.shape
+    if k_pool.dtype == torch.bfloat16:
+        if k_scale is not None or v_scale is not None:
+            raise ValueError("k_scale / v_scale are for fp8 pools only")
+    else:
+        if k_scale is None or v_scale is None:
+            raise ValueError("an fp8 pool needs k_scale and v_scale")
+        _want(k_scale, "k_scale", (torch.float32,), (num_pages, hkv))
+        _want(v_scale, "v_scale", (torch.float32,), (num_pages, hkv))
+    return num_pages, hkv, page, d
+
+
+def _check_call(q, k_new, v_new, k_pool, v_pool, block_table, num_seqs, total, gqa_group,
+                k_scale=None, v_scale=None, out=None, lse=None):
+    """dtype and shape of every tensor of an attention call against its lengths
+    (`total` packed rows, `num_seqs` sequences); returns the pool dimensions."""
+    num_pages, hkv, page, d = _check_pools(k_pool, v_pool, k_scale, v_scale)
+    if not isinstance(block_table, torch.Tensor) or block_table.dim() != 2 \
+            or block_table.dtype != torch.int32:
+        raise ValueError("block_table must be a 2-D int32 tensor [num_seqs, bt_stride]")
+    if block_table.shape[0] < num_seqs:
+        raise ValueError(f"block_table has {block_table.shape[0]} rows for {num_seqs} sequences")
+    if int(gqa_group) < 1:
+        raise ValueError(f"gqa_group = {gqa_group} must be >= 1")
+    hq = hkv * int(gqa_group)
+    if q is not None:
+        _want(q, "q", _BF16, (total, hq, d))
+    if out is not None:
+        _want(out, "out", _BF16, (total, hq, d))
+    _want(k_new, "k_new", _BF16, (total, hkv, d))
+    _want(v_new, "v_new", _BF16, (total, hkv, d))
+    if lse is not None:
+        _want(lse, "lse", (torch.float32,), (total, hq))
+    devs = {t.device for t in (q, out, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, lse)
+            if t is not None}
+    if len(devs) > 1:
+        raise ValueError(f"tensors are on different devices: {sorted(map(str, devs))}")
+    return num_pages, hkv, page, d
+
+
+def _lens_pair(prefix_lens, suffix_lens):
+    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
+    if lp.ndim != 1 or lp.shape != ls.shape:
+        raise ValueError(f"prefix_lens {lp.shape} and suffix_lens {ls.shape} must be 1-D of one length")
+    return lp, ls
+
+
+def init():
+    """cw_init on the current device (the one-time pinned staging set-up)."""
+    _check(library().cw_init())
+
+
+def pinned_allocations() -> int:
+    """Pinned host allocations the library has made in this process."""
+    return int(library().cw_pinned_allocations())
+
+
 def _stream():
     return C.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -99,11 +183,10 @@ def _dtype_code(kv_dtype) -> int:
 
 
 def extend_workspace_bytes(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim,
-                           page_size, kv_dtype="bf16") -> int:
+                           page_size) -> int:
     lp, ls = _lens(prefix_lens), _lens(suffix_lens)
     return int(library().cw_extend_workspace_bytes(_ptr(lp), _ptr(ls), len(lp), num_kv_heads,
-                                                   gqa_group, head_dim, page_size,
-                                                   _dtype_code(kv_dtype)))
+                                                   gqa_group, head_dim, page_size))
 
 
 def decode_workspace_bytes(prefix_lens, num_kv_heads, gqa_group, head_dim, page_size,
@@ -117,26 +200,25 @@ def set_tuning(key: int, value: int):
     _check(library().cw_set_tuning(key, value))
 
 
-def plan_items(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page_size,
-               kv_dtype="bf16") -> np.ndarray:
+def plan_items(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page_size) -> np.ndarray:
     """The extend work list in launch order, int32 [n, 8] (see cw_extend_plan_items)."""
     lp, ls = _lens(prefix_lens), _lens(suffix_lens)
     lib = library()
-    dt = _dtype_code(kv_dtype)
     n = lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
-                                 page_size, dt, None, 0)
+                                 page_size, None, 0)
     if n < 0:
         raise CWError(L.CW_ERR_UNSUPPORTED, "invalid plan arguments")
     out = np.zeros((max(n, 1), 8), dtype=np.int32)
     lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
-                             page_size, dt, out.ctypes.data, n)
+                             page_size, out.ctypes.data, n)
     return out[:n]
 
 
 def kv_write_pages(k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
                    k_scale=None, v_scale=None, workspace=None):
-    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
-    num_pages, hkv, page, d = k_pool.shape
+    lp, ls = _lens_pair(prefix_lens, suffix_lens)
+    num_pages, hkv, page, d = _check_call(None, k_new, v_new, k_pool, v_pool, block_table, len(lp),
+                                          int(ls.sum()), 1, k_scale, v_scale)
     ws = _workspace(write_pages_workspace_bytes(len(lp)), k_pool.device, workspace)
     _check(library().cw_kv_write_pages(
         _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale), _dptr(v_scale),
@@ -147,12 +229,13 @@ def kv_write_pages(k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffi
 def extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
                      gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None, lse=None,
                      workspace=None):
-    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
-    num_pages, hkv, page, d = k_pool.shape
+    lp, ls = _lens_pair(prefix_lens, suffix_lens)
+    num_pages, hkv, page, d = _check_call(q, k_new, v_new, k_pool, v_pool, block_table, len(lp),
+                                          int(ls.sum()), gqa_group, k_scale, v_scale, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
-        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
+        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page),
                                q.device, None)
     _check(library().cw_extend_attention(
         _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
@@ -166,12 +249,13 @@ def write_extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_
                            gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None,
                            lse=None, workspace=None):
     """kv_write_pages + extend_attention in one launch (the pools are written)."""
-    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
-    num_pages, hkv, page, d = k_pool.shape
+    lp, ls = _lens_pair(prefix_lens, suffix_lens)
+    num_pages, hkv, page, d = _check_call(q, k_new, v_new, k_pool, v_pool, block_table, len(lp),
+                                          int(ls.sum()), gqa_group, k_scale, v_scale, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
-        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page, _kv_dtype(k_pool)),
+        workspace = _workspace(extend_workspace_bytes(lp, ls, hkv, gqa_group, d, page),
                                q.device, None)
     _check(library().cw_write_extend_attention(
         _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
@@ -192,8 +276,9 @@ def step_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, su
                    gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None, lse=None,
                    workspace=None):
     """One serving step: page write + attention, decodes on the decode kernel."""
-    lp, ls = _lens(prefix_lens), _lens(suffix_lens)
-    num_pages, hkv, page, d = k_pool.shape
+    lp, ls = _lens_pair(prefix_lens, suffix_lens)
+    num_pages, hkv, page, d = _check_call(q, k_new, v_new, k_pool, v_pool, block_table, len(lp),
+                                          int(ls.sum()), gqa_group, k_scale, v_scale, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
@@ -256,7 +341,10 @@ def kv_swap_in(k_host, v_host, k_pool, v_pool, host_blocks, pages, k_scale_host=
 def decode_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, gqa_group,
                      softmax_scale, k_scale=None, v_scale=None, out=None, lse=None, workspace=None):
     lp = _lens(prefix_lens)
-    num_pages, hkv, page, d = k_pool.shape
+    if lp.ndim != 1:
+        raise ValueError("prefix_lens must be 1-D")
+    num_pages, hkv, page, d = _check_call(q, k_new, v_new, k_pool, v_pool, block_table, len(lp),
+                                          len(lp), gqa_group, k_scale, v_scale, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:

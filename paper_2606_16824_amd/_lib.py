@@ -11,7 +11,7 @@ LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(
     os.path.dirname(os.path.abspath(__file__)), "libcw.so")
 
 (CW_OK, CW_ERR_NULL, CW_ERR_UNSUPPORTED, CW_ERR_BAD_LENS, CW_ERR_ALIGN, CW_ERR_WORKSPACE, CW_ERR_HIP,
- CW_ERR_ALIAS) = range(8)
+ CW_ERR_ALIAS, CW_ERR_INIT) = range(9)
 CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1
 CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS = 0, 1
 CW_CEILING_LOW_ENTROPY, CW_CEILING_RANDOM = 0, 1
@@ -27,7 +27,7 @@ SIGNATURES = {
     "cw_write_pages_workspace_bytes": (_sz, [_i32]),
     "cw_kv_write_pages": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32,
                                     _i32, _i32, _i32, C.c_int, _vp, _sz, _vp]),
-    "cw_extend_workspace_bytes": (_sz, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32]),
+    "cw_extend_workspace_bytes": (_sz, [_vp, _vp, _i32, _i32, _i32, _i32, _i32]),
     "cw_extend_attention": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                       _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int, _vp, _vp,
                                       _vp, _sz, _vp]),
@@ -50,7 +50,9 @@ SIGNATURES = {
     "cw_check_block_table": (C.c_int, [_vp, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _sz, _vp]),
     "cw_set_tuning": (C.c_int, [C.c_int, _i32]),
     "cw_set_timing_events": (C.c_int, [_vp, _vp]),
-    "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),
+    "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),
+    "cw_init": (C.c_int, []),
+    "cw_pinned_allocations": (C.c_int64, []),
     "cw_status_string": (C.c_char_p, [C.c_int]),
     "cw_last_error_message": (C.c_char_p, []),
     "cw_version": (_i32, []),

@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -53,11 +54,13 @@ Tuning current_tuning() {
 
 constexpr int kMaxDevices = 64;
 constexpr int kStagingSlots = 8;
+// Every staging slot has this fixed size, allocated once per device (cw_init or
+// the first call that uploads a plan); a plan larger than a slot is rejected.
+constexpr size_t kStagingSlotBytes = size_t(4) << 20;
 
 struct StagingSlot {
   void* host = nullptr;
   void* dev = nullptr;  // the same pinned memory as the device addresses it
-  size_t cap = 0;
   hipEvent_t ev = nullptr;
   bool pending = false;
 };
@@ -66,12 +69,14 @@ struct DeviceState {
   std::once_flag props_once;
   int32_t num_cus = 256;
   int32_t num_xcds = 8;
-  std::mutex staging_mu;
+  std::mutex staging_mu;  // guards everything below
+  bool ready = false;     // staging ring allocated
   StagingSlot slots[kStagingSlots];
   int next_slot = 0;
 };
 
 DeviceState g_devices[kMaxDevices];
+std::atomic<int64_t> g_pinned_allocs{0};
 
 // Current device, or -1 when no GPU runtime is usable (host-only queries).
 int current_device() {
@@ -106,48 +111,84 @@ void device_shape(int32_t* cus, int32_t* xcds) {
   *xcds = st.num_xcds;
 }
 
+// The device's one-time set-up, under st.staging_mu: the pinned staging ring
+// (kStagingSlots slots of kStagingSlotBytes, with their events).  Nothing is allocated
+// after it succeeds; a failure frees what it allocated and can be retried.
+cw_status_t init_locked(DeviceState& st) {
+  if (st.ready) return CW_OK;
+  hipError_t e = hipSuccess;
+  int made = 0;
+  auto undo = [&]() {
+    for (int i = 0; i < made; ++i) {
+      (void)hipHostFree(st.slots[i].host);
+      if (st.slots[i].ev) (void)hipEventDestroy(st.slots[i].ev);
+      st.slots[i] = StagingSlot{};
+    }
+  };
+  for (; made < kStagingSlots; ++made) {
+    StagingSlot& s = st.slots[made];
+    e = hipHostMalloc(&s.host, kStagingSlotBytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      s.host = nullptr;
+      undo();
+      return hip_fail(e, "hipHostMalloc of the plan staging ring");
+    }
+    g_pinned_allocs.fetch_add(1);
+    // The event only tells the host that the upload kernel has finished reading
+    // the slot; it needs no system-scope fence (by default an L2 write-back and
+    // invalidate, which held the next kernel back by ~5 us and left it a cold L2).
+    e = hipHostGetDevicePointer(&s.dev, s.host, 0);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming | hipEventDisableSystemFence);
+    if (e != hipSuccess) {
+      ++made;
+      undo();
+      return hip_fail(e, "staging slot set-up");
+    }
+  }
+  st.next_slot = 0;
+  st.ready = true;
+  return CW_OK;
+}
+
+cw_status_t current_state(DeviceState** out) {
+  int dev = -1;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(CW_ERR_HIP, "device index %d out of range", dev);
+  *out = &g_devices[dev];
+  return CW_OK;
+}
+
 // Copies `bytes` of host data to `dst` on `stream` through a pinned staging
 // slot, so that the copy is asynchronous and the caller's host buffer can be
 // reused at once.  A slot is reused only after its previous copy completed.
 // `fill(host)` writes the `bytes` bytes into the slot (the plan is packed there
-// directly, without an intermediate buffer).
+// directly, without an intermediate buffer).  The ring is set up on the first
+// use on a device when cw_init has not done it.
 template <class Fill>
 cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill) {
   if (bytes == 0) return CW_OK;
-  int dev = -1;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  if (dev < 0 || dev >= kMaxDevices) return fail(CW_ERR_HIP, "device index %d out of range", dev);
-  DeviceState& st = g_devices[dev];
+  if (bytes > kStagingSlotBytes)
+    return fail(CW_ERR_UNSUPPORTED,
+                "the call's plan takes %zu bytes, more than the %zu-byte staging slot "
+                "(too many sequences or work items for one call)",
+                bytes, kStagingSlotBytes);
+  DeviceState* stp = nullptr;
+  cw_status_t s0 = current_state(&stp);
+  if (s0 != CW_OK) return s0;
+  DeviceState& st = *stp;
   std::lock_guard<std::mutex> g(st.staging_mu);
+  if (!st.ready) {
+    s0 = init_locked(st);
+    if (s0 != CW_OK) return s0;
+  }
   StagingSlot& s = st.slots[st.next_slot];
   st.next_slot = (st.next_slot + 1) % kStagingSlots;
-  if (s.ev == nullptr) {
-    // The event only tells the host that the upload kernel has finished reading
-    // the slot; it needs no system-scope fence (by default an L2 write-back and
-    // invalidate, which held the next kernel back by ~5 us and left it a cold L2).
-    e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming | hipEventDisableSystemFence);
-    if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
-  }
+  hipError_t e = hipSuccess;
   if (s.pending) {
     e = hipEventSynchronize(s.ev);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
     s.pending = false;
-  }
-  if (s.cap < bytes) {
-    if (s.host) (void)hipHostFree(s.host);
-    s.host = nullptr;
-    s.cap = 0;
-    const size_t cap = std::max<size_t>(bytes, size_t(1) << 20);
-    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
-    if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
-    e = hipHostGetDevicePointer(&s.dev, s.host, 0);
-    if (e != hipSuccess) {
-      (void)hipHostFree(s.host);
-      s.host = nullptr;
-      return hip_fail(e, "hipHostGetDevicePointer");
-    }
-    s.cap = cap;
   }
   fill(static_cast<uint8_t*>(s.host));
   e = launch_stage_copy(s.dev, dst, bytes, stream);
@@ -268,12 +309,12 @@ int64_t sum_suffix(const int32_t* ls, int32_t num_seqs) {
   return t;
 }
 
-// Both pool dtypes run the LDS-staged kernel: LDS_BLOCK_M rows per work item,
-// one workgroup per CU.
+// Both pool dtypes run the LDS-staged kernel with the same row block
+// (LDS_BLOCK_M rows per work item, one workgroup per CU), so the extend plan
+// does not depend on the pool dtype.
 ExtendPlan make_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, int32_t num_kv_heads,
-                     int32_t gqa_group, int32_t head_dim, cw_kv_dtype_t kv_dtype,
-                     const int32_t* cu_rows = nullptr, const int32_t* bt_rows = nullptr) {
-  (void)kv_dtype;
+                     int32_t gqa_group, int32_t head_dim, const int32_t* cu_rows = nullptr,
+                     const int32_t* bt_rows = nullptr) {
   int32_t cus = 256, xcds = 8;
   device_shape(&cus, &xcds);
   return build_extend_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, LDS_BLOCK_M, 1,
@@ -329,7 +370,7 @@ StepPlan make_step_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, 
   }
   if (!sp.ext.empty())
     sp.ext_plan = make_plan(lp_e.data(), ls_e.data(), static_cast<int32_t>(sp.ext.size()), num_kv_heads,
-                            gqa_group, head_dim, kv_dtype, cu_e.data(), sp.ext.data());
+                            gqa_group, head_dim, cu_e.data(), sp.ext.data());
   if (!sp.dec.empty())
     sp.dec_plan = make_decode_plan(lp_d.data(), static_cast<int32_t>(sp.dec.size()), num_kv_heads,
                                    gqa_group, head_dim, page_size, kv_dtype, cu_d.data(), sp.dec.data());
@@ -387,7 +428,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   if ((reinterpret_cast<uintptr_t>(block_table) & 3u)) return fail(CW_ERR_ALIGN, "block_table not 4-byte aligned");
 
   ExtendPlan plan = decode ? make_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype)
-                           : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype);
+                           : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim);
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
   s = check_attention_alias(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table,
@@ -781,15 +822,13 @@ cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool
 
 size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                  int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                                 int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype) {
+                                 int32_t head_dim, int32_t page_size) {
   if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
-  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
   if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
                  head_dim, false) != CW_OK)
     return 0;
   if (num_seqs == 0) return 256;
-  return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype)
-      .total_bytes;
+  return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim).total_bytes;
 }
 
 cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_new,
@@ -882,6 +921,16 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
                      out, lse, workspace, workspace_bytes, stream, true, false);
 }
 
+cw_status_t cw_init(void) {
+  DeviceState* st = nullptr;
+  const cw_status_t s = current_state(&st);
+  if (s != CW_OK) return s;
+  std::lock_guard<std::mutex> g(st->staging_mu);
+  return init_locked(*st);
+}
+
+int64_t cw_pinned_allocations(void) { return g_pinned_allocs.load(); }
+
 cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
   if (value < 0) return fail(CW_ERR_UNSUPPORTED, "tuning value %d is negative", value);
   std::lock_guard<std::mutex> g(g_tuning_mu);
@@ -902,15 +951,13 @@ cw_status_t cw_set_timing_events(hipEvent_t start, hipEvent_t stop) {
 
 int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
-                             int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype,
-                             int32_t* items_out, int64_t capacity) {
+                             int32_t head_dim, int32_t page_size, int32_t* items_out,
+                             int64_t capacity) {
   if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return -1;
-  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return -1;
   if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
                  head_dim, false) != CW_OK)
     return -1;
-  ExtendPlan plan =
-      make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, kv_dtype);
+  ExtendPlan plan = make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim);
   const int64_t n = static_cast<int64_t>(plan.items.size());
   if (items_out) {
     for (int64_t i = 0; i < std::min(n, capacity); ++i) {
@@ -940,6 +987,6 @@ const char* cw_status_string(cw_status_t status) {
 
 const char* cw_last_error_message(void) { return g_last_error.c_str(); }
 
-int32_t cw_version(void) { return 101; }
+int32_t cw_version(void) { return 200; }
 
 }  // extern "C"

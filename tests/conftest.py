@@ -42,3 +42,20 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Error against tolerance of every GPU comparison of the run (largest first by
+    share of the bound), so the headroom shows even in a quiet (-q) run."""
+    try:
+        from gpu_util import MARGINS
+    except Exception:  # pragma: no cover
+        return
+    if not MARGINS:
+        return
+    tr = terminalreporter
+    tr.section("parity margins (error / bound)")
+    rows = sorted(MARGINS, key=lambda r: -(r[2] / r[3] if r[3] else 0.0))
+    for what, n, mx, mxb, mean, meanb in rows:
+        mean_s = f"mean {mean:.2e}/{meanb:.0e}" if meanb else f"mean {mean:.2e}"
+        tr.write_line(f"{mx / mxb:6.1%} of max  max {mx:.2e}/{mxb:.0e}  {mean_s}  n={n}  {what}")

@@ -49,6 +49,11 @@ def as_f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().cpu().to(torch.float64).numpy()
 
 
+# every comparison of the session, (what, n, max_abs, bound, mean_abs, bound), printed
+# as one table at the end of the run (tests/conftest.py) so the headroom shows
+MARGINS = []
+
+
 def assert_close(got: np.ndarray, ref: np.ndarray, max_abs: float, mean_abs: float = None, what=""):
     assert got.shape == ref.shape, (got.shape, ref.shape)
     bad = ~np.isfinite(got)
@@ -60,6 +65,7 @@ def assert_close(got: np.ndarray, ref: np.ndarray, max_abs: float, mean_abs: flo
     err = np.abs(got - ref)
     mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
     print(f"[{what}] max_abs={mx:.3e} mean_abs={mean:.3e} n={err.size}", flush=True)
+    MARGINS.append((what, int(err.size), mx, max_abs, mean, mean_abs))
     assert mx <= max_abs, f"{what}: max abs error {mx:.3e} > {max_abs:.1e}"
     if mean_abs is not None:
         assert mean <= mean_abs, f"{what}: mean abs error {mean:.3e} > {mean_abs:.1e}"

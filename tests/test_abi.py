@@ -140,10 +140,10 @@ def test_write_pages_validation():
 def test_workspace_query_rejects_bad_args():
     lp = np.array([5], dtype=np.int32)
     ls = np.array([-1], dtype=np.int32)
-    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, ls.ctypes.data, 1, 1, 1, 64, 16, 0) == 0
-    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 72, 16, 0) == 0
-    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16, 7) == 0
-    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16, 0) > 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, ls.ctypes.data, 1, 1, 1, 64, 16) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 72, 16) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 24) == 0
+    assert lib().cw_extend_workspace_bytes(lp.ctypes.data, lp.ctypes.data, 1, 1, 1, 64, 16) > 0
     assert lib().cw_decode_workspace_bytes(lp.ctypes.data, 1, 1, 1, 64, 16, 7) == 0
     assert lib().cw_decode_workspace_bytes(lp.ctypes.data, 1, 1, 1, 72, 16, 0) == 0
     assert lib().cw_decode_workspace_bytes(ls.ctypes.data, 1, 1, 1, 64, 16, 0) == 0
@@ -303,3 +303,16 @@ def test_decode_output_alias_is_rejected():
         None, _BASES["block_table"], 4, 100, lp.ctypes.data, 2, 2, 4, 128, 16, 0.088, 0,
         _BASES["k_new"] + 128, None, _BASES["workspace"], 1 << 24, None)
     assert r == L.CW_ERR_ALIAS and b"k_new" in lib().cw_last_error_message()
+
+
+def test_plan_larger_than_a_staging_slot_is_rejected_before_any_gpu_work():
+    # 20000 one-token decodes x 8 kv heads = 160000 work items: a 5 MB plan, more than
+    # one 4 MiB staging slot (the ring is never grown)
+    n = 20000
+    lp = np.zeros(n, dtype=np.int32)
+    gb = 1 << 30
+    st = lib().cw_decode_attention(FAKE, FAKE + gb, FAKE + 2 * gb, FAKE + 3 * gb, FAKE + 4 * gb,
+                                   None, None, FAKE + 5 * gb, 1, 1, lp.ctypes.data, n, 8, 4, 128,
+                                   16, 0.088, 0, FAKE + 6 * gb, None, FAKE + 7 * gb, 1 << 29, None)
+    assert st == L.CW_ERR_UNSUPPORTED
+    assert "staging slot" in lib().cw_last_error_message().decode()

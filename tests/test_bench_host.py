@@ -29,13 +29,21 @@ def test_smi_report_without_fields():
     assert bench.parse_smi_metric(None) == (None, None)
 
 
-def test_committed_traffic_matches_the_kernel_sources():
-    # every committed summary carries the hash of the kernel source it was taken on;
-    # the bench reports its bytes only while that source is unchanged
+def test_committed_traffic_is_tied_to_the_kernel_sources():
+    # every committed summary carries the bytes per launch and the hash of the kernel
+    # source it was taken on; the bench reports the bytes only while that source is
+    # unchanged, else null
+    import hashlib
+    import re
     for kind, wl in (("bf16", "turn"), ("bf16", "long"), ("bf16", "batch16"), ("fp8", "mixed"),
                      ("decode", "decode")):
-        t = bench.measured_traffic(kind, wl)
-        assert t is not None and t > 0, (kind, wl)
+        kernel, src, prof = bench.KERNEL_SOURCES[kind]
+        text = open(os.path.join(ROOT, "profiles", prof.format(wl=wl))).read()
+        m = re.search(r"traffic_bytes_per_launch=(\d+) kernel_source_sha256=([0-9a-f]{64})", text)
+        assert m and int(m.group(1)) > 0, (kind, wl)
+        sha = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
+        want = int(m.group(1)) if m.group(2) == sha else None
+        assert bench.measured_traffic(kind, wl) == want, (kind, wl)
     assert bench.measured_traffic("bf16", "no_such_workload") is None
 
 

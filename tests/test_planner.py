@@ -5,12 +5,12 @@ import pytest
 import paper_2606_16824_amd as cwlib
 
 BN = 64
-BM = {"bf16": 256, "fp8": 256}  # rows per work item of each pool dtype's kernel
+BM = 256  # packed query rows per work item (both pool dtypes)
 
 
-def check_plan(lp, ls, hkv, g, d=128, p=16, dt="bf16"):
-    items = cwlib.plan_items(lp, ls, hkv, g, d, p, dt)
-    bm = BM[dt]
+def check_plan(lp, ls, hkv, g, d=128, p=16):
+    items = cwlib.plan_items(lp, ls, hkv, g, d, p)
+    bm = BM
     real = items[items[:, 0] >= 0]
     # every (seq, kv head, query tile) key range [0, kv_len) is covered exactly once
     cover = {}
@@ -40,21 +40,19 @@ def check_plan(lp, ls, hkv, g, d=128, p=16, dt="bf16"):
 
 
 def test_turn_plan_fills_every_cu():
-    # 256-row items, one resident per CU, for both pool dtypes
-    for dt, n in (("bf16", 256), ("fp8", 256)):
-        items = check_plan([16384], [1024], 8, 4, dt=dt)
-        assert len(items) == n
-        # XCD-aware: workgroup i runs on XCD i % 8; all work of a kv head on one XCD
-        for x in range(8):
-            assert len(set(items[x::8, 1].tolist())) == 1
+    # 256-row items, one resident per CU
+    items = check_plan([16384], [1024], 8, 4)
+    assert len(items) == 256
+    # XCD-aware: workgroup i runs on XCD i % 8; all work of a kv head on one XCD
+    for x in range(8):
+        assert len(set(items[x::8, 1].tolist())) == 1
 
 
 def test_long_plan_is_unsplit_and_head_aligned():
-    for dt, n in (("bf16", 2048), ("fp8", 2048)):
-        items = check_plan([131072], [8192], 8, 8, p=64, dt=dt)
-        assert len(items) == n and np.all(items[:, 5] == -1)
-        for x in range(8):
-            assert len(set(items[x::8, 1].tolist())) == 1
+    items = check_plan([131072], [8192], 8, 8, p=64)
+    assert len(items) == 2048 and np.all(items[:, 5] == -1)
+    for x in range(8):
+        assert len(set(items[x::8, 1].tolist())) == 1
 
 
 @pytest.mark.parametrize("lp,ls,hkv,g", [
@@ -64,15 +62,14 @@ def test_long_plan_is_unsplit_and_head_aligned():
     ([5000, 30000, 12000], [1, 1, 1], 8, 4),
     ([100] * 40, [300] * 40, 4, 2),
 ])
-@pytest.mark.parametrize("dt", ["bf16", "fp8"])
-def test_plan_coverage(lp, ls, hkv, g, dt):
-    check_plan(np.array(lp), np.array(ls), hkv, g, dt=dt)
+def test_plan_coverage(lp, ls, hkv, g):
+    check_plan(np.array(lp), np.array(ls), hkv, g)
 
 
 def test_forced_chunking():
     cwlib.set_tuning(0, 3)
     try:
-        items = check_plan(np.array([700]), np.array([150]), 2, 4, dt="fp8")
+        items = check_plan(np.array([700]), np.array([150]), 2, 4)
         real = items[items[:, 0] >= 0]
         assert np.all(real[:, 4] - real[:, 3] <= 3 * BN)
     finally:
