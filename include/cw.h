@@ -37,8 +37,9 @@
  * workspace.  Per device the library keeps a cache of device properties, a
  * pinned host staging ring for the per-call plan (8 slots of 4 MiB, allocated
  * once by cw_init or by the first call that needs it, never grown or freed;
- * a call whose plan exceeds a slot fails with CW_ERR_UNSUPPORTED).  No call
- * allocates device or pinned memory after that one-time set-up.  All work is
+ * a call whose plan exceeds a slot fails with CW_ERR_UNSUPPORTED) and the
+ * static scratch array of cw_extend_attention_noalloc.  No call allocates
+ * device or pinned memory after that one-time set-up.  All work is
  * enqueued on `stream`; returning CW_OK means enqueued, not finished; buffers
  * must stay valid until the stream has passed the work.  Calls on one stream
  * may share one workspace; calls that may run concurrently need separate ones.
@@ -79,6 +80,7 @@ typedef enum {
   CW_ERR_WORKSPACE = 5,   /* workspace_bytes smaller than the matching *_workspace_bytes() */
   CW_ERR_HIP = 6,         /* a HIP runtime call failed while enqueuing */
   CW_ERR_ALIAS = 7,       /* out or lse overlaps an input, the workspace or each other */
+  CW_ERR_INIT = 8,        /* cw_extend_attention_noalloc before cw_init on this device */
   CW_STATUS_RANGE_MIN_ = -2147483647 - 1,
   CW_STATUS_RANGE_MAX_ = 2147483647
 } cw_status_t;
@@ -133,6 +135,32 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
                                 int32_t head_dim, int32_t page_size, float softmax_scale,
                                 cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream);
+
+/* For callers that cannot allocate (code under HIP graph capture, serving
+ * loops or harnesses that forbid hipMalloc): cw_extend_attention without a
+ * workspace argument.  The work list and split-K partials live in a static
+ * device array of CW_NOALLOC_SCRATCH_BYTES per GPU, held until the process
+ * ends; the call allocates nothing (no hipMalloc, hipFree or pinned memory),
+ * so cw_init() must have been called on the current device first, else
+ * CW_ERR_INIT.  A call whose plan needs more scratch than the array holds
+ * (cw_extend_workspace_bytes of its lengths > CW_NOALLOC_SCRATCH_BYTES) fails
+ * with CW_ERR_WORKSPACE before anything is enqueued.  Every call on one GPU
+ * shares that GPU's array: calls that may overlap on one GPU (different
+ * streams, or different host threads) race and give wrong results; calls
+ * ordered on one stream are safe.  Nothing in the array needs to start at
+ * zero (each call uploads its plan and writes every partial it reads).
+ * Results are bit-identical to cw_extend_attention with the same arguments. */
+#define CW_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+cw_status_t cw_extend_attention_noalloc(const void* q, const void* k_new, const void* v_new,
+                                        const void* k_pool, const void* v_pool,
+                                        const float* k_scale, const float* v_scale,
+                                        const int32_t* block_table, int32_t bt_stride,
+                                        int32_t num_pages, const int32_t* prefix_lens_h,
+                                        const int32_t* suffix_lens_h, int32_t num_seqs,
+                                        int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                        int32_t page_size, float softmax_scale,
+                                        cw_kv_dtype_t kv_dtype, void* out, float* lse,
+                                        hipStream_t stream);
 
 /* cw_kv_write_pages and cw_extend_attention of the same arguments in one
  * launch (the extend kernel's workgroups scatter the new K/V into the pools
@@ -285,7 +313,9 @@ int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix
                              int64_t capacity);
 
 /* One-time set-up of the current device: allocates the pinned plan staging
- * ring.  Idempotent; every other call does it on first use.  CW_ERR_HIP on failure
+ * ring (which every other call otherwise does on first use) and resolves this
+ * device's copy of the static scratch array of cw_extend_attention_noalloc
+ * (which requires this call).  Idempotent.  CW_ERR_HIP on failure
  * (nothing stays allocated then, and the call can be repeated). */
 cw_status_t cw_init(void);
 

@@ -33,7 +33,7 @@ import torch
 
 from . import _lib as L
 
-__all__ = ["CWError", "init", "pinned_allocations", "extend_attention", "write_extend_attention", "decode_attention", "kv_write_pages",
+__all__ = ["CWError", "init", "pinned_allocations", "extend_attention", "extend_attention_noalloc", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
            "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
            "step_attention", "step_workspace_bytes", "check_block_table", "ceiling_mfma_bf16", "ceiling_stream_read",
@@ -242,6 +242,25 @@ def extend_attention(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, 
         _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
         len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),
         _dptr(lse), _dptr(workspace), workspace.numel(), _stream()))
+    return out
+
+
+def extend_attention_noalloc(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,
+                             gqa_group, softmax_scale, k_scale=None, v_scale=None, out=None,
+                             lse=None):
+    """extend_attention with the library's static scratch instead of a workspace
+    (cw_extend_attention_noalloc; init() must have run on this device).  With
+    `out` given, the call allocates nothing."""
+    lp, ls = _lens_pair(prefix_lens, suffix_lens)
+    num_pages, hkv, page, d = _check_call(q, k_new, v_new, k_pool, v_pool, block_table, len(lp),
+                                          int(ls.sum()), gqa_group, k_scale, v_scale, out, lse)
+    if out is None:
+        out = torch.empty_like(q)
+    _check(library().cw_extend_attention_noalloc(
+        _dptr(q), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale),
+        _dptr(v_scale), _dptr(block_table), block_table.shape[1], num_pages, _ptr(lp), _ptr(ls),
+        len(lp), hkv, gqa_group, d, page, float(softmax_scale), _kv_dtype(k_pool), _dptr(out),
+        _dptr(lse), _stream()))
     return out
 
 

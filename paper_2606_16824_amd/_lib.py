@@ -52,6 +52,9 @@ SIGNATURES = {
     "cw_set_timing_events": (C.c_int, [_vp, _vp]),
     "cw_extend_plan_items": (C.c_int64, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, C.c_int64]),
     "cw_init": (C.c_int, []),
+    "cw_extend_attention_noalloc": (C.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
+                                              _vp, _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int,
+                                              _vp, _vp, _vp]),
     "cw_pinned_allocations": (C.c_int64, []),
     "cw_status_string": (C.c_char_p, [C.c_int]),
     "cw_last_error_message": (C.c_char_p, []),

@@ -16,6 +16,12 @@
 #include "cw_internal.h"
 #include "planner.h"
 
+// Scratch memory of cw_extend_attention_noalloc (plan and split-K partials):
+// every GPU the library runs on holds its own copy until the process ends.  In
+// host code this name is only a stand-in; kernels get the device address that
+// hipGetSymbolAddress returns for the current device (DeviceState::scratch).
+static __device__ __align__(256) uint8_t scratch[CW_NOALLOC_SCRATCH_BYTES];
+
 namespace cw {
 namespace {
 
@@ -73,6 +79,7 @@ struct DeviceState {
   bool ready = false;     // staging ring allocated
   StagingSlot slots[kStagingSlots];
   int next_slot = 0;
+  uint8_t* scratch = nullptr;  // this device's copy of the static scratch array (cw_init)
 };
 
 DeviceState g_devices[kMaxDevices];
@@ -164,9 +171,11 @@ cw_status_t current_state(DeviceState** out) {
 // reused at once.  A slot is reused only after its previous copy completed.
 // `fill(host)` writes the `bytes` bytes into the slot (the plan is packed there
 // directly, without an intermediate buffer).  The ring is set up on the first
-// use on a device when cw_init has not done it.
+// use on a device when cw_init has not done it, unless `no_alloc` is set, in
+// which case an uninitialised device is an error (CW_ERR_INIT).
 template <class Fill>
-cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill) {
+cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
+                        bool no_alloc = false) {
   if (bytes == 0) return CW_OK;
   if (bytes > kStagingSlotBytes)
     return fail(CW_ERR_UNSUPPORTED,
@@ -179,6 +188,7 @@ cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill
   DeviceState& st = *stp;
   std::lock_guard<std::mutex> g(st.staging_mu);
   if (!st.ready) {
+    if (no_alloc) return fail(CW_ERR_INIT, "cw_init() has not been called on this device");
     s0 = init_locked(st);
     if (s0 != CW_OK) return s0;
   }
@@ -404,7 +414,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
                         int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
                         int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype, void* out,
                         float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
-                        bool decode, bool write_pages) {
+                        bool decode, bool write_pages, bool no_alloc = false) {
   cw_status_t s = check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size);
   if (s != CW_OK) return s;
   s = check_dtype(kv_dtype, k_scale, v_scale);
@@ -429,6 +439,9 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
 
   ExtendPlan plan = decode ? make_decode_plan(lp, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype)
                            : make_plan(lp, ls, num_seqs, num_kv_heads, gqa_group, head_dim);
+  if (no_alloc && plan.total_bytes > workspace_bytes)
+    return fail(CW_ERR_WORKSPACE, "the call needs %zu bytes of scratch; the static scratch array holds %zu",
+                plan.total_bytes, workspace_bytes);
   if (workspace == nullptr || workspace_bytes < plan.total_bytes)
     return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, plan.total_bytes);
   s = check_attention_alias(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table,
@@ -437,7 +450,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   if (s != CW_OK) return s;
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  s = upload_fill(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); });
+  s = upload_fill(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); }, no_alloc);
   if (s != CW_OK) return s;
 
   ExtendParams p{};
@@ -923,10 +936,45 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
 
 cw_status_t cw_init(void) {
   DeviceState* st = nullptr;
-  const cw_status_t s = current_state(&st);
+  cw_status_t s = current_state(&st);
   if (s != CW_OK) return s;
   std::lock_guard<std::mutex> g(st->staging_mu);
-  return init_locked(*st);
+  s = init_locked(*st);
+  if (s != CW_OK || st->scratch != nullptr) return s;
+  // this device's copy of the scratch array: the name is a host-side stand-in,
+  // the address the runtime returns (with this device current) is the one kernels use
+  void* ptr = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(::scratch));
+  if (e != hipSuccess || ptr == nullptr)
+    return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)");
+  st->scratch = static_cast<uint8_t*>(ptr);
+  return CW_OK;
+}
+
+cw_status_t cw_extend_attention_noalloc(const void* q, const void* k_new, const void* v_new,
+                                        const void* k_pool, const void* v_pool,
+                                        const float* k_scale, const float* v_scale,
+                                        const int32_t* block_table, int32_t bt_stride,
+                                        int32_t num_pages, const int32_t* prefix_lens_h,
+                                        const int32_t* suffix_lens_h, int32_t num_seqs,
+                                        int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
+                                        int32_t page_size, float softmax_scale,
+                                        cw_kv_dtype_t kv_dtype, void* out, float* lse,
+                                        hipStream_t stream) {
+  DeviceState* st = nullptr;
+  const cw_status_t s = current_state(&st);
+  if (s != CW_OK) return s;
+  uint8_t* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> g(st->staging_mu);
+    if (!st->ready || st->scratch == nullptr)
+      return fail(CW_ERR_INIT, "cw_init() has not been called on this device");
+    ws = st->scratch;
+  }
+  return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
+                     v_scale, block_table, bt_stride, num_pages, prefix_lens_h, suffix_lens_h,
+                     num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
+                     out, lse, ws, CW_NOALLOC_SCRATCH_BYTES, stream, false, false, true);
 }
 
 int64_t cw_pinned_allocations(void) { return g_pinned_allocs.load(); }
@@ -980,6 +1028,7 @@ const char* cw_status_string(cw_status_t status) {
     case CW_ERR_WORKSPACE: return "CW_ERR_WORKSPACE: workspace too small";
     case CW_ERR_HIP: return "CW_ERR_HIP: HIP runtime error";
     case CW_ERR_ALIAS: return "CW_ERR_ALIAS: an output overlaps an input or the workspace";
+    case CW_ERR_INIT: return "CW_ERR_INIT: cw_init() has not been called on the current device";
     default: break;
   }
   return "unknown cw_status_t";
