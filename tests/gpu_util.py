@@ -70,3 +70,21 @@ def assert_close(got: np.ndarray, ref: np.ndarray, max_abs: float, mean_abs: flo
     if mean_abs is not None:
         assert mean <= mean_abs, f"{what}: mean abs error {mean:.3e} > {mean_abs:.1e}"
     return mx, mean
+
+
+def assert_within_bf16_ulps(got: np.ndarray, ref: np.ndarray, ulps: int = 2, what=""):
+    """Two bf16 results of the same quantity computed in different orders (another
+    split of the keys, another kernel): |got - ref| <= `ulps` bf16 ulps of the larger
+    magnitude, taken at least at 0.5 (so values below 1 get 2^-7 with ulps = 2)."""
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.isfinite(got).all(), f"{what}: non-finite GPU output"
+    mag = np.maximum(np.maximum(np.abs(got), np.abs(ref)), 0.5)
+    bound = ulps * np.exp2(np.floor(np.log2(mag)) - 7)  # bf16 keeps 8 significant bits
+    ratio = np.abs(got - ref) / bound
+    worst = float(ratio.max()) if ratio.size else 0.0
+    err = np.abs(got - ref)
+    print(f"[{what}] max_abs={float(err.max()) if err.size else 0.0:.3e} "
+          f"worst {worst:.2f} of {ulps} ulps n={err.size}", flush=True)
+    MARGINS.append((what + f" (in units of {ulps} bf16 ulps)", int(err.size), worst, 1.0,
+                    float(err.mean()) if err.size else 0.0, None))
+    assert worst <= 1.0, f"{what}: difference above {ulps} bf16 ulps (worst {worst:.2f})"
