@@ -56,6 +56,9 @@ def parse():
                     help="skip the host KV-block policy comparison added to an extend run")
     ap.add_argument("--no-swap", dest="swap", action="store_false",
                     help="skip the page swap measurement added to an extend run")
+    ap.add_argument("--extend-kernel", type=int, default=0, choices=[0, 1, 2],
+                    help="extend kernel for bf16 pools: 0 or 1 eight waves of 32 rows (default), "
+                         "2 four waves of 64 rows")
     ap.add_argument("--separate-calls", action="store_true",
                     help="time a step as cw_kv_write_pages + cw_extend_attention (or "
                          "cw_decode_attention) instead of cw_step_attention")
@@ -89,6 +92,8 @@ def calibrate_copy(mib: int):
     torch.cuda.synchronize()
     print(json.dumps({"calibration": "copy", "bytes_read": n, "bytes_written": n, "launches": 3}))
 
+
+EXTEND_KERNEL = 0  # --extend-kernel
 
 KERNEL_SOURCES = {  # dominant kernel per pool dtype: (kernel, source, profile summary)
     "bf16": ("extend_lds_kernel", "paper_2606_16824_amd/csrc/kernels/extend_lds.hip", "extend_lds_{wl}.md"),
@@ -383,6 +388,8 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
         host.append(time.perf_counter() - t0)
     torch.cuda.synchronize()
     kernel = "decode_kernel" if decode else KERNEL_SOURCES[s.kv_dtype][0]
+    if not decode and s.kv_dtype == "bf16" and EXTEND_KERNEL == 2:
+        kernel = "extend_w64_kernel"
     res = {"spec": s, "workload": w, "ms": ms, "kern_ms": float(kern.mean()),
            "kern_ms_median": float(np.median(kern)), "kern_ms_min": float(kern.min()),
            "host_us": float(np.median(host)) * 1e6, "kernel": kernel}
@@ -534,6 +541,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
+    global EXTEND_KERNEL
+    EXTEND_KERNEL = args.extend_kernel
+    cwlib.set_tuning(cwlib._lib.CW_TUNE_EXTEND_KERNEL, args.extend_kernel)
     res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,
                        cold_steps=args.cold_steps, power_s=args.power_seconds)
     ceil = measure_ceilings(power_s=args.power_seconds) if args.ceilings else None
@@ -557,7 +567,7 @@ def main():
         achieved = flops / (kern_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": measured_traffic(s.kv_dtype, args.workload),
+                "traffic": measured_traffic(s.kv_dtype, args.workload) if EXTEND_KERNEL != 2 else None,
                 "kernel": res["kernel"], "kernel_ms": round(kern_ms, 5)}
         rate = lambda t: flops / (t * 1e-3) / 1e12
         ceil_key = "mfma_bf16_TFLOP_s"

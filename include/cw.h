@@ -282,10 +282,15 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           range into chunks of n 64-key tiles.
  *   CW_TUNE_TARGET_WGS      0 = automatic; n > 0 = split-K until at least n
  *                           workgroups are launched.
+ *   CW_TUNE_EXTEND_KERNEL   0 or 1 = eight waves of 32 query rows per work
+ *                           item (the default), 2 = four waves of 64 rows
+ *                           (bf16 pools only; fp8 pools always run the
+ *                           eight-wave kernel).
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {
   CW_TUNE_KV_CHUNK_TILES = 0,
   CW_TUNE_TARGET_WGS = 1,
+  CW_TUNE_EXTEND_KERNEL = 2,
   CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
   CW_TUNE_RANGE_MAX_ = 2147483647
 } cw_tune_key_t;

@@ -55,6 +55,15 @@ Tuning current_tuning() {
   return g_tuning;
 }
 
+// Extend kernel: the eight-wave kernel (32 rows per wave) unless the four-wave
+// one (64 rows per wave, bf16 pools only) is asked for.  Both own LDS_BLOCK_M
+// rows per work item, so they share the plan.
+hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
+                         hipStream_t stream) {
+  if (!fp8 && current_tuning().extend_kernel == 2) return launch_extend_w64(p, head_dim, page_size, stream);
+  return launch_extend_lds(p, head_dim, page_size, fp8, stream);
+}
+
 // ---------------------------------------------------------------------------
 // per-device state
 
@@ -501,7 +510,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
   if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
-  else e = launch_extend_lds(p, head_dim, page_size, fp8, stream);
+  else e = launch_extend(p, head_dim, page_size, fp8, stream);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
   if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if (p.n_groups > 0) {
@@ -697,7 +706,7 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     common(pe);
     pe.w = w;  // every sequence's new K/V, written under the extend's first tiles
     if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if ((e = launch_extend_lds(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
+    if ((e = launch_extend(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
       return hip_fail(e, "extend kernel launch");
     if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     if (pe.n_groups > 0) {
@@ -985,6 +994,10 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
   switch (key) {
     case CW_TUNE_KV_CHUNK_TILES: g_tuning.kv_chunk_tiles = value; return CW_OK;
     case CW_TUNE_TARGET_WGS: g_tuning.target_wgs = value; return CW_OK;
+    case CW_TUNE_EXTEND_KERNEL:
+      if (value > 2) return fail(CW_ERR_UNSUPPORTED, "extend kernel %d is not 0, 1 or 2", value);
+      g_tuning.extend_kernel = value;
+      return CW_OK;
     default: break;
   }
   return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));

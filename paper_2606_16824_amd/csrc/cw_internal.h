@@ -120,6 +120,7 @@ void set_last_error(const char* msg);
 // Kernel launchers (each defined in the translation unit of its kernel).
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                              hipStream_t stream);
+hipError_t launch_extend_w64(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream);
 hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream);
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream);

@@ -13,6 +13,7 @@ namespace cw {
 struct Tuning {
   int32_t kv_chunk_tiles = 0;  // 0 = automatic
   int32_t target_wgs = 0;      // 0 = automatic
+  int32_t extend_kernel = 0;   // 0 = automatic, 1 = eight waves of 32 rows, 2 = four waves of 64 rows
 };
 
 struct ExtendPlan {

@@ -156,6 +156,11 @@ def test_tuning_keys():
     assert lib().cw_set_tuning(9, 1) == L.CW_ERR_UNSUPPORTED
     assert lib().cw_set_tuning(0, 0) == L.CW_OK
     assert lib().cw_set_tuning(1, 0) == L.CW_OK
+    # extend kernel choice: 0/1 eight waves, 2 four waves of 64 rows, nothing else
+    for v in (0, 1, 2):
+        assert lib().cw_set_tuning(L.CW_TUNE_EXTEND_KERNEL, v) == L.CW_OK
+    assert lib().cw_set_tuning(L.CW_TUNE_EXTEND_KERNEL, 3) == L.CW_ERR_UNSUPPORTED
+    assert lib().cw_set_tuning(L.CW_TUNE_EXTEND_KERNEL, 0) == L.CW_OK
 
 
 def _swap(out=True, **over):
