@@ -24,19 +24,21 @@
 //
 //  * Buffer-addressed staging.  The page base sits in a scalar buffer
 //    descriptor and each lane's offset within the page is a constant register.
-//    bf16 rows travel from HBM straight into LDS (buffer_load_dwordx4 ... lds);
-//    fp8-e4m3fn pool rows are loaded into registers one iteration ahead,
-//    widened exactly to bf16 (every e4m3fn value is a bf16 value) and stored to
-//    the same LDS layout, each lane converting only the 16 bytes it loaded, so
-//    the compute loop is the same for both pool dtypes.
+//    bf16 rows travel from HBM straight into LDS (buffer_load_dwordx4 ... lds).
 //
-// fp8 scales (one K and one V scale per (page, kv head)) never touch the
-// tiles: the K scale multiplies a page's scores and log2 of the V scale is
-// added to their exponent, so P arrives already multiplied by the V scale,
-// rounded to bf16 once, and the row sum divides it back out (dot with the
-// bf16-rounded reciprocal).  A 16-key group of a tile lies in one page; per
-// tile, one wave per page computes the group's three numbers and leaves them in
-// a small LDS ring.  A tile straddling the prefix end treats each key on its own.
+// fp8-e4m3fn pools run the same loop in fp16 (v_mfma_f32_32x32x16_f16): pool
+// rows are loaded into registers one iteration ahead and dequantised while they
+// are widened into LDS, code x page scale rounded to fp16 once (the scale's
+// power of two is applied exactly by the conversion, its significand by one
+// packed fp16 multiply per two values), so the loop itself never sees a scale.
+// The new tokens' bf16 rows arrive by DMA like bf16 pool rows, and the wave
+// that staged them converts them to fp16 in place before the barrier that
+// publishes the tile.  Q is scaled into fp16 the same way as into bf16 for bf16
+// pools, and P is rounded to fp16.  fp16 keeps 11 significant bits against
+// bf16's 8, so every rounding of this path is finer than the bf16 path's; the
+// values must lie within the fp16 range (|x| < 65504), which holds for the
+// scaled e4m3fn codes of any page scale below 146 and for the new K/V rows the
+// path is used with.
 //
 // LDS holds K and V rows in their natural [key][dim] order, 16-byte chunks
 // XOR-swizzled per row so that every fragment read is bank-conflict free:
@@ -65,6 +67,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -73,6 +77,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // waiting for them never waits for tile staging issued before them.
 typedef __attribute__((address_space(4))) const int32_t const_i32;
 typedef __attribute__((address_space(4))) const float const_f32;
+constexpr uint32_t kOnePairF16 = 0x3C003C00u;  // fp16 pair (1, 1)
 
 constexpr float kNegBig = -1.0e30f;
 constexpr float kLn2 = 0.69314718055994531f;
@@ -96,16 +101,49 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_void* dst, u
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
 }
 
-// Two e4m3fn codes (bytes 0,1 or 2,3 of `w`) -> two bf16 in one dword, exact
-// (a unit scale leaves the value as it is).
-template <bool HI>
-__device__ __forceinline__ uint32_t fp8x2_bf16x2(uint32_t w) {
-  return __builtin_bit_cast(uint32_t,
-                            __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(static_cast<int>(w), 1.0f, HI));
+// Page scale s = p2 x fm with p2 a positive power of two and |fm| in [1, 2):
+// the conversion applies p2 exactly, fm is rounded to fp16 for the packed
+// multiply (s finite and normal; 0 dequantises to 0).
+struct PageScale {
+  float p2;
+  f16x2 fm;
+};
+__device__ __forceinline__ PageScale page_scale(float s) {
+  const uint32_t b = __float_as_uint(s);
+  const float p2 = __uint_as_float(b & 0x7F800000u);                   // exponent
+  const float f = __uint_as_float((b & 0x807FFFFFu) | 0x3F800000u);    // sign, significand in [1, 2)
+  const _Float16 m = static_cast<_Float16>(f);
+  return PageScale{p2, f16x2{m, m}};
 }
-__device__ __forceinline__ u32x4 fp8x8_bf16x8(uint32_t lo, uint32_t hi) {
-  return u32x4{fp8x2_bf16x2<false>(lo), fp8x2_bf16x2<true>(lo), fp8x2_bf16x2<false>(hi),
-               fp8x2_bf16x2<true>(hi)};
+// Two e4m3fn codes (bytes 0,1 or 2,3 of `w`) -> two fp16 code x s in one dword.
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_f16x2(uint32_t w, PageScale sc) {
+  const f16x2 v = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(static_cast<int>(w), sc.p2, HI);
+  return __builtin_bit_cast(uint32_t, v * sc.fm);
+}
+__device__ __forceinline__ u32x4 fp8x8_f16x8(uint32_t lo, uint32_t hi, PageScale sc) {
+  return u32x4{fp8x2_f16x2<false>(lo, sc), fp8x2_f16x2<true>(lo, sc), fp8x2_f16x2<false>(hi, sc),
+               fp8x2_f16x2<true>(hi, sc)};
+}
+// Eight bf16 -> eight fp16 (exact within the fp16 range: bf16 keeps 8
+// significant bits, fp16 11).
+__device__ __forceinline__ u32x4 bf16x8_f16x8(u32x4 x) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __uint_as_float(x[i] << 16), hi = __uint_as_float(x[i] & 0xFFFF0000u);
+    r[i] = __builtin_bit_cast(uint32_t, f16x2{static_cast<_Float16>(lo), static_cast<_Float16>(hi)});
+  }
+  return r;
+}
+// 32x32x16 MFMA on 16-bit operands held as raw bits: fp16 for fp8 pools, bf16
+// otherwise.
+template <bool F16>
+__device__ __forceinline__ f32x16 mfma16(u32x4 a, u32x4 b, f32x16 c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
 __device__ __forceinline__ int swap_bits_2_3(int r) {
@@ -154,9 +192,6 @@ void extend_lds_kernel(ExtendParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[T::TILE];
-  // fp8: per-tile group numbers, ring of four tiles: [0,4) K scale times the
-  // softmax scale, [4,8) log2 of the V scale, [8,12) 1 / V scale (fp32 bits)
-  __shared__ __attribute__((aligned(16))) uint32_t prm[4][12];
 
   // Fused page write: this workgroup's share of the new rows' 16-byte pieces
   // goes to the pools.  The extend never reads a slot at or past a sequence's
@@ -208,10 +243,11 @@ void extend_lds_kernel(ExtendParams p) {
   }
 
   // Q^T as the B operand: k-step kk holds dims 16 kk + 8 h + [0, 8) of this row.
-  // bf16 pools: Q carries the softmax scale in log2 units (q c rounded to bf16),
-  // so the score MFMAs, started from -m, leave s c - m with no vector work.
+  // Q carries the softmax scale in log2 units (q c rounded to bf16, or to fp16
+  // for fp8 pools), so the score MFMAs, started from -m, leave s c - m with no
+  // vector work.
   const float c = p.scale_log2;
-  bf16x8 qf[T::KT];
+  u32x4 qf[T::KT];
   {
     const uint16_t* qrow =
         static_cast<const uint16_t*>(p.q) + (size_t(sq.cu + t) * hq + size_t(kvh) * G + g) * D;
@@ -219,10 +255,17 @@ void extend_lds_kernel(ExtendParams p) {
     for (int kk = 0; kk < T::KT; ++kk) {
       u32x4 v = {0u, 0u, 0u, 0u};
       if (row_ok) v = *reinterpret_cast<const u32x4*>(qrow + 16 * kk + 8 * h);
-      qf[kk] = __builtin_bit_cast(bf16x8, v);
-      if constexpr (!FP8) {
+      const bf16x8 qb = __builtin_bit_cast(bf16x8, v);
+      if constexpr (FP8) {
+        f16x8 qh;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qf[kk][e] = static_cast<__bf16>(static_cast<float>(qf[kk][e]) * c);
+        for (int e = 0; e < 8; ++e) qh[e] = static_cast<_Float16>(static_cast<float>(qb[e]) * c);
+        qf[kk] = __builtin_bit_cast(u32x4, qh);
+      } else {
+        bf16x8 qs;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qs[e] = static_cast<__bf16>(static_cast<float>(qb[e]) * c);
+        qf[kk] = __builtin_bit_cast(u32x4, qs);
       }
     }
   }
@@ -333,20 +376,33 @@ void extend_lds_kernel(ExtendParams p) {
     }
     return v;
   };
-  // ... widened to bf16 and stored at the swizzled positions of their rows
-  auto store8 = [&](int j0, u32x4 v, uint8_t* dst, bool is_k) __attribute__((always_inline)) {
+  // ... dequantised to fp16 with the page's scale and stored at the swizzled
+  // positions of their rows
+  auto store8 = [&](int j0, u32x4 v, uint8_t* dst, bool is_k, float scale) __attribute__((always_inline)) {
+    if (j0 + wrow0 >= lp) return;
+    const PageScale sc = page_scale(scale);
     if constexpr (T::B8 == 16) {
-      if (j0 + wrow0 < lp) {
-        if (j0 + r8u[0] < lp)
-          *reinterpret_cast<u32x4*>(dst + wrow0 * T::RB + 16 * lane) = fp8x8_bf16x8(v.x, v.y);
-        if (j0 + r8u[1] < lp)
-          *reinterpret_cast<u32x4*>(dst + (wrow0 + 4) * T::RB + 16 * lane) = fp8x8_bf16x8(v.z, v.w);
-      }
-    } else if (j0 + wrow0 < lp && j0 + r8 < lp) {
+      if (j0 + r8u[0] < lp)
+        *reinterpret_cast<u32x4*>(dst + wrow0 * T::RB + 16 * lane) = fp8x8_f16x8(v.x, v.y, sc);
+      if (j0 + r8u[1] < lp)
+        *reinterpret_cast<u32x4*>(dst + (wrow0 + 4) * T::RB + 16 * lane) = fp8x8_f16x8(v.z, v.w, sc);
+    } else if (j0 + r8 < lp) {
       const int swz = is_k ? k_swz<D>(r8) : v_swz<D>(r8);
-      uint8_t* row = dst + r8 * T::RB;
-      {
-        *reinterpret_cast<u32x4*>(row + 16 * (q8 ^ swz)) = fp8x8_bf16x8(v.x, v.y);
+      *reinterpret_cast<u32x4*>(dst + r8 * T::RB + 16 * (q8 ^ swz)) = fp8x8_f16x8(v.x, v.y, sc);
+    }
+  };
+  // fp8 pools: the new tokens' rows of the tile at j0 that this wave staged by
+  // DMA into dst (bf16) are converted to fp16 in place, each lane its own 16
+  // bytes (before the barrier that publishes the tile)
+  auto convert_new = [&](int j0, uint8_t* dst) __attribute__((always_inline)) {
+    const int k_first = j0 + wrow0, k_last = k_first + 7;
+    if (k_last < lp || k_first >= total_len) return;
+#pragma unroll
+    for (int j = 0; j < T::NI; ++j) {
+      const int key = k_first + T::RPI * j + dma_row;
+      if (key >= lp && key < total_len) {
+        u32x4* ptr = reinterpret_cast<u32x4*>(dst + (wrow0 + T::RPI * j) * T::RB + 16 * lane);
+        *ptr = bf16x8_f16x8(*ptr);
       }
     }
   };
@@ -381,50 +437,29 @@ void extend_lds_kernel(ExtendParams p) {
   // limits) keeps m = kNegBig and l = 0, so its partial gets weight 0 in the
   // merge whatever the other chunks' maxima are.
   float m_run = kNegBig, l_run = 0.f;
-  f32x16 negm = f32x16{};  // bf16: -m_run in every element (the score MFMAs' start)
+  f32x16 negm = f32x16{};  // -m_run in every element (the score MFMAs' start)
 
   const int n_tiles = (it.kv_end - it.kv_begin + BLOCK_N - 1) / BLOCK_N;
   auto tile0 = [&](int j) { return it.kv_begin + j * BLOCK_N; };
   auto visible = [&](int j) { return wave_active && tile0(j) < wave_max_lim; };
-  // tile crosses the prefix end: fp8 scales apply key by key
-  auto straddles = [&](int j0) { return j0 < lp && lp < j0 + BLOCK_N; };
 
-  // ---- fp8 group numbers.  Group gi (keys 16 gi .. 16 gi + 15 of a tile) lies
-  // in page (16 gi) / P of the tile; the wave staging the group's first rows
-  // (P = 16: wave 2 gi; P = 64: wave 0 for all four groups) writes them.
+  // ---- fp8 page scales: the wave's rows of a tile lie in one page, so one K
+  // and one V scale per wave and tile (1 where its rows hold no prefix key)
   const_f32* ks_s = (const_f32*)p.k_scale;
   const_f32* vs_s = (const_f32*)p.v_scale;
-  const bool prm_writer = P == 16 ? (wave & 1) == 0 : wave == 0;
-  // this wave's page scales for the tile at j0 (1 where its rows hold no prefix key)
-  auto load_scales = [&](int j0, int pg, float& ksc, float& vsc) __attribute__((always_inline)) {
-    const bool pre = j0 + wrow0 < lp;
-    const size_t si = size_t(pg) * hkv + kvh;
-    ksc = pre ? ks_s[si] : 1.f;
-    vsc = pre ? vs_s[si] : 1.f;
-  };
-  auto write_params = [&](int j0, int slot, float ksc, float vsc) __attribute__((always_inline)) {
-    if (!prm_writer || lane != 0) return;
-    const float cg = c * ksc, lv = __builtin_amdgcn_logf(vsc), iv = 1.f / vsc;
-    const int g0 = P == 16 ? (wave >> 1) : 0, g1 = P == 16 ? g0 + 1 : 4;
-    for (int gi = g0; gi < g1; ++gi) {
-      const bool pre = j0 + 16 * gi < lp;  // any prefix key in the group
-      prm[slot][gi] = __float_as_uint(pre ? cg : c);
-      prm[slot][4 + gi] = __float_as_uint(pre ? lv : 0.f);
-      prm[slot][8 + gi] = __float_as_uint(pre ? iv : 1.f);
-    }
+  auto load_scale = [&](const_f32* tbl, int j0, int pg) -> float {
+    return j0 + wrow0 < lp ? tbl[size_t(pg) * hkv + kvh] : 1.f;
   };
 
-  // scores S^T = K Q^T of the tile in `ks`, two 32-key blocks: raw for fp8
-  // pools, s c - m_run for bf16 pools (scaled Q, accumulation started at -m_run)
+  // scores S^T = K Q^T of the tile in `ks`, two 32-key blocks: s c - m_run
+  // (scaled Q, accumulation started at -m_run)
   auto scores = [&](const uint8_t* ks, f32x16(&s)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int kk = 0; kk < T::KT; ++kk) {
-      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(ks + k_addr[kk]);
-      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(ks + k_addr[kk] + 32 * T::RB);
-      const f32x16 c0 = kk > 0 ? s[0] : FP8 ? f32x16{} : negm;
-      const f32x16 c1 = kk > 0 ? s[1] : FP8 ? f32x16{} : negm;
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[kk], c0, 0, 0, 0);
-      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[kk], c1, 0, 0, 0);
+      const u32x4 k0 = *reinterpret_cast<const u32x4*>(ks + k_addr[kk]);
+      const u32x4 k1 = *reinterpret_cast<const u32x4*>(ks + k_addr[kk] + 32 * T::RB);
+      s[0] = mfma16<FP8>(k0, qf[kk], kk > 0 ? s[0] : negm);
+      s[1] = mfma16<FP8>(k1, qf[kk], kk > 0 ? s[1] : negm);
     }
   };
   // causal mask (only tiles that cross some row's limit).  Element i of block
@@ -439,85 +474,41 @@ void extend_lds_kernel(ExtendParams p) {
           if (j0 + 32 * blk + 16 * (i >> 3) + 8 * h + (i & 7) >= lim) s[blk][i] = -INFINITY;
     }
   };
-  // fp8: log2 units relative to the running max, times the page's K scale,
-  // plus log2 of its V scale (bf16 scores leave the MFMAs in these units)
-  auto to_log2 = [&](int j0, int slot, f32x16(&s)[2], bool edge) __attribute__((always_inline)) {
+  // weights of 16-key slice gi in B-operand order (bf16, fp16 for fp8 pools)
+  // and their half-row sum (of the rounded weights, so numerator and
+  // denominator agree)
+  auto weights = [&](const f32x16(&x)[2], u32x4(&pf)[4], float& lsum) __attribute__((always_inline)) {
+    float la = 0.f, lb = 0.f;
     if constexpr (FP8) {
-      uint32_t cgv[4], lvv[4];
+      const f16x2 one = __builtin_bit_cast(f16x2, kOnePairF16);
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
-        cgv[gi] = prm[slot][gi];
-        lvv[gi] = prm[slot][4 + gi];
-      }
-      if (!(edge && straddles(j0))) {
+        f16x8 w;
 #pragma unroll
-        for (int gi = 0; gi < 4; ++gi) {
-          const float cg = __uint_as_float(cgv[gi]), lo = __uint_as_float(lvv[gi]) - m_run;
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            s[gi >> 1][8 * (gi & 1) + e] = fmaf(s[gi >> 1][8 * (gi & 1) + e], cg, lo);
-        }
-      } else {
-#pragma unroll
-        for (int gi = 0; gi < 4; ++gi)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const bool pre = j0 + 16 * gi + 8 * h + e < lp;
-            s[gi >> 1][8 * (gi & 1) + e] =
-                fmaf(s[gi >> 1][8 * (gi & 1) + e], pre ? __uint_as_float(cgv[gi]) : c,
-                     (pre ? __uint_as_float(lvv[gi]) : 0.f) - m_run);
-          }
-      }
-    }
-  };
-  // bf16 weights of 16-key slice gi in B-operand order, and their half-row sum
-  // (of the rounded weights, so numerator and denominator agree).  fp8: each
-  // weight carries its page's V scale, which the sum divides back out: per
-  // 16-key group the rounded weights are summed, then scaled by 1 / V scale in
-  // fp32 (key by key in a tile straddling the prefix end).
-  auto weights = [&](int j0, int slot, const f32x16(&x)[2], bf16x8(&pf)[4], float& lsum,
-                     bool edge) __attribute__((always_inline)) {
-    const bf16x2 one = __builtin_bit_cast(bf16x2, kOnePair);
-#pragma unroll
-    for (int gi = 0; gi < 4; ++gi)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        pf[gi][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(x[gi >> 1][8 * (gi & 1) + e]));
-    if constexpr (!FP8) {
-      float la = 0.f, lb = 0.f;
-#pragma unroll
-      for (int gi = 0; gi < 4; ++gi)
+        for (int e = 0; e < 8; ++e) w[e] = static_cast<_Float16>(__builtin_amdgcn_exp2f(x[gi >> 1][8 * (gi & 1) + e]));
 #pragma unroll
         for (int e = 0; e < 8; e += 4) {
-          la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, la, false);
-          lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e + 2], pf[gi][e + 3]}, one, lb, false);
+          la = __builtin_amdgcn_fdot2(f16x2{w[e], w[e + 1]}, one, la, false);
+          lb = __builtin_amdgcn_fdot2(f16x2{w[e + 2], w[e + 3]}, one, lb, false);
         }
-      lsum = la + lb;
-    } else {
-      float iv[4];
-#pragma unroll
-      for (int gi = 0; gi < 4; ++gi) iv[gi] = __uint_as_float(prm[slot][8 + gi]);
-      float acc = 0.f;
-      if (!(edge && straddles(j0))) {
-#pragma unroll
-        for (int gi = 0; gi < 4; ++gi) {
-          float la = 0.f, lb = 0.f;
-#pragma unroll
-          for (int e = 0; e < 8; e += 4) {
-            la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e], pf[gi][e + 1]}, one, la, false);
-            lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pf[gi][e + 2], pf[gi][e + 3]}, one, lb, false);
-          }
-          acc = fmaf(la + lb, iv[gi], acc);
-        }
-      } else {
-#pragma unroll
-        for (int gi = 0; gi < 4; ++gi)
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            acc = fmaf(static_cast<float>(pf[gi][e]), j0 + 16 * gi + 8 * h + e < lp ? iv[gi] : 1.f, acc);
+        pf[gi] = __builtin_bit_cast(u32x4, w);
       }
-      lsum = acc;
+    } else {
+      const bf16x2 one = __builtin_bit_cast(bf16x2, kOnePair);
+#pragma unroll
+      for (int gi = 0; gi < 4; ++gi) {
+        bf16x8 w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w[e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(x[gi >> 1][8 * (gi & 1) + e]));
+#pragma unroll
+        for (int e = 0; e < 8; e += 4) {
+          la = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[e], w[e + 1]}, one, la, false);
+          lb = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[e + 2], w[e + 3]}, one, lb, false);
+        }
+        pf[gi] = __builtin_bit_cast(u32x4, w);
+      }
     }
+    lsum = la + lb;
   };
   // row max of x over both halves of the row (lanes l and l + 32)
   auto row_max = [&](const f32x16(&x)[2]) -> float {
@@ -531,10 +522,10 @@ void extend_lds_kernel(ExtendParams p) {
     return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
   };
   // O^T += V^T P^T over four 16-key slices of the V tile in `vs`
-  auto accumulate = [&](const uint8_t* vs, const bf16x8(&pf)[4]) __attribute__((always_inline)) {
+  auto accumulate = [&](const uint8_t* vs, const u32x4(&pf)[4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      bf16x8 vf[T::DB];
+      u32x4 vf[T::DB];
 #pragma unroll
       for (int b = 0; b < T::DB; ++b) {
         i16x4 half[2];
@@ -542,11 +533,10 @@ void extend_lds_kernel(ExtendParams p) {
         for (int e4 = 0; e4 < 2; ++e4)
           half[e4] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (lds_i16x4*)(vs + v_addr[b] + (16 * u + 4 * e4) * T::RB));
-        vf[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        vf[b] = __builtin_bit_cast(u32x4, __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7));
       }
 #pragma unroll
-      for (int b = 0; b < T::DB; ++b)
-        o[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b], pf[u], o[b], 0, 0, 0);
+      for (int b = 0; b < T::DB; ++b) o[b] = mfma16<FP8>(vf[b], pf[u], o[b]);
     }
   };
 
@@ -564,29 +554,28 @@ void extend_lds_kernel(ExtendParams p) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
   };
-  // P V: one slice of V fragments ahead, then per MFMA two scaling FMAs and
-  // two more reads
-  auto interleave_pv_scale = [&]() __attribute__((always_inline)) {
+  // P V: one slice of V fragments ahead, then per MFMA two more reads
+  auto interleave_pv = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_sched_group_barrier(0x100, 2 * T::DB, 0);
 #pragma unroll
     for (int i = 0; i < 4 * T::DB; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 32 / (4 * T::DB), 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
   };
 
   // ---- prologue: tiles 0 and 1 of K and tile 0 of V staged, tile 0's scores
   // against its exact max.  bf16: K_0, V_0, K_1 by DMA, the loop then stages
-  // K_{j+2} and V_{j+1} in iteration j.  fp8: the same tiles widened here, and
-  // the loop's first iteration finds K_2 and V_1 already in registers.
+  // K_{j+2} and V_{j+1} in iteration j.  fp8: the same tiles dequantised here
+  // (new tokens' rows by DMA, converted in place), and the loop's first
+  // iteration finds K_2 and V_1 already in registers.
   // scores of tile j in log2 units: xa for even j, xb for odd j (the stage
   // parity), so tile j+1's scores land in place with no copy
   f32x16 xa[2] = {f32x16{}, f32x16{}}, xb[2] = {f32x16{}, f32x16{}};
   int pg_v = 0;    // bf16: page of V_{j+1};  fp8: page of V_{j+2} (uniform)
   int pg_raw = 0;  // bf16: page of K_{j+2};  fp8: page of K_{j+3} (scalar load in flight)
   u32x4 k8 = {0u, 0u, 0u, 0u}, v8 = {0u, 0u, 0u, 0u};  // fp8: K_{j+2}, V_{j+1} rows
-  float ks_n = 1.f, vs_n = 1.f;  // fp8: this wave's page scales of tile j+2
+  float sk8 = 1.f, sv8 = 1.f;  // fp8: the page scales of the rows in k8 and v8
   __syncthreads();  // zero fill done before any tile lands
   if (n_tiles > 0) {
     const int pg0 = load_page(tile0(0));
@@ -601,32 +590,34 @@ void extend_lds_kernel(ExtendParams p) {
       const u32x4 a = load8(tile0(0), pg0, k_pool, true), b = load8(tile0(0), pg0, v_pool, false);
       u32x4 k1 = {0u, 0u, 0u, 0u};
       if (n_tiles > 1) k1 = load8(tile0(1), pg1, k_pool, true);
-      float ks0, vs0, ks1 = 1.f, vs1 = 1.f;
-      load_scales(tile0(0), pg0, ks0, vs0);
-      if (n_tiles > 1) load_scales(tile0(1), pg1, ks1, vs1);
+      const float sk0 = load_scale(ks_s, tile0(0), pg0), sv0 = load_scale(vs_s, tile0(0), pg0);
+      const float sk1 = n_tiles > 1 ? load_scale(ks_s, tile0(1), pg1) : 1.f;
       const int pg2 = n_tiles > 2 ? load_page(tile0(2)) : 0;
       __builtin_amdgcn_s_waitcnt(0);
-      store8(tile0(0), a, lds_k0, true);
-      store8(tile0(0), b, lds_v0, false);
-      if (n_tiles > 1) store8(tile0(1), k1, lds_k1, true);
-      write_params(tile0(0), 0, ks0, vs0);
-      if (n_tiles > 1) write_params(tile0(1), 1, ks1, vs1);
+      store8(tile0(0), a, lds_k0, true, sk0);
+      store8(tile0(0), b, lds_v0, false, sv0);
+      if (n_tiles > 1) store8(tile0(1), k1, lds_k1, true, sk1);
       if (n_tiles > 2) {
         k8 = load8(tile0(2), pg2, k_pool, true);
-        load_scales(tile0(2), pg2, ks_n, vs_n);
+        sk8 = load_scale(ks_s, tile0(2), pg2);
       }
-      if (n_tiles > 1) v8 = load8(tile0(1), pg1, v_pool, false);
+      if (n_tiles > 1) {
+        v8 = load8(tile0(1), pg1, v_pool, false);
+        sv8 = load_scale(vs_s, tile0(1), pg1);
+      }
       pg_v = pg2;
       if (n_tiles > 3) pg_raw = load_page(tile0(3));
     }
     if (p.w.total_tokens > 0) fused_write();  // under the first tiles' latency
     __builtin_amdgcn_s_waitcnt(0);
+    // K_0's DMA'd new-token rows become fp16 here; K_1 and V_0 before the barrier
+    // of iteration 0, which reads them first (every tile is converted once)
+    if constexpr (FP8) convert_new(tile0(0), lds_k0);
     __syncthreads();
     if (visible(0)) {
       m_run = 0.f;  // the scores below are taken relative to 0 (negm is 0 too)
       scores(lds_k0, xa);
       mask(tile0(0), xa);
-      to_log2(tile0(0), 0, xa, true);
       const float mx = row_max(xa);
       // a row with no visible key in the first tile sees none in the item
       const float d = mx == -INFINITY ? 0.f : mx;
@@ -641,15 +632,14 @@ void extend_lds_kernel(ExtendParams p) {
 
   // the work of iteration j after its staging is issued: tile j+1's scores
   // (discarded after the last visible tile: the stage then holds finite stale
-  // data) while tile j's weights are formed, then tile j's P V while tile j+1's
-  // scores are scaled.  `edge` false: tiles j and j+1 lie wholly in the prefix
-  // (no mask, no tile straddling the prefix end).
+  // data) while tile j's weights are formed, then tile j's P V.  `edge` false:
+  // tiles j and j+1 lie wholly in the prefix (no mask).
   auto compute = [&](int j, const uint8_t* k_nxt, const uint8_t* v_cur, bool edge,
                      f32x16(&x)[2], f32x16(&s)[2]) __attribute__((always_inline)) {
-    bf16x8 pf[4];
+    u32x4 pf[4];
     float lsum;
     scores(k_nxt, s);
-    weights(tile0(j), j & 3, x, pf, lsum, edge);
+    weights(x, pf, lsum);
     interleave_scores_weights();
     if (__any(!(lsum <= kSumLimit))) {
       // raise the running max to this tile's row max and redo its weights
@@ -661,37 +651,34 @@ void extend_lds_kernel(ExtendParams p) {
       for (int b = 0; b < T::DB; ++b) o[b] *= alpha;
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) x[blk] -= d;
-      weights(tile0(j), j & 3, x, pf, lsum, edge);
-      if constexpr (!FP8) {
-        // tile j+1's scores were started from the old -m_run
+      weights(x, pf, lsum);
+      // tile j+1's scores were started from the old -m_run
 #pragma unroll
-        for (int blk = 0; blk < 2; ++blk) s[blk] -= d;
-        negm = -m_run;
-      }
+      for (int blk = 0; blk < 2; ++blk) s[blk] -= d;
+      negm = -m_run;
     }
     l_run += lsum;
     if (edge) mask(tile0(j + 1), s);
     accumulate(v_cur, pf);
-    to_log2(tile0(j + 1), (j + 1) & 3, s, edge);
-    interleave_pv_scale();
+    interleave_pv();
   };
 
-  // fp8 staging of iteration j (after the barrier): widen K_{j+2} (into K_j's
-  // stage) and V_{j+1} (into V_{j-1}'s) from registers, leave tile j+2's group
-  // numbers, then load K_{j+3} and V_{j+2}
+  // fp8 staging of iteration j (after the barrier): dequantise K_{j+2} (into
+  // K_j's stage) and V_{j+1} (into V_{j-1}'s) from registers, then load the
+  // codes and page scales of K_{j+3} and V_{j+2}
   auto stage8 = [&](int j, uint8_t* k_cur, uint8_t* v_nxt,
                     bool all_prefix) __attribute__((always_inline)) {
-    if (all_prefix || j + 2 < n_tiles) {
-      store8(tile0(j + 2), k8, k_cur, true);
-      write_params(tile0(j + 2), (j + 2) & 3, ks_n, vs_n);
-    }
-    if (all_prefix || j + 1 < n_tiles) store8(tile0(j + 1), v8, v_nxt, false);
+    if (all_prefix || j + 2 < n_tiles) store8(tile0(j + 2), k8, k_cur, true, sk8);
+    if (all_prefix || j + 1 < n_tiles) store8(tile0(j + 1), v8, v_nxt, false, sv8);
     const int pg3 = pg_raw;
     if (all_prefix || j + 3 < n_tiles) {
       k8 = load8(tile0(j + 3), pg3, k_pool, true);
-      load_scales(tile0(j + 3), pg3, ks_n, vs_n);
+      sk8 = load_scale(ks_s, tile0(j + 3), pg3);
     }
-    if (all_prefix || j + 2 < n_tiles) v8 = load8(tile0(j + 2), pg_v, v_pool, false);
+    if (all_prefix || j + 2 < n_tiles) {
+      v8 = load8(tile0(j + 2), pg_v, v_pool, false);
+      sv8 = load_scale(vs_s, tile0(j + 2), pg_v);
+    }
     pg_v = pg3;
     pg_raw = load_page(tile0(j + 4));  // an in-range entry whenever it is a prefix page
   };
@@ -701,6 +688,11 @@ void extend_lds_kernel(ExtendParams p) {
   auto iteration = [&](int j, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_nxt,
                        f32x16(&x)[2], f32x16(&xn)[2]) __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);  // this wave's staging of K_{j+1} and V_j has landed
+    if constexpr (FP8) {
+      // its DMA'd new-token rows of K_{j+1} and V_j become fp16 before the barrier
+      if (j + 1 < n_tiles) convert_new(tile0(j + 1), k_nxt);
+      convert_new(tile0(j), v_cur);
+    }
     __syncthreads();                // everyone's has; K_j and V_{j-1} are no longer read
     if constexpr (!FP8) {
       const int pg_k = pg_raw;
