@@ -39,6 +39,7 @@ WORKLOAD_DESC = {
     "decode": "decode: the 48 decodes of the mixed step (prefix U[2k,32k]), 32q/8kv, D=128, P=16, fp8-e4m3fn pool",
     "decode_bf16": "decode: the 48 decodes of the mixed step, 32q/8kv, D=128, P=16, bf16 pool",
     "decode_long": "decode: 1 sequence, prefix 131072, 64q/8kv (GQA 8), D=128, P=64, bf16 pool",
+    "chunked": "chunked prefill step: 32 chunks of U[128,512] tokens on prefixes U[8k,32k] + 32 decodes (prefix U[2k,32k]), 32q/8kv, D=128, P=16, bf16",
 }
 
 
@@ -54,6 +55,10 @@ def parse():
                     help="target CPU time of the oracle sample (0 disables)")
     ap.add_argument("--no-policy", dest="policy", action="store_false",
                     help="skip the host KV-block policy comparison added to an extend run")
+    ap.add_argument("--no-other-workloads", dest="others", action="store_false",
+                    help="skip the other named workloads (batch16, long, mixed, decode_bf16, decode_long)")
+    ap.add_argument("--other-steps", type=int, default=20,
+                    help="timed steps per other workload (after 5 warm-up steps)")
     ap.add_argument("--no-swap", dest="swap", action="store_false",
                     help="skip the page swap measurement added to an extend run")
     ap.add_argument("--extend-kernel", type=int, default=0, choices=[0, 1, 2],
@@ -300,12 +305,14 @@ def sample_power(enqueue, seconds: float, settle: float = 0.5):
 
 
 def run_workload(name: str, steps: int, warmup: int, separate: bool = False, cold_steps: int = 0,
-                 power_s: float = 0.0):
+                 power_s: float = 0.0, one_launch: bool = False):
     """Times `steps` hot-path steps (page write + attention) of a named workload: one
     cw_step_attention per step (decodes on the decode kernel, extends on the extend
     kernel, the page write fused into the extend launch, or into the decode launch
     when there are no extends); with `separate`, cw_kv_write_pages followed by
-    cw_extend_attention or cw_decode_attention."""
+    cw_extend_attention or cw_decode_attention; with `one_launch`, one
+    cw_write_extend_attention over every sequence (decodes as one-token extends:
+    the page write and all attention in one extend launch, plus the split-K merge)."""
     import torch
     import cw_workloads as cw
     import paper_2606_16824_amd as cwlib
@@ -324,7 +331,7 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
     if decode and separate:
         nb = cwlib.decode_workspace_bytes(s.prefix_lens, s.num_kv_heads, s.gqa_group, s.head_dim,
                                           s.page_size, s.kv_dtype)
-    elif separate:
+    elif separate or one_launch:
         nb = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
                                           s.gqa_group, s.head_dim, s.page_size)
     else:
@@ -335,6 +342,11 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
     stream = torch.cuda.current_stream()
 
     def step():
+        if one_launch:
+            cwlib.write_extend_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
+                                         s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs,
+                                         out=out, lse=lse, workspace=ws_att)
+            return
         if not separate:
             cwlib.step_attention(q, kn, vn, kp, vp, bt, s.prefix_lens, s.suffix_lens,
                                  s.gqa_group, s.softmax_scale, k_scale=ks, v_scale=vs,
@@ -415,6 +427,54 @@ def run_workload(name: str, steps: int, warmup: int, separate: bool = False, col
                 step()
         res["power"] = sample_power(batch, power_s)
     return res
+
+
+OTHER_WORKLOADS = ("batch16", "long", "mixed", "chunked", "decode_bf16", "decode_long")
+
+
+def run_others(names, steps: int, warmup: int = 5):
+    """The other named workloads, each timed like the main one (one step = one
+    cw_step_attention on inputs resident in HBM; kernel time by HIP events in a
+    second pass), reported per workload."""
+    import gc
+    import torch
+    import cw_workloads as cw
+
+    out = {}
+    for name in names:
+        res = run_workload(name, steps, warmup)
+        s, ms, kern = res["spec"], res["ms"], res["kern_ms"]
+        if name.startswith("decode"):
+            nbytes = cw.decode_bytes(s)
+            out[name] = {"workload": WORKLOAD_DESC[name], "ms_per_step": round(ms, 5),
+                         "kernel": res["kernel"], "kernel_ms": round(kern, 5),
+                         "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                         "kernel_GB_s": round(nbytes / (kern * 1e-3) / 1e9, 1),
+                         "frac_hbm_peak": round(nbytes / (kern * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                         "algorithmic_bytes": nbytes}
+        else:
+            flops = s.flops()
+            out[name] = {"workload": WORKLOAD_DESC[name], "ms_per_step": round(ms, 5),
+                         "kernel": res["kernel"], "kernel_ms": round(kern, 5),
+                         "TFLOP_s": round(flops / (ms * 1e-3) / 1e12, 2),
+                         "kernel_TFLOP_s": round(flops / (kern * 1e-3) / 1e12, 2),
+                         "frac_bf16_peak": round(flops / (kern * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                         "new_tok_s": round(s.total_new_tokens / (ms * 1e-3), 1),
+                         "tflop_per_step": round(flops / 1e12, 5), "seed": s.seed,
+                         "traffic": measured_traffic(s.kv_dtype, name) if EXTEND_KERNEL != 2 else None}
+        out[name]["steps"] = steps
+        if name == "chunked":
+            # the same step as one extend launch (decodes as one-token extends)
+            one = run_workload(name, steps, warmup, one_launch=True)
+            out[name]["one_launch"] = {
+                "calls": "cw_write_extend_attention (one extend launch, decodes as one-token extends)",
+                "ms_per_step": round(one["ms"], 5), "kernel_ms": round(one["kern_ms"], 5)}
+            del one
+        print(f"[bench] {name}: step {ms:.4f} ms, kernel {kern:.4f} ms", file=sys.stderr, flush=True)
+        del res
+        gc.collect()
+        torch.cuda.empty_cache()
+    return out
 
 
 def measure_ceilings(reps: int = 5, power_s: float = 0.0):
@@ -640,6 +700,8 @@ def main():
                 nbytes / (d["kern_ms"] * 1e-3) / 1e9 / ceil["hbm_read_GB_s"], 4)
         print(f"[bench] decode step {d['ms']:.4f} ms, kernel {d['kern_ms']:.4f} ms", file=sys.stderr,
               flush=True)
+    if args.others and args.workload == "turn":
+        result["workloads"] = run_others(OTHER_WORKLOADS, args.other_steps)
     if not decode and args.policy:
         from paper_2606_16824_amd import policy_bench
         result["policy"] = policy_bench.run()

@@ -50,6 +50,9 @@ CONFIG_NAMES = ("tiny", "turn", "batch16", "long", "mixed")
 # decode-only workloads (every suffix length 1): the 48 decodes of the mixed step
 # with its fp8 pool, the same lengths with a bf16 pool, and one 131072-token decode
 DECODE_NAMES = ("decode", "decode_bf16", "decode_long")
+# chunked prefill as a serving engine schedules it (the paper serves with prefill
+# chunks of at most 512 tokens, co-scheduled with decodes)
+EXTRA_NAMES = ("chunked",)
 
 
 @dataclasses.dataclass
@@ -142,6 +145,8 @@ def spec_for(name: str, seed: Optional[int] = None) -> WorkloadSpec:
     """Draw the lengths of one of the named workloads."""
     if name in DECODE_NAMES:
         return _decode_spec(name, seed)
+    if name == "chunked":
+        return _chunked_spec(seed)
     idx = CONFIG_NAMES.index(name)
     seed = 1000 + idx if seed is None else seed
     rng = np.random.default_rng(seed)
@@ -171,6 +176,22 @@ def spec_for(name: str, seed: Optional[int] = None) -> WorkloadSpec:
         spec.num_pages = _pool_size(int(spec.pages_needed().sum()))
         return spec
     raise ValueError(name)
+
+
+def _chunked_spec(seed: Optional[int]) -> WorkloadSpec:
+    """One step of chunked prefill: 32 sequences each extending a cached prefix
+    U[8192, 32768] by a chunk of U[128, 512] tokens, and 32 decodes (prefix
+    U[2048, 32768]), in a seeded order; 32q/8kv, D = 128, P = 16, bf16 pool."""
+    seed = 1008 if seed is None else seed
+    rng = np.random.default_rng(seed)
+    kinds = np.array([0] * 32 + [1] * 32)
+    rng.shuffle(kinds)
+    lp = np.where(kinds == 0, rng.integers(2048, 32768 + 1, size=64),
+                  rng.integers(8192, 32768 + 1, size=64)).astype(np.int32)
+    ls = np.where(kinds == 0, 1, rng.integers(128, 512 + 1, size=64)).astype(np.int32)
+    spec = WorkloadSpec("chunked", lp, ls, 8, 4, 128, 16, 0, seed=seed)
+    spec.num_pages = _pool_size(int(spec.pages_needed().sum()))
+    return spec
 
 
 def _decode_spec(name: str, seed: Optional[int]) -> WorkloadSpec:

@@ -1,6 +1,8 @@
 """Full-size parity: the named workloads at their real sizes, in the launch
 configuration the benchmark times (one cw_step_attention: the page write fused
-into the extend launch, decodes on the decode kernel), against the oracle.
+into the extend launch, decodes on the decode kernel), against the oracle:
+the named workloads, and a chunked-prefill step (32 chunks of at most 512
+tokens and 32 decodes).
 
 Outputs start as NaN and must all be finite afterwards.  The turn is compared
 row by row in full.  For batch16, long and mixed, whole query tiles of the
@@ -49,7 +51,7 @@ def _run_step(dw):
     return out, lse
 
 
-@pytest.mark.parametrize("name", ["turn", "batch16", "long", "mixed"])
+@pytest.mark.parametrize("name", ["turn", "batch16", "long", "mixed", "chunked"])
 def test_full_size_step(name):
     w = cw.make(name)
     s = w.spec
@@ -81,7 +83,7 @@ def test_full_size_step(name):
     assert_close(got_lse, ref_lse, 1e-2, None, f"full {name} lse")
 
 
-@pytest.mark.parametrize("name", ["turn", "batch16", "mixed"])
+@pytest.mark.parametrize("name", ["turn", "batch16", "mixed", "chunked"])
 def test_full_size_write_pages(name):
     w = cw.make(name)
     s = w.spec
@@ -119,3 +121,18 @@ def test_full_size_write_pages(name):
     keep = mask[:, None, :, None].expand(dw.k_pool.shape)
     raw = (lambda t: t.view(torch.int16)) if dw.k_pool.dtype == torch.bfloat16 else (lambda t: t)
     assert torch.equal(raw(dw.k_pool)[keep], raw(before_k)[keep])
+
+
+def test_chunked_step_one_launch_matches_two():
+    """The chunked-prefill step through one extend launch (decodes as one-token
+    extends) gives the rows of the two-kernel step within 2 bf16 ulps."""
+    from gpu_util import assert_within_bf16_ulps
+    w = cw.make("chunked")
+    s = w.spec
+    print("\n[case] chunked one launch vs step", flush=True)
+    dw = to_gpu(w)
+    two, _ = _run_step(dw)
+    one = cwlib.write_extend_attention(dw.q, dw.k_new, dw.v_new, dw.k_pool, dw.v_pool, dw.block_table,
+                                       s.prefix_lens, s.suffix_lens, s.gqa_group, s.softmax_scale)
+    torch.cuda.synchronize()
+    assert_within_bf16_ulps(as_f64(one), as_f64(two), 2, "chunked one launch vs two")

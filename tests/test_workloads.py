@@ -30,6 +30,12 @@ def test_named_specs():
     assert m.suffix_lens[ext].min() >= 256 and m.suffix_lens[ext].max() <= 2048
     assert m.prefix_lens[ext].min() >= 8192 and m.prefix_lens[~ext].min() >= 2048
     assert m.kv_dtype == "fp8"
+    c = cw.spec_for("chunked")
+    dec = c.suffix_lens == 1
+    assert dec.sum() == 32 and (~dec).sum() == 32
+    assert c.suffix_lens[~dec].min() >= 128 and c.suffix_lens[~dec].max() <= 512
+    assert c.prefix_lens[~dec].min() >= 8192 and c.prefix_lens.max() <= 32768
+    assert c.prefix_lens[dec].min() >= 2048 and c.kv_dtype == "bf16"
 
 
 def test_block_table_and_sentinels():
