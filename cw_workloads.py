@@ -392,16 +392,22 @@ class AgentTrace:
     block_tokens: int
     prefill_s_per_token: float
     decode_s_per_token: float
+    groups: Optional[list] = None         # shared-prefix group of each session (None: no sharing)
+    shared_tokens: Optional[list] = None  # shared prefix tokens of each group
 
 
 def agent_sessions(num_sessions: int = 32, seed: int = 2000, max_turns: int = 24,
                    block_tokens: int = 16, capacity_fraction: float = 0.4,
-                   history_samples: int = 400) -> AgentTrace:
+                   history_samples: int = 400, shared_groups: int = 0,
+                   shared_prefix_tokens: int = 0) -> AgentTrace:
     """Seeded synthetic sessions: a 2-6k-token opening prompt, then turns whose
     inputs are tool outputs (lognormal, median 300 tokens) and outputs of 20-300
     tokens, each followed by a tool call of one of AGENT_TOOLS; starts U[0, 30) s.
     The node holds `capacity_fraction` of the sessions' final KV blocks (at least
-    the largest session's), so they compete for memory."""
+    the largest session's), so they compete for memory.  With `shared_groups`,
+    session s belongs to group s % shared_groups, whose members' opening prompts
+    begin with the same `shared_prefix_tokens` tokens (a system prompt and tool
+    schema): trace.groups[s], trace.shared_tokens[g]."""
     ss = np.random.SeedSequence(seed)
     c_sess, c_hist = ss.spawn(2)
     g = np.random.default_rng(c_sess)
@@ -423,4 +429,9 @@ def agent_sessions(num_sessions: int = 32, seed: int = 2000, max_turns: int = 24
     gh = np.random.default_rng(c_hist)
     history = [gh.lognormal(np.log(med), sig, size=history_samples).tolist() for med, sig in AGENT_TOOLS]
     cap = max(max(final_blocks), int(capacity_fraction * sum(final_blocks)))
-    return AgentTrace(sessions, history, cap, block_tokens, 5e-5, 1e-2)
+    tr = AgentTrace(sessions, history, cap, block_tokens, 5e-5, 1e-2)
+    if shared_groups > 0:
+        assert shared_prefix_tokens <= 2000, "opening prompts start at 2000 tokens"
+        tr.groups = [s % shared_groups for s in range(num_sessions)]
+        tr.shared_tokens = [shared_prefix_tokens] * shared_groups
+    return tr

@@ -36,6 +36,7 @@ class Turn:
 class SessionSpec:
     start: float
     turns: List[Turn]
+    group: int = -1        # shared-prefix group (-1: none)
 
 
 @dataclass
@@ -180,3 +181,193 @@ def simulate(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Seq
     total = sum(tr.in_tokens + tr.out_tokens for s in sessions for tr in s.turns)
     r.goodput_tok_s = total / r.makespan_s if r.makespan_s > 0 else 0.0
     return r
+
+
+# ---------------------------------------------------------------------------
+# The same model at block granularity, with prefix blocks shared across sessions.
+#
+# Readings (the paper's engine keeps prefix blocks cached by content and shares
+# them; its formal model leaves these open):
+#  * group g shares the first shared_tokens[g] tokens of each member's context;
+#    the whole blocks among them (G_g = shared_tokens // B) are one copy, the
+#    rest of a member's context is private.  A member's first turn's input
+#    starts with the shared tokens.
+#  * a request's resident run k is the leading run of its blocks that are
+#    resident (shared blocks count even before the session's first request);
+#    the tokens whose K/V it finds resident are min(k B, max(context, G B)):
+#    its own context, or the shared prefix before its first request.  It
+#    prefills the rest of context + input; `recomputed` counts the tokens of its
+#    own context among them.
+#  * eviction takes one block at a time, the largest key first.  A private
+#    block of session s at position p has key (v_s, -s, p) with v_s the
+#    policy's value (predictive: priority; LRU: -last use; Belady: true time
+#    to next use).  A shared block's v is the value of the sharer that needs it
+#    soonest (smallest priority or time to next use, latest last use) over the
+#    sessions attached to the group, its s that sharer.  So every sharer's
+#    private blocks (positions after it) leave first: resident blocks stay a
+#    leading run of every context.  The dispatching session's resident run is
+#    never a candidate.
+# With no groups this is exactly simulate() above (pinned by a test).
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Dispatch:
+    session: int
+    cached_tokens: int     # prompt tokens whose K/V are resident (attention prefix)
+    new_tokens: int        # tokens prefilled (context + input - cached)
+    blocks: int            # blocks of the request (context + input + output)
+
+
+def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Sequence[float]],
+                    shared_tokens: Sequence[int] = ()) -> tuple:
+    """Returns (Result, [Dispatch])."""
+    B = cfg.block_tokens
+    n = len(sessions)
+    G = [shared_tokens[s.group] // B if s.group >= 0 else 0 for s in sessions]
+    nxt = [0] * n
+    ctx = [0] * n
+    state = ["wait"] * n
+    arrival = [s.start for s in sessions]
+    last_use = [0.0] * n
+    tool_start = [0.0] * n
+    tool = [0] * n
+    prio = [0.0] * n
+    done_at = [0.0] * n
+    attached = [False] * n
+    res_private = [0] * n               # resident private blocks (positions G .. G + r - 1)
+    res_shared = [0] * len(shared_tokens)  # resident shared blocks of each group (leading)
+    for i, s in enumerate(sessions):
+        if not s.turns:
+            state[i], done_at[i], prio[i] = "done", s.start, INF
+    r = Result()
+    log = []
+    t = 0.0
+    running, run_end = -1, 0.0
+
+    def resident_run(i):
+        g = sessions[i].group
+        if g < 0:
+            return res_private[i]
+        if res_shared[g] < G[i]:
+            return res_shared[g]
+        return G[i] + res_private[i]
+
+    def need(i):
+        tr = sessions[i].turns[nxt[i]]
+        return _blocks(ctx[i] + tr.in_tokens + tr.out_tokens, B)
+
+    def tau_true(j):
+        if state[j] == "done":
+            return INF
+        if state[j] == "queued":
+            return 0.0
+        return max(0.0, arrival[j] - t)
+
+    def value(j):
+        if cfg.evict == "lru":
+            return -last_use[j]
+        if cfg.evict == "predictive":
+            return prio[j]
+        return tau_true(j)
+
+    def victim(i):
+        """Largest key among the tail blocks of other sessions' private runs and of
+        the groups' shared runs: ('p', session) or ('g', group)."""
+        best, best_key = None, None
+        for j in range(n):
+            if j != i and res_private[j] > 0:
+                key = (value(j), -j, G[j] + res_private[j] - 1)
+                if best_key is None or key > best_key:
+                    best, best_key = ("p", j), key
+        for g in range(len(shared_tokens)):
+            if res_shared[g] == 0:
+                continue
+            if sessions[i].group == g and res_shared[g] <= resident_run(i):
+                continue  # every resident shared block is in the dispatching run
+            sharers = [j for j in range(n) if sessions[j].group == g and attached[j]]
+            v, jmin = min((value(j), j) for j in sharers)
+            key = (v, -jmin, res_shared[g] - 1)
+            if best_key is None or key > best_key:
+                best, best_key = ("g", g), key
+        return best
+
+    while True:
+        for i in range(n):
+            if state[i] == "wait" and arrival[i] <= t:
+                state[i] = "queued"
+        if running < 0:
+            queued = [i for i in range(n) if state[i] == "queued"]
+            if queued:
+                if cfg.sched == "prefix":
+                    i = min(queued, key=lambda q: (need(q) - resident_run(q), arrival[q], q))
+                else:
+                    i = min(queued, key=lambda q: (arrival[q], q))
+                r.requests += 1
+                if cfg.evict == "predictive" and r.requests % cfg.n_rebuild == 0:
+                    for j in range(n):
+                        if state[j] == "done":
+                            prio[j] = INF
+                        elif state[j] == "queued":
+                            prio[j] = 0.0
+                        elif state[j] == "wait":
+                            prio[j] = predict_remaining(history[tool[j]], t - tool_start[j])
+                    r.heap_rebuilds += 1
+                tr = sessions[i].turns[nxt[i]]
+                d = need(i)
+                k = resident_run(i)
+                if k < _blocks(ctx[i], B):
+                    r.faults += 1
+                a = d - k
+                free = cfg.M - sum(res_private) - sum(res_shared)
+                while free < a:
+                    kind, x = victim(i)
+                    if kind == "p":
+                        res_private[x] -= 1
+                    else:
+                        res_shared[x] -= 1
+                    free += 1
+                    r.evicted_blocks += 1
+                k = resident_run(i)
+                known = max(ctx[i], G[i] * B)
+                hit = min(k * B, known)
+                recompute = max(0, ctx[i] - hit)
+                r.recomputed_tokens += recompute
+                r.prefilled_tokens += ctx[i] + tr.in_tokens - hit
+                log.append(Dispatch(i, hit, ctx[i] + tr.in_tokens - hit, d))
+                g = sessions[i].group
+                if g >= 0:
+                    res_shared[g] = max(res_shared[g], min(d, G[i]))
+                res_private[i] = max(0, d - G[i])
+                attached[i] = True
+                state[i] = "running"
+                running = i
+                run_end = t + (cfg.prefill_s_per_token * (ctx[i] + tr.in_tokens - hit)
+                               + cfg.decode_s_per_token * tr.out_tokens)
+                r.dispatch.append(i)
+                continue
+        nexts = [arrival[i] for i in range(n) if state[i] == "wait"]
+        if running >= 0:
+            nexts.append(run_end)
+        if not nexts:
+            break
+        t = max(t, min(nexts))
+        if running >= 0 and run_end <= t:
+            i = running
+            tr = sessions[i].turns[nxt[i]]
+            ctx[i] += tr.in_tokens + tr.out_tokens
+            last_use[i] = t
+            nxt[i] += 1
+            if nxt[i] == len(sessions[i].turns):
+                state[i], done_at[i], prio[i] = "done", t, INF
+            else:
+                state[i] = "wait"
+                tool[i], tool_start[i] = tr.tool, t
+                arrival[i] = t + tr.tool_s
+                prio[i] = predict_remaining(history[tr.tool], 0.0)
+            running = -1
+    r.makespan_s = max(done_at) if n else 0.0
+    spans = [done_at[i] - sessions[i].start for i in range(n) if sessions[i].turns]
+    r.mean_session_s = sum(spans) / len(spans) if spans else 0.0
+    total = sum(tr.in_tokens + tr.out_tokens for s in sessions for tr in s.turns)
+    r.goodput_tok_s = total / r.makespan_s if r.makespan_s > 0 else 0.0
+    return r, log

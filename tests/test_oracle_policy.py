@@ -150,3 +150,86 @@ def test_unbounded_capacity_never_evicts():
         assert r.evicted_blocks == 0 and r.faults == 0 and r.recomputed_tokens == 0
         assert r.prefilled_tokens == sum(t.in_tokens for s in sessions for t in s.turns)
         assert r.requests == sum(len(s.turns) for s in sessions)
+
+
+# ---- block-level model with shared prefix blocks (simulate_blocks)
+
+def _to_oracle_sessions(sessions, groups=None):
+    return [cp.SessionSpec(st, [cp.Turn(*t) for t in turns], group=-1 if groups is None else groups[i])
+            for i, (st, turns) in enumerate(sessions)]
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("sched,evict", list(itertools.product(("fcfs", "prefix"),
+                                                               ("lru", "predictive", "belady"))))
+def test_block_model_without_groups_is_the_session_model(seed, sched, evict):
+    import cw_workloads as cw
+    tr = cw.agent_sessions(num_sessions=12, seed=2000 + seed, max_turns=12)
+    cfg = cp.Config(M=tr.capacity_blocks, block_tokens=tr.block_tokens,
+                    prefill_s_per_token=tr.prefill_s_per_token, decode_s_per_token=tr.decode_s_per_token,
+                    sched=sched, evict=evict, n_rebuild=3)
+    a = cp.simulate(cfg, _to_oracle_sessions(tr.sessions), tr.history)
+    b, log = cp.simulate_blocks(cfg, _to_oracle_sessions(tr.sessions), tr.history)
+    assert a.dispatch == b.dispatch and [d.session for d in log] == a.dispatch
+    for f in ("requests", "faults", "evicted_blocks", "recomputed_tokens", "prefilled_tokens",
+              "heap_rebuilds", "makespan_s", "mean_session_s"):
+        assert getattr(a, f) == getattr(b, f), f
+    assert sum(d.new_tokens for d in log) == a.prefilled_tokens
+
+
+def test_shared_prefix_hit_worked_example():
+    # B = 4, shared prefix of 8 tokens (2 blocks).  S0 prefills its 10-token prompt
+    # (no hit) into 3 blocks; S1 arrives later, finds both shared blocks resident
+    # and prefills 1 of its 9 prompt tokens.
+    cfg = cp.Config(M=10, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict="lru")
+    ss = [cp.SessionSpec(0.0, [cp.Turn(10, 2)], group=0), cp.SessionSpec(100.0, [cp.Turn(9, 3)], group=0)]
+    r, log = cp.simulate_blocks(cfg, ss, [[1.0]], shared_tokens=[8])
+    assert [(d.session, d.cached_tokens, d.new_tokens, d.blocks) for d in log] == [(0, 0, 10, 3), (1, 8, 1, 3)]
+    assert (r.requests, r.evicted_blocks, r.prefilled_tokens, r.recomputed_tokens) == (2, 0, 11, 0)
+
+
+def test_shared_blocks_outlive_their_sharers_private_tails_worked_example():
+    # M = 5 blocks of 4 tokens, LRU.  S0 (group 0) and S1 (group 0) share 2 blocks and
+    # hold one private block each; S2 arrives at t = 30 needing 2 blocks with 1 free:
+    # the least recently used candidate is S0's private block (last use 10; the shared
+    # blocks count as used at 21 by S1).  S0's second turn at t = 60 finds its shared
+    # blocks but not its private one (a fault, 4 context tokens recomputed) and needs 2
+    # blocks with none free: S1's private block (21) goes, then S2's tail (38).
+    cfg = cp.Config(M=5, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict="lru")
+    ss = [cp.SessionSpec(0.0, [cp.Turn(10, 2, 0, 50.0), cp.Turn(4, 0)], group=0),
+          cp.SessionSpec(20.0, [cp.Turn(9, 3)], group=0),
+          cp.SessionSpec(30.0, [cp.Turn(8, 0)])]
+    r, log = cp.simulate_blocks(cfg, ss, [[1.0]], shared_tokens=[8])
+    assert r.dispatch == [0, 1, 2, 0]
+    assert [(d.cached_tokens, d.new_tokens, d.blocks) for d in log] == [(0, 10, 3), (8, 1, 3), (0, 8, 2), (8, 8, 4)]
+    assert (r.evicted_blocks, r.faults, r.recomputed_tokens, r.prefilled_tokens) == (3, 1, 4, 27)
+
+
+def test_shared_blocks_of_finished_sharers_are_evicted_first_worked_example():
+    # Predictive eviction, rebuilt every dispatch.  S0 (group 0) fills the 2 shared
+    # blocks and finishes; S1 needs all 4 blocks: the shared blocks' only attached
+    # sharer is done (priority +inf), so they go; S2 of group 0 then misses them.
+    cfg = cp.Config(M=4, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict="predictive",
+                    n_rebuild=1)
+    ss = [cp.SessionSpec(0.0, [cp.Turn(8, 0)], group=0), cp.SessionSpec(10.0, [cp.Turn(12, 4)]),
+          cp.SessionSpec(20.0, [cp.Turn(8, 4)], group=0)]
+    r, log = cp.simulate_blocks(cfg, ss, [[5.0]], shared_tokens=[8])
+    assert [d.cached_tokens for d in log] == [0, 0, 0]
+    assert (r.requests, r.evicted_blocks, r.prefilled_tokens, r.heap_rebuilds) == (3, 5, 28, 3)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_block_model_with_groups_accounting(seed):
+    import cw_workloads as cw
+    tr = cw.agent_sessions(num_sessions=10, seed=2100 + seed, max_turns=8, shared_groups=2,
+                           shared_prefix_tokens=1024)
+    cfg = cp.Config(M=tr.capacity_blocks, block_tokens=tr.block_tokens, prefill_s_per_token=1e-5,
+                    decode_s_per_token=1e-3, sched="prefix", evict="predictive", n_rebuild=3)
+    r, log = cp.simulate_blocks(cfg, _to_oracle_sessions(tr.sessions, tr.groups), tr.history,
+                                shared_tokens=tr.shared_tokens)
+    assert sum(d.new_tokens for d in log) == r.prefilled_tokens
+    # every session's later turns and every group's first requests after the first can hit
+    assert any(d.cached_tokens > 0 for d in log)
+    # the same sessions without the groups prefill at least as much
+    r0, _ = cp.simulate_blocks(cfg, _to_oracle_sessions(tr.sessions), tr.history)
+    assert r0.prefilled_tokens >= r.prefilled_tokens
