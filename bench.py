@@ -705,6 +705,7 @@ def main():
     if not decode and args.policy:
         from paper_2606_16824_amd import policy_bench
         result["policy"] = policy_bench.run()
+        result["policy_shared_prefix"] = policy_bench.run(shared_groups=4, shared_prefix_tokens=2000)
         print("[bench] policy simulation done", file=sys.stderr, flush=True)
     if not decode and args.swap:
         result["swap"] = run_swap()

@@ -31,7 +31,24 @@
  *  - A request takes prefill_s_per_token x (context tokens not resident +
  *    in_tokens) + decode_s_per_token x out_tokens seconds.
  *  - The predictor estimates E[tau | tau > e] of a tool type as the mean of
- *    (x - e) over its history samples x > e, and e when no sample exceeds e. */
+ *    (x - e) over its history samples x > e, and e when no sample exceeds e.
+ *
+ * Blocks (the KV block manager below, on which the simulation runs): every
+ * resident block is private to a session or shared by a prefix group (the
+ * whole blocks of the first shared_tokens tokens its members' contexts have in
+ * common, one copy; a member's first input starts with them) and carries a
+ * reference count of the running requests that use it.  Blocks left
+ * unreferenced when a request is released enter an eviction heap keyed by
+ * their owner's eviction value (predictive: priority; LRU: minus last use;
+ * Belady: true time to next use; larger evicts first), then the session id,
+ * then the block's position (tail first); a shared block takes the smallest
+ * value among its group's attached sessions (ties: the largest session id),
+ * so the sharers' private blocks leave before it.  The heap is rebuilt from
+ * current values every rebuild_every dispatches (predictive) and before every
+ * dispatch (Belady).  A request's resident run is its leading resident
+ * blocks (shared ones count before its first request), and the prompt tokens
+ * it finds resident are min(run x block_tokens, max(context, shared whole
+ * blocks x block_tokens)).  Without groups this is the session model above. */
 #ifndef CW_POLICY_H_
 #define CW_POLICY_H_
 
@@ -71,6 +88,9 @@ typedef struct {
   int32_t num_tools;
   const int32_t* hist_off;      /* [num_tools + 1] */
   const double* hist_s;         /* [hist_off[num_tools]], >= 0 */
+  int32_t num_groups;           /* shared-prefix groups (0: none) */
+  const int32_t* session_group; /* [num_sessions], in [-1, num_groups) (-1: none); NULL if no groups */
+  const int32_t* group_shared_tokens; /* [num_groups], >= 0, <= each member's first input */
 } cw_sim_trace_t;
 
 typedef struct {
@@ -94,6 +114,60 @@ typedef struct {
 cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
                                cw_sim_result_t* result, int32_t* dispatch,
                                int64_t dispatch_capacity);
+
+/* Per-dispatch log of a simulation (caller-owned host arrays): session,
+ * cached_tokens (prompt tokens whose K/V the request found resident: the
+ * attention prefix of its prefill), new_tokens (prompt tokens it prefilled:
+ * context + input - cached), and its block table (physical ids of its blocks
+ * for context + input + output tokens, logical order) at
+ * tables[table_off[i] .. table_off[i + 1]).  At most `capacity` dispatches and
+ * `table_capacity` table entries are written (tables are cut at the end);
+ * `written` returns the dispatches written. */
+typedef struct {
+  int64_t capacity;
+  int32_t* session;        /* [capacity] */
+  int32_t* cached_tokens;  /* [capacity] */
+  int32_t* new_tokens;     /* [capacity] */
+  int64_t* table_off;      /* [capacity + 1] */
+  int32_t* tables;         /* [table_capacity] */
+  int64_t table_capacity;
+  int64_t written;         /* out */
+} cw_sim_log_t;
+
+/* cw_policy_simulate with the per-dispatch log instead of the dispatch order. */
+cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
+                                   cw_sim_result_t* result, cw_sim_log_t* log);
+
+/* The KV block manager on its own, for a serving loop (host-only; one
+ * manager is not safe to use from several threads at once).  Sessions are
+ * registered with their prefix group (-1: none) before their first request.
+ * cw_bm_admit admits a session's next request (its context holds
+ * context_tokens, the request adds input_tokens and will generate
+ * output_tokens): references its resident leading blocks, evicts unreferenced
+ * blocks of others in heap order until the missing blocks fit, allocates and
+ * references them, and returns its block table (physical ids of all `blocks`
+ * = ceil((context + input + output) / block_tokens) blocks, logical order;
+ * at most table_capacity written), the prompt tokens found resident and the
+ * blocks evicted.  CW_ERR_WORKSPACE (nothing changed) when the blocks it needs
+ * exceed the capacity left by referenced blocks.  cw_bm_release drops the
+ * request's references; blocks left unreferenced enter the eviction heap with
+ * `value` (larger evicts first).  cw_bm_rebuild sets the values of the listed
+ * sessions and rebuilds the heap from every session's value (the periodic
+ * rebuild).  Errors: CW_ERR_NULL, CW_ERR_BAD_LENS (unknown or running
+ * session, negative counts, NaN values), CW_ERR_UNSUPPORTED (sizes). */
+typedef struct cw_block_manager cw_block_manager_t;
+cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out);
+cw_status_t cw_bm_destroy(cw_block_manager_t* bm);
+cw_status_t cw_bm_add_session(cw_block_manager_t* bm, int32_t session, int32_t group,
+                              int32_t shared_tokens);
+cw_status_t cw_bm_admit(cw_block_manager_t* bm, int32_t session, int64_t context_tokens,
+                        int64_t input_tokens, int64_t output_tokens, int32_t* table,
+                        int32_t table_capacity, int32_t* blocks, int64_t* cached_tokens,
+                        int64_t* evicted_blocks);
+cw_status_t cw_bm_release(cw_block_manager_t* bm, int32_t session, double value);
+cw_status_t cw_bm_rebuild(cw_block_manager_t* bm, const int32_t* sessions, const double* values,
+                          int32_t n);
+cw_status_t cw_bm_stats(cw_block_manager_t* bm, int64_t* free_blocks, int64_t* referenced_blocks);
 
 /* The predictor alone: the expected remaining time of a tool call of type
  * `tool` that has run for elapsed_s seconds, from the trace's history samples

@@ -203,10 +203,10 @@ def simulate(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Seq
 #    policy's value (predictive: priority; LRU: -last use; Belady: true time
 #    to next use).  A shared block's v is the value of the sharer that needs it
 #    soonest (smallest priority or time to next use, latest last use) over the
-#    sessions attached to the group, its s that sharer.  So every sharer's
-#    private blocks (positions after it) leave first: resident blocks stay a
-#    leading run of every context.  The dispatching session's resident run is
-#    never a candidate.
+#    sessions attached to the group, its s the largest id among the sharers with
+#    that value.  So every sharer's private blocks (positions after it) leave
+#    first: resident blocks stay a leading run of every context.  The
+#    dispatching session's resident run is never a candidate.
 # With no groups this is exactly simulate() above (pinned by a test).
 # ---------------------------------------------------------------------------
 
@@ -285,8 +285,9 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
             if sessions[i].group == g and res_shared[g] <= resident_run(i):
                 continue  # every resident shared block is in the dispatching run
             sharers = [j for j in range(n) if sessions[j].group == g and attached[j]]
-            v, jmin = min((value(j), j) for j in sharers)
-            key = (v, -jmin, res_shared[g] - 1)
+            v = min(value(j) for j in sharers)
+            jsel = max(j for j in sharers if value(j) == v)
+            key = (v, -jsel, res_shared[g] - 1)
             if best_key is None or key > best_key:
                 best, best_key = ("g", g), key
         return best
@@ -325,6 +326,8 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
                         res_private[x] -= 1
                     else:
                         res_shared[x] -= 1
+                        # the key order keeps every sharer's private blocks out first
+                        assert all(res_private[j] == 0 for j in range(n) if sessions[j].group == x)
                     free += 1
                     r.evicted_blocks += 1
                 k = resident_run(i)

@@ -66,6 +66,14 @@ SIGNATURES = {
     # include/cw_policy.h (host-only)
     "cw_policy_simulate": (C.c_int, [_vp, _vp, _vp, _vp, C.c_int64]),
     "cw_policy_predict": (C.c_int, [_vp, _i32, C.c_double, _vp]),
+    "cw_policy_simulate_log": (C.c_int, [_vp, _vp, _vp, _vp]),
+    "cw_bm_create": (C.c_int, [_i32, _i32, _vp]),
+    "cw_bm_destroy": (C.c_int, [_vp]),
+    "cw_bm_add_session": (C.c_int, [_vp, _i32, _i32, _i32]),
+    "cw_bm_admit": (C.c_int, [_vp, _i32, C.c_int64, C.c_int64, C.c_int64, _vp, _i32, _vp, _vp, _vp]),
+    "cw_bm_release": (C.c_int, [_vp, _i32, C.c_double]),
+    "cw_bm_rebuild": (C.c_int, [_vp, _vp, _vp, _i32]),
+    "cw_bm_stats": (C.c_int, [_vp, _vp, _vp]),
 }
 
 _lib = None

@@ -1,6 +1,7 @@
-// CacheWise host policy: block manager, prefix-aware scheduling and predictive
-// eviction, simulated over closed-loop agent sessions (see cw_policy.h for the
-// model).  Paper anchors: Sec. 4 (formal model: capacity M, resident prefix
+// CacheWise host policy: prefix-aware scheduling and predictive eviction over
+// the KV block manager (block_manager.h), simulated over closed-loop agent
+// sessions (see cw_policy.h for the model), and the block manager's C ABI.
+// Paper anchors: Sec. 4 (formal model: capacity M, resident prefix
 // k_i, new blocks a_i = d_i - k_i, eviction when the working set exceeds M),
 // Sec. 5.1 (dispatch the request with the fewest a_i), Sec. 5.2 (evict in
 // decreasing order of the predicted time to next reuse, from tool-duration
@@ -13,8 +14,11 @@
 #include <limits>
 #include <vector>
 
+#include <memory>
+
 #include "../../../include/cw_policy.h"
 #include "../cw_internal.h"
+#include "block_manager.h"
 
 namespace cw {
 namespace {
@@ -63,9 +67,20 @@ cw_status_t check_trace(const cw_sim_trace_t& tr, const cw_sim_config_t* cfg) {
   for (int32_t k = 0; k < tr.hist_off[tr.num_tools]; ++k)
     if (!(tr.hist_s[k] >= 0.0) || !std::isfinite(tr.hist_s[k]))
       return policy_fail(CW_ERR_BAD_LENS, "history sample %d = %g", k, tr.hist_s[k]);
+  if (tr.num_groups < 0) return policy_fail(CW_ERR_BAD_LENS, "num_groups = %d", tr.num_groups);
+  if (tr.num_groups > 0 && (!tr.session_group || !tr.group_shared_tokens))
+    return policy_fail(CW_ERR_NULL, "session_group and group_shared_tokens are required with groups");
+  for (int32_t g = 0; g < tr.num_groups; ++g)
+    if (tr.group_shared_tokens[g] < 0)
+      return policy_fail(CW_ERR_BAD_LENS, "group %d shares %d tokens", g, tr.group_shared_tokens[g]);
   for (int32_t s = 0; s < tr.num_sessions; ++s) {
     if (!(tr.session_start[s] >= 0.0) || !std::isfinite(tr.session_start[s]))
       return policy_fail(CW_ERR_BAD_LENS, "session %d starts at %g", s, tr.session_start[s]);
+    const int32_t g = tr.num_groups > 0 ? tr.session_group[s] : -1;
+    if (g < -1 || g >= tr.num_groups)
+      return policy_fail(CW_ERR_BAD_LENS, "session %d: group %d of %d", s, g, tr.num_groups);
+    if (g >= 0 && tr.turn_off[s + 1] > tr.turn_off[s] && tr.in_tokens[tr.turn_off[s]] < tr.group_shared_tokens[g])
+      return policy_fail(CW_ERR_BAD_LENS, "session %d: first input shorter than its group's shared prefix", s);
     int64_t ctx = 0;
     for (int32_t j = tr.turn_off[s]; j < tr.turn_off[s + 1]; ++j) {
       if (tr.in_tokens[j] < 0 || tr.out_tokens[j] < 0)
@@ -90,7 +105,6 @@ struct Session {
   int32_t first = 0, n = 0;  // turns [first, first + n)
   int32_t next = 0;          // next turn (index within the session)
   int64_t ctx = 0;           // context tokens
-  int64_t resident = 0;      // k_i: leading resident blocks
   State state = kWaiting;
   double arrival = 0.0;      // arrival of the pending request
   double last_use = 0.0;     // end of its last request
@@ -119,44 +133,50 @@ cw_status_t cw_policy_predict(const cw_sim_trace_t* trace, int32_t tool, double 
   return CW_OK;
 }
 
-cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
-                               cw_sim_result_t* result, int32_t* dispatch,
-                               int64_t dispatch_capacity) {
-  if (!config || !trace || !result) return policy_fail(CW_ERR_NULL, "config, trace and result are required");
-  const cw_sim_config_t& c = *config;
+}  // extern "C"
+
+namespace {
+
+cw_status_t check_config(const cw_sim_config_t& c) {
   if (c.capacity_blocks < 1 || c.block_tokens < 1 || !(c.prefill_s_per_token >= 0.0) ||
       !(c.decode_s_per_token >= 0.0) || !std::isfinite(c.prefill_s_per_token) ||
       !std::isfinite(c.decode_s_per_token) || c.rebuild_every < 1 ||
       (c.sched != CW_SCHED_FCFS && c.sched != CW_SCHED_PREFIX_AWARE) ||
       (c.evict != CW_EVICT_LRU && c.evict != CW_EVICT_PREDICTIVE && c.evict != CW_EVICT_BELADY))
     return policy_fail(CW_ERR_UNSUPPORTED, "invalid simulation configuration");
-  const cw_sim_trace_t& tr = *trace;
-  cw_status_t st = check_trace(tr, &c);
-  if (st != CW_OK) return st;
-  if (dispatch_capacity < 0) return policy_fail(CW_ERR_BAD_LENS, "dispatch_capacity < 0");
+  return CW_OK;
+}
 
+// The simulation proper; `log` may be null.
+cw_status_t simulate(const cw_sim_config_t& c, const cw_sim_trace_t& tr, cw_sim_result_t* result,
+                     int32_t* dispatch, int64_t dispatch_capacity, cw_sim_log_t* log) {
   const int32_t S = tr.num_sessions;
-  const int64_t B = c.block_tokens, M = c.capacity_blocks;
+  const int64_t B = c.block_tokens;
   std::vector<Session> ss(S);
+  BlockManager bm(c.capacity_blocks, c.block_tokens);
   int64_t total_tokens = 0;
   for (int32_t s = 0; s < S; ++s) {
     ss[s].first = tr.turn_off[s];
     ss[s].n = tr.turn_off[s + 1] - tr.turn_off[s];
     ss[s].arrival = tr.session_start[s];
+    const int32_t g = tr.num_groups > 0 ? tr.session_group[s] : -1;
+    bm.add_session(s, g, g >= 0 ? tr.group_shared_tokens[g] : 0);
     if (ss[s].n == 0) {
       ss[s].state = kDone;
       ss[s].done_at = tr.session_start[s];
       ss[s].priority = kInf;
+      bm.set_value(s, c.evict == CW_EVICT_LRU ? -0.0 : kInf);
     }
     for (int32_t j = ss[s].first; j < ss[s].first + ss[s].n; ++j)
       total_tokens += int64_t(tr.in_tokens[j]) + tr.out_tokens[j];
   }
+  if (log) log->written = 0;
 
   cw_sim_result_t r{};
-  int64_t used = 0;  // resident blocks over all sessions
-  int64_t dispatches = 0;
+  int64_t dispatches = 0, table_used = 0;
   int32_t running = -1;
   double run_end = 0.0, t = 0.0;
+  std::vector<int32_t> ids;
 
   // time to next use of session k's blocks as Belady's rule sees it
   auto true_next_use = [&](const Session& k) {
@@ -164,57 +184,55 @@ cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace
     if (k.state == kQueued) return 0.0;
     return std::max(0.0, k.arrival - t);
   };
+  // the periodic rebuild: every unreferenced session's priority re-estimated
   auto rebuild = [&]() {
-    for (Session& k : ss) {
+    for (int32_t s = 0; s < S; ++s) {
+      Session& k = ss[s];
       if (k.state == kDone) k.priority = kInf;
       else if (k.state == kQueued) k.priority = 0.0;
       else if (k.state == kWaiting) k.priority = predict_remaining(tr, k.tool, t - k.tool_start);
+      bm.set_value(s, k.priority);
     }
+    bm.rebuild();
     ++r.heap_rebuilds;
   };
-  // next victim among the other sessions' resident blocks
-  auto victim = [&](int32_t self) {
-    int32_t best = -1;
-    double best_key = 0.0;
-    for (int32_t k = 0; k < S; ++k) {
-      if (k == self || ss[k].resident == 0) continue;
-      double key;  // larger evicts first
-      if (c.evict == CW_EVICT_LRU) key = -ss[k].last_use;
-      else if (c.evict == CW_EVICT_PREDICTIVE) key = ss[k].priority;
-      else key = true_next_use(ss[k]);
-      if (best < 0 || key > best_key) {
-        best = k;
-        best_key = key;
-      }
-    }
-    return best;
-  };
-  auto dispatch_one = [&](int32_t i) {
+  auto dispatch_one = [&](int32_t i) -> cw_status_t {
     Session& s = ss[i];
     const int32_t j = s.first + s.next;
     ++dispatches;
     if (c.evict == CW_EVICT_PREDICTIVE && dispatches % c.rebuild_every == 0) rebuild();
-    const int64_t need = (s.ctx + tr.in_tokens[j] + tr.out_tokens[j] + B - 1) / B;
-    const int64_t a = need - s.resident;
-    if (s.resident < (s.ctx + B - 1) / B) ++r.faults;  // part of its context was evicted
-    while (M - used < a) {
-      const int32_t v = victim(i);  // exists: need <= M
-      const int64_t take = std::min(ss[v].resident, a - (M - used));
-      ss[v].resident -= take;  // from the tail of its context
-      used -= take;
-      r.evicted_blocks += take;
+    if (c.evict == CW_EVICT_BELADY) {  // Belady's values change with time: fresh keys
+      for (int32_t k = 0; k < S; ++k) bm.set_value(k, true_next_use(ss[k]));
+      bm.rebuild();
     }
-    const int64_t recompute = std::max<int64_t>(0, s.ctx - s.resident * B);
-    r.recomputed_tokens += recompute;
-    r.prefilled_tokens += recompute + tr.in_tokens[j];
-    used += need - s.resident;
-    s.resident = need;
+    if (bm.resident_run(i) < (s.ctx + B - 1) / B) ++r.faults;  // part of its context was evicted
+    BlockManager::Admission adm;
+    if (!bm.admit(i, s.ctx, tr.in_tokens[j], tr.out_tokens[j], &adm))
+      return policy_fail(CW_ERR_HIP, "block manager: request of session %d did not fit", i);
+    r.evicted_blocks += adm.evicted;
+    const int64_t hit = adm.cached_tokens;
+    const int64_t prefill = s.ctx + tr.in_tokens[j] - hit;
+    r.recomputed_tokens += std::max<int64_t>(0, s.ctx - hit);
+    r.prefilled_tokens += prefill;
+    if (log && r.requests < log->capacity) {
+      bm.table(i, &ids);
+      const int64_t w = r.requests;
+      if (w == 0) log->table_off[0] = 0;
+      log->session[w] = i;
+      log->cached_tokens[w] = static_cast<int32_t>(hit);
+      log->new_tokens[w] = static_cast<int32_t>(prefill);
+      const int64_t n = std::min<int64_t>(int64_t(ids.size()), std::max<int64_t>(0, log->table_capacity - table_used));
+      for (int64_t q = 0; q < n; ++q) log->tables[table_used + q] = ids[q];
+      table_used += n;
+      log->table_off[w + 1] = table_used;
+      log->written = w + 1;
+    }
     s.state = kRunning;
     running = i;
-    run_end = t + c.prefill_s_per_token * double(recompute + tr.in_tokens[j]) +
-              c.decode_s_per_token * double(tr.out_tokens[j]);
+    run_end = t + c.prefill_s_per_token * double(prefill) + c.decode_s_per_token * double(tr.out_tokens[j]);
     if (dispatch && r.requests < dispatch_capacity) dispatch[r.requests] = i;
     ++r.requests;
+    return CW_OK;
   };
   auto complete = [&](int32_t i) {
     Session& s = ss[i];
@@ -233,6 +251,8 @@ cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace
       s.arrival = t + tr.tool_s[j];
       s.priority = predict_remaining(tr, s.tool, 0.0);  // unreferenced now: fresh estimate
     }
+    // its blocks lose their reference and enter the eviction heap
+    bm.release(i, c.evict == CW_EVICT_LRU ? -s.last_use : s.priority);
   };
 
   while (true) {
@@ -240,26 +260,26 @@ cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace
       if (k.state == kWaiting && k.arrival <= t) k.state = kQueued;
     if (running < 0) {
       int32_t pick = -1;
+      int64_t pick_a = 0;
       for (int32_t k = 0; k < S; ++k) {
         if (ss[k].state != kQueued) continue;
-        if (pick < 0) {
+        const Session& a = ss[k];
+        const int32_t ja = a.first + a.next;
+        const int64_t aa = (a.ctx + tr.in_tokens[ja] + tr.out_tokens[ja] + B - 1) / B - bm.resident_run(k);
+        bool better = pick < 0;
+        if (!better) {
+          const Session& b = ss[pick];
+          if (c.sched == CW_SCHED_PREFIX_AWARE) better = aa < pick_a || (aa == pick_a && a.arrival < b.arrival);
+          else better = a.arrival < b.arrival;
+        }
+        if (better) {
           pick = k;
-          continue;
+          pick_a = aa;
         }
-        const Session &a = ss[k], &b = ss[pick];
-        bool better;
-        if (c.sched == CW_SCHED_PREFIX_AWARE) {
-          const int32_t ja = a.first + a.next, jb = b.first + b.next;
-          const int64_t aa = (a.ctx + tr.in_tokens[ja] + tr.out_tokens[ja] + B - 1) / B - a.resident;
-          const int64_t ab = (b.ctx + tr.in_tokens[jb] + tr.out_tokens[jb] + B - 1) / B - b.resident;
-          better = aa < ab || (aa == ab && a.arrival < b.arrival);
-        } else {
-          better = a.arrival < b.arrival;
-        }
-        if (better) pick = k;
       }
       if (pick >= 0) {
-        dispatch_one(pick);
+        const cw_status_t st = dispatch_one(pick);
+        if (st != CW_OK) return st;
         continue;
       }
     }
@@ -287,6 +307,133 @@ cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace
   r.mean_session_s = counted > 0 ? sum_sessions / counted : 0.0;
   r.goodput_tok_s = r.makespan_s > 0.0 ? double(total_tokens) / r.makespan_s : 0.0;
   *result = r;
+  return CW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
+                               cw_sim_result_t* result, int32_t* dispatch,
+                               int64_t dispatch_capacity) {
+  if (!config || !trace || !result) return policy_fail(CW_ERR_NULL, "config, trace and result are required");
+  cw_status_t st = check_config(*config);
+  if (st != CW_OK) return st;
+  st = check_trace(*trace, config);
+  if (st != CW_OK) return st;
+  if (dispatch_capacity < 0) return policy_fail(CW_ERR_BAD_LENS, "dispatch_capacity < 0");
+  return simulate(*config, *trace, result, dispatch, dispatch_capacity, nullptr);
+}
+
+cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
+                                   cw_sim_result_t* result, cw_sim_log_t* log) {
+  if (!config || !trace || !result || !log) return policy_fail(CW_ERR_NULL, "config, trace, result and log are required");
+  cw_status_t st = check_config(*config);
+  if (st != CW_OK) return st;
+  st = check_trace(*trace, config);
+  if (st != CW_OK) return st;
+  if (log->capacity < 0 || log->table_capacity < 0)
+    return policy_fail(CW_ERR_BAD_LENS, "negative log capacity");
+  if (log->capacity > 0 && (!log->session || !log->cached_tokens || !log->new_tokens || !log->table_off))
+    return policy_fail(CW_ERR_NULL, "log arrays are required");
+  if (log->table_capacity > 0 && !log->tables) return policy_fail(CW_ERR_NULL, "log tables are required");
+  return simulate(*config, *trace, result, nullptr, 0, log);
+}
+
+struct cw_block_manager {
+  std::unique_ptr<BlockManager> bm;
+  int32_t sessions = 0;  // registered ids are [0, sessions)
+  std::vector<uint8_t> known;
+};
+
+cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out) {
+  if (!out) return policy_fail(CW_ERR_NULL, "out is required");
+  *out = nullptr;
+  if (capacity_blocks < 1 || block_tokens < 1)
+    return policy_fail(CW_ERR_UNSUPPORTED, "capacity_blocks = %d, block_tokens = %d", capacity_blocks, block_tokens);
+  auto* m = new (std::nothrow) cw_block_manager;
+  if (!m) return policy_fail(CW_ERR_UNSUPPORTED, "out of host memory");
+  m->bm.reset(new (std::nothrow) BlockManager(capacity_blocks, block_tokens));
+  if (!m->bm) {
+    delete m;
+    return policy_fail(CW_ERR_UNSUPPORTED, "out of host memory");
+  }
+  *out = m;
+  return CW_OK;
+}
+
+cw_status_t cw_bm_destroy(cw_block_manager_t* m) {
+  delete m;
+  return CW_OK;
+}
+
+cw_status_t cw_bm_add_session(cw_block_manager_t* m, int32_t session, int32_t group, int32_t shared_tokens) {
+  if (!m) return policy_fail(CW_ERR_NULL, "block manager is NULL");
+  if (session < 0 || group < -1 || shared_tokens < 0)
+    return policy_fail(CW_ERR_BAD_LENS, "session %d, group %d, shared_tokens %d", session, group, shared_tokens);
+  if (session < m->sessions && m->known[session])
+    return policy_fail(CW_ERR_BAD_LENS, "session %d is already registered", session);
+  if (session >= m->sessions) {
+    m->sessions = session + 1;
+    m->known.resize(session + 1, 0);
+  }
+  m->known[session] = 1;
+  m->bm->add_session(session, group, shared_tokens);
+  return CW_OK;
+}
+
+cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_tokens, int64_t input_tokens,
+                        int64_t output_tokens, int32_t* table, int32_t table_capacity, int32_t* blocks,
+                        int64_t* cached_tokens, int64_t* evicted_blocks) {
+  if (!m || !blocks || !cached_tokens) return policy_fail(CW_ERR_NULL, "block manager, blocks and cached_tokens are required");
+  if (session < 0 || session >= m->sessions || !m->known[session])
+    return policy_fail(CW_ERR_BAD_LENS, "session %d is not registered", session);
+  if (context_tokens < 0 || input_tokens < 0 || output_tokens < 0)
+    return policy_fail(CW_ERR_BAD_LENS, "negative token counts");
+  if (m->bm->is_running(session)) return policy_fail(CW_ERR_BAD_LENS, "session %d already has a request running", session);
+  BlockManager::Admission adm;
+  if (!m->bm->admit(session, context_tokens, input_tokens, output_tokens, &adm))
+    return policy_fail(CW_ERR_WORKSPACE, "request of session %d does not fit: the referenced blocks would exceed the capacity", session);
+  std::vector<int32_t> ids;
+  m->bm->table(session, &ids);
+  *blocks = adm.blocks;
+  *cached_tokens = adm.cached_tokens;
+  if (evicted_blocks) *evicted_blocks = adm.evicted;
+  if (table) {
+    const int32_t n = std::min<int32_t>(table_capacity, static_cast<int32_t>(ids.size()));
+    for (int32_t q = 0; q < n; ++q) table[q] = ids[q];
+  }
+  return CW_OK;
+}
+
+cw_status_t cw_bm_release(cw_block_manager_t* m, int32_t session, double value) {
+  if (!m) return policy_fail(CW_ERR_NULL, "block manager is NULL");
+  if (session < 0 || session >= m->sessions || !m->known[session])
+    return policy_fail(CW_ERR_BAD_LENS, "session %d is not registered", session);
+  if (!m->bm->is_running(session)) return policy_fail(CW_ERR_BAD_LENS, "session %d has no request running", session);
+  if (std::isnan(value)) return policy_fail(CW_ERR_BAD_LENS, "eviction value is NaN");
+  m->bm->release(session, value);
+  return CW_OK;
+}
+
+cw_status_t cw_bm_rebuild(cw_block_manager_t* m, const int32_t* sessions, const double* values, int32_t n) {
+  if (!m) return policy_fail(CW_ERR_NULL, "block manager is NULL");
+  if (n < 0 || (n > 0 && (!sessions || !values))) return policy_fail(CW_ERR_NULL, "sessions and values are required");
+  for (int32_t q = 0; q < n; ++q) {
+    if (sessions[q] < 0 || sessions[q] >= m->sessions || !m->known[sessions[q]])
+      return policy_fail(CW_ERR_BAD_LENS, "session %d is not registered", sessions[q]);
+    if (std::isnan(values[q])) return policy_fail(CW_ERR_BAD_LENS, "eviction value is NaN");
+  }
+  for (int32_t q = 0; q < n; ++q) m->bm->set_value(sessions[q], values[q]);
+  m->bm->rebuild();
+  return CW_OK;
+}
+
+cw_status_t cw_bm_stats(cw_block_manager_t* m, int64_t* free_blocks, int64_t* referenced_blocks) {
+  if (!m || !free_blocks || !referenced_blocks) return policy_fail(CW_ERR_NULL, "arguments are required");
+  *free_blocks = m->bm->free_blocks();
+  *referenced_blocks = m->bm->referenced_blocks();
   return CW_OK;
 }
 

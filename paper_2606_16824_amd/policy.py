@@ -4,7 +4,9 @@ Argument marshalling only: the simulation runs in the library's C++ code.
 
 Sessions are given as a list of (start_s, turns) with turns a list of
 (in_tokens, out_tokens, tool_type, tool_s); `history[y]` is the list of past
-durations of tool type y that the predictor conditions on.
+durations of tool type y that the predictor conditions on; `groups[s]` (or
+None) the shared-prefix group of session s and `shared_tokens[g]` the tokens
+group g shares.  BlockManager wraps the stateful KV block manager.
 """
 from __future__ import annotations
 
@@ -29,7 +31,14 @@ class _Trace(C.Structure):
     _fields_ = [("num_sessions", C.c_int32), ("turn_off", C.c_void_p), ("session_start", C.c_void_p),
                 ("in_tokens", C.c_void_p), ("out_tokens", C.c_void_p), ("tool", C.c_void_p),
                 ("tool_s", C.c_void_p), ("num_tools", C.c_int32), ("hist_off", C.c_void_p),
-                ("hist_s", C.c_void_p)]
+                ("hist_s", C.c_void_p), ("num_groups", C.c_int32), ("session_group", C.c_void_p),
+                ("group_shared_tokens", C.c_void_p)]
+
+
+class _Log(C.Structure):
+    _fields_ = [("capacity", C.c_int64), ("session", C.c_void_p), ("cached_tokens", C.c_void_p),
+                ("new_tokens", C.c_void_p), ("table_off", C.c_void_p), ("tables", C.c_void_p),
+                ("table_capacity", C.c_int64), ("written", C.c_int64)]
 
 
 class _Result(C.Structure):
@@ -40,7 +49,7 @@ class _Result(C.Structure):
 
 
 def _trace(sessions: Sequence[Tuple[float, Sequence[Tuple[int, int, int, float]]]],
-           history: Sequence[Sequence[float]]):
+           history: Sequence[Sequence[float]], groups=None, shared_tokens=None):
     turns = [t for _, ts in sessions for t in ts]
     arr = {
         "turn_off": np.cumsum([0] + [len(ts) for _, ts in sessions]).astype(np.int32),
@@ -51,28 +60,100 @@ def _trace(sessions: Sequence[Tuple[float, Sequence[Tuple[int, int, int, float]]
         "tool_s": np.asarray([t[3] for t in turns], dtype=np.float64),
         "hist_off": np.cumsum([0] + [len(h) for h in history]).astype(np.int32),
         "hist_s": np.asarray([x for h in history for x in h], dtype=np.float64),
+        "session_group": np.asarray(groups if groups is not None else [], dtype=np.int32),
+        "group_shared_tokens": np.asarray(shared_tokens if shared_tokens is not None else [], dtype=np.int32),
     }
     ptr = lambda a: a.ctypes.data if a.size else None
+    n_groups = len(arr["group_shared_tokens"]) if groups is not None else 0
     tr = _Trace(len(sessions), ptr(arr["turn_off"]), ptr(arr["session_start"]), ptr(arr["in_tokens"]),
                 ptr(arr["out_tokens"]), ptr(arr["tool"]), ptr(arr["tool_s"]), len(history),
-                ptr(arr["hist_off"]), ptr(arr["hist_s"]))
+                ptr(arr["hist_off"]), ptr(arr["hist_s"]), n_groups,
+                ptr(arr["session_group"]) if n_groups else None,
+                ptr(arr["group_shared_tokens"]) if n_groups else None)
     return tr, arr  # keep the arrays alive with the struct
 
 
 def simulate(sessions, history, *, capacity_blocks: int, block_tokens: int,
              prefill_s_per_token: float = 0.0, decode_s_per_token: float = 0.0,
-             sched: str = "prefix", evict: str = "predictive", rebuild_every: int = 3) -> Dict:
-    tr, keep = _trace(sessions, history)
+             sched: str = "prefix", evict: str = "predictive", rebuild_every: int = 3,
+             groups=None, shared_tokens=None, log: bool = False) -> Dict:
+    """Runs the simulation; with `log`, out["log"] lists per dispatch (session,
+    cached_tokens, new_tokens, block table)."""
+    tr, keep = _trace(sessions, history, groups, shared_tokens)
     cfg = _Config(capacity_blocks, block_tokens, prefill_s_per_token, decode_s_per_token,
                   SCHED[sched], EVICT[evict], rebuild_every)
     res = _Result()
     n_turns = int(keep["turn_off"][-1])
-    order = np.zeros(max(n_turns, 1), dtype=np.int32)
-    _check(library().cw_policy_simulate(C.byref(cfg), C.byref(tr), C.byref(res), order.ctypes.data,
-                                        n_turns))
+    if not log:
+        order = np.zeros(max(n_turns, 1), dtype=np.int32)
+        _check(library().cw_policy_simulate(C.byref(cfg), C.byref(tr), C.byref(res), order.ctypes.data,
+                                            n_turns))
+        out = {name: getattr(res, name) for name, _ in _Result._fields_}
+        out["dispatch"] = order[:min(res.requests, n_turns)].tolist()
+        return out
+    cap = max(n_turns, 1)
+    tcap = int(sum(-(-sum(t[0] + t[1] for t in ts[:j + 1]) // block_tokens)
+                   for _, ts in sessions for j in range(len(ts)))) + 1
+    a = {"session": np.zeros(cap, np.int32), "cached_tokens": np.zeros(cap, np.int32),
+         "new_tokens": np.zeros(cap, np.int32), "table_off": np.zeros(cap + 1, np.int64),
+         "tables": np.zeros(max(tcap, 1), np.int32)}
+    lg = _Log(cap, a["session"].ctypes.data, a["cached_tokens"].ctypes.data, a["new_tokens"].ctypes.data,
+              a["table_off"].ctypes.data, a["tables"].ctypes.data, len(a["tables"]), 0)
+    _check(library().cw_policy_simulate_log(C.byref(cfg), C.byref(tr), C.byref(res), C.byref(lg)))
     out = {name: getattr(res, name) for name, _ in _Result._fields_}
-    out["dispatch"] = order[:min(res.requests, n_turns)].tolist()
+    n = lg.written
+    out["dispatch"] = a["session"][:n].tolist()
+    out["log"] = [(int(a["session"][i]), int(a["cached_tokens"][i]), int(a["new_tokens"][i]),
+                   a["tables"][a["table_off"][i]:a["table_off"][i + 1]].tolist()) for i in range(n)]
     return out
+
+
+class BlockManager:
+    """The KV block manager (cw_bm_*): register sessions, admit and release
+    their requests, rebuild the eviction heap."""
+
+    def __init__(self, capacity_blocks: int, block_tokens: int):
+        self._h = C.c_void_p()
+        _check(library().cw_bm_create(capacity_blocks, block_tokens, C.byref(self._h)))
+        self.capacity_blocks, self.block_tokens = capacity_blocks, block_tokens
+
+    def close(self):
+        if self._h:
+            library().cw_bm_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def add_session(self, session: int, group: int = -1, shared_tokens: int = 0):
+        _check(library().cw_bm_add_session(self._h, session, group, shared_tokens))
+
+    def admit(self, session: int, context_tokens: int, input_tokens: int, output_tokens: int):
+        """Returns (block table, cached prompt tokens, evicted blocks)."""
+        need = -(-(context_tokens + input_tokens + output_tokens) // self.block_tokens)
+        table = np.zeros(max(need, 1), dtype=np.int32)
+        blocks, cached, evicted = C.c_int32(), C.c_int64(), C.c_int64()
+        _check(library().cw_bm_admit(self._h, session, context_tokens, input_tokens, output_tokens,
+                                     table.ctypes.data, len(table), C.byref(blocks), C.byref(cached),
+                                     C.byref(evicted)))
+        return table[:blocks.value].copy(), cached.value, evicted.value
+
+    def release(self, session: int, value: float):
+        _check(library().cw_bm_release(self._h, session, float(value)))
+
+    def rebuild(self, values: Dict[int, float]):
+        s = np.asarray(list(values.keys()), dtype=np.int32)
+        v = np.asarray(list(values.values()), dtype=np.float64)
+        _check(library().cw_bm_rebuild(self._h, s.ctypes.data if s.size else None,
+                                       v.ctypes.data if v.size else None, len(s)))
+
+    def stats(self):
+        f, r = C.c_int64(), C.c_int64()
+        _check(library().cw_bm_stats(self._h, C.byref(f), C.byref(r)))
+        return {"free_blocks": f.value, "referenced_blocks": r.value}
 
 
 def predict(history: Sequence[Sequence[float]], tool: int, elapsed_s: float) -> float:

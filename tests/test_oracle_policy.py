@@ -218,13 +218,15 @@ def test_shared_blocks_of_finished_sharers_are_evicted_first_worked_example():
     assert (r.requests, r.evicted_blocks, r.prefilled_tokens, r.heap_rebuilds) == (3, 5, 28, 3)
 
 
-@pytest.mark.parametrize("seed", range(4))
-def test_block_model_with_groups_accounting(seed):
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("sched,evict", list(itertools.product(("fcfs", "prefix"),
+                                                               ("lru", "predictive", "belady"))))
+def test_block_model_with_groups_accounting(seed, sched, evict):
     import cw_workloads as cw
     tr = cw.agent_sessions(num_sessions=10, seed=2100 + seed, max_turns=8, shared_groups=2,
                            shared_prefix_tokens=1024)
     cfg = cp.Config(M=tr.capacity_blocks, block_tokens=tr.block_tokens, prefill_s_per_token=1e-5,
-                    decode_s_per_token=1e-3, sched="prefix", evict="predictive", n_rebuild=3)
+                    decode_s_per_token=1e-3, sched=sched, evict=evict, n_rebuild=3)
     r, log = cp.simulate_blocks(cfg, _to_oracle_sessions(tr.sessions, tr.groups), tr.history,
                                 shared_tokens=tr.shared_tokens)
     assert sum(d.new_tokens for d in log) == r.prefilled_tokens

@@ -80,3 +80,100 @@ def test_validation():
         t2, k2 = policy._trace(bad_sessions, hist)
         assert _raw(good, t2) == L.CW_ERR_BAD_LENS
     assert policy.library().cw_last_error_message()
+
+
+# ---- the block manager with shared prefix groups
+
+def _to_oracle_groups(sessions, groups):
+    return [cp.SessionSpec(st, [cp.Turn(*t) for t in turns], group=groups[i])
+            for i, (st, turns) in enumerate(sessions)]
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("sched,evict", list(itertools.product(("fcfs", "prefix"),
+                                                               ("lru", "predictive", "belady"))))
+def test_simulator_with_shared_prefixes_matches_oracle(seed, sched, evict):
+    tr = cw.agent_sessions(num_sessions=10, seed=2100 + seed, max_turns=8, shared_groups=2,
+                           shared_prefix_tokens=1024)
+    kw = dict(capacity_blocks=tr.capacity_blocks, block_tokens=tr.block_tokens,
+              prefill_s_per_token=tr.prefill_s_per_token, decode_s_per_token=tr.decode_s_per_token)
+    got = policy.simulate(tr.sessions, tr.history, sched=sched, evict=evict, rebuild_every=3,
+                          groups=tr.groups, shared_tokens=tr.shared_tokens, log=True, **kw)
+    want, wlog = cp.simulate_blocks(
+        cp.Config(M=tr.capacity_blocks, block_tokens=tr.block_tokens,
+                  prefill_s_per_token=tr.prefill_s_per_token, decode_s_per_token=tr.decode_s_per_token,
+                  sched=sched, evict=evict, n_rebuild=3),
+        _to_oracle_groups(tr.sessions, tr.groups), tr.history, shared_tokens=tr.shared_tokens)
+    assert got["dispatch"] == want.dispatch
+    for f in FIELDS_EXACT:
+        assert got[f] == getattr(want, f), f
+    for f in FIELDS_TIME:
+        assert got[f] == pytest.approx(getattr(want, f), rel=1e-12), f
+    assert [(s, c, n, len(t)) for s, c, n, t in got["log"]] == \
+        [(d.session, d.cached_tokens, d.new_tokens, d.blocks) for d in wlog]
+    assert any(c > 0 for _, c, _, _ in got["log"])
+    for _, _, _, t in got["log"]:
+        assert len(set(t)) == len(t) and min(t) >= 0 and max(t) < tr.capacity_blocks
+
+
+def test_simulator_worked_sharing_examples():
+    # the oracle's hand-worked cases, through the library
+    got = policy.simulate([(0.0, [(10, 2, 0, 0.0)]), (100.0, [(9, 3, 0, 0.0)])], [[1.0]],
+                          capacity_blocks=10, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs",
+                          evict="lru", groups=[0, 0], shared_tokens=[8], log=True)
+    assert [(s, c, n, len(t)) for s, c, n, t in got["log"]] == [(0, 0, 10, 3), (1, 8, 1, 3)]
+    assert got["log"][0][3][:2] == got["log"][1][3][:2]  # the shared blocks are the same blocks
+    got = policy.simulate([(0.0, [(10, 2, 0, 50.0), (4, 0, 0, 0.0)]), (20.0, [(9, 3, 0, 0.0)]),
+                           (30.0, [(8, 0, 0, 0.0)])], [[1.0]], capacity_blocks=5, block_tokens=4,
+                          prefill_s_per_token=1.0, sched="fcfs", evict="lru", groups=[0, 0, -1],
+                          shared_tokens=[8], log=True)
+    assert got["dispatch"] == [0, 1, 2, 0]
+    assert [(c, n, len(t)) for _, c, n, t in got["log"]] == [(0, 10, 3), (8, 1, 3), (0, 8, 2), (8, 8, 4)]
+    assert (got["evicted_blocks"], got["faults"], got["recomputed_tokens"], got["prefilled_tokens"]) == (3, 1, 4, 27)
+
+
+def test_block_manager_references_sharing_and_eviction_order():
+    bm = policy.BlockManager(capacity_blocks=6, block_tokens=4)
+    bm.add_session(0, group=0, shared_tokens=8)
+    bm.add_session(1, group=0, shared_tokens=8)
+    bm.add_session(2)
+    t0, cached, ev = bm.admit(0, 0, 10, 2)  # 3 blocks: 2 shared + 1 private
+    assert len(t0) == 3 and cached == 0 and ev == 0
+    assert bm.stats() == {"free_blocks": 3, "referenced_blocks": 3}
+    t1, cached, ev = bm.admit(1, 0, 9, 3)   # both requests run at once: the shared blocks have 2 refs
+    assert list(t1[:2]) == list(t0[:2]) and cached == 8 and len(t1) == 3 and t1[2] != t0[2]
+    assert bm.stats() == {"free_blocks": 2, "referenced_blocks": 4}
+    with pytest.raises(RuntimeError):
+        bm.admit(2, 0, 12, 0)  # 3 blocks, only 2 free and nothing unreferenced
+    bm.release(0, 5.0)
+    assert bm.stats()["referenced_blocks"] == 3  # session 1 still holds the shared blocks
+    t2, cached, ev = bm.admit(2, 0, 12, 0)      # evicts session 0's private block only
+    assert cached == 0 and ev == 1 and t0[2] in list(t2)
+    bm.release(1, 1.0)
+    bm.release(2, 9.0)
+    # session 3 needs 5 blocks with none free: session 2's blocks go first (value
+    # 9), then session 1's private block (value 1), then the tail shared block
+    # (the smallest sharer value, 1, and after the sharers' private blocks)
+    bm.add_session(3)
+    t3, _, ev = bm.admit(3, 0, 20, 0)
+    assert ev == 5 and set(t3) == set(t2) | {t1[2], t1[1]}
+    assert bm.stats() == {"free_blocks": 0, "referenced_blocks": 5}
+    bm.release(3, 7.0)
+    t0b, cached, _ = bm.admit(0, 12, 4, 0)      # only the head shared block is still resident
+    assert cached == 4 and t0b[0] == t0[0]
+    with pytest.raises(RuntimeError):
+        bm.release(2, 0.0)  # no request running
+    bm.close()
+
+
+def test_block_manager_rebuild_reorders_eviction():
+    bm = policy.BlockManager(capacity_blocks=4, block_tokens=4)
+    for s in range(3):
+        bm.add_session(s)
+    a, _, _ = bm.admit(0, 0, 8, 0)
+    bm.release(0, 1.0)
+    b, _, _ = bm.admit(1, 0, 8, 0)
+    bm.release(1, 2.0)  # larger value: evicted first
+    bm.rebuild({0: 3.0, 1: 2.0})  # now session 0's blocks go first
+    c, _, ev = bm.admit(2, 0, 8, 0)
+    assert ev == 2 and set(c) == set(a)
