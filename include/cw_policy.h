@@ -153,7 +153,11 @@ cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_t
  * request's references; blocks left unreferenced enter the eviction heap with
  * `value` (larger evicts first).  cw_bm_rebuild sets the values of the listed
  * sessions and rebuilds the heap from every session's value (the periodic
- * rebuild).  Errors: CW_ERR_NULL, CW_ERR_BAD_LENS (unknown or running
+ * rebuild).  Several requests may be admitted before any runs (one serving
+ * step), with one restriction: while a group's shared blocks are not all
+ * resident, admit at most one of its members per step, since the blocks that
+ * member allocates are reported as the next member's resident prefix before
+ * they hold its K/V.  Errors: CW_ERR_NULL, CW_ERR_BAD_LENS (unknown or running
  * session, negative counts, NaN values), CW_ERR_UNSUPPORTED (sizes). */
 typedef struct cw_block_manager cw_block_manager_t;
 cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out);
