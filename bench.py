@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--extend-kernel", type=int, default=0, choices=[0, 1, 2],
                     help="extend kernel for bf16 pools: 0 or 1 eight waves of 32 rows (default), "
                          "2 four waves of 64 rows")
+    ap.add_argument("--deal-rounds", type=int, default=1, choices=[0, 1],
+                    help="1 (default): a (sequence, kv head) that fills whole GPU rounds is dealt "
+                         "across all XCDs round by round; 0: it stays on one XCD")
     ap.add_argument("--separate-calls", action="store_true",
                     help="time a step as cw_kv_write_pages + cw_extend_attention (or "
                          "cw_decode_attention) instead of cw_step_attention")
@@ -604,6 +607,7 @@ def main():
     global EXTEND_KERNEL
     EXTEND_KERNEL = args.extend_kernel
     cwlib.set_tuning(cwlib._lib.CW_TUNE_EXTEND_KERNEL, args.extend_kernel)
+    cwlib.set_tuning(cwlib._lib.CW_TUNE_DEAL_ROUNDS, args.deal_rounds)
     res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,
                        cold_steps=args.cold_steps, power_s=args.power_seconds)
     ceil = measure_ceilings(power_s=args.power_seconds) if args.ceilings else None

@@ -286,11 +286,17 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           item (the default), 2 = four waves of 64 rows
  *                           (bf16 pools only; fp8 pools always run the
  *                           eight-wave kernel).
+ *   CW_TUNE_DEAL_ROUNDS     1 = the work of a (sequence, kv head) that fills
+ *                           whole rounds of the GPU (a work item per resident
+ *                           workgroup on every XCD) is dealt across all XCDs a
+ *                           round at a time (the default); 0 = it stays on one
+ *                           XCD.  Larger values act as 1.
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {
   CW_TUNE_KV_CHUNK_TILES = 0,
   CW_TUNE_TARGET_WGS = 1,
   CW_TUNE_EXTEND_KERNEL = 2,
+  CW_TUNE_DEAL_ROUNDS = 3,
   CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
   CW_TUNE_RANGE_MAX_ = 2147483647
 } cw_tune_key_t;

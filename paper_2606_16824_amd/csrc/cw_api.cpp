@@ -998,6 +998,7 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
       if (value > 2) return fail(CW_ERR_UNSUPPORTED, "extend kernel %d is not 0, 1 or 2", value);
       g_tuning.extend_kernel = value;
       return CW_OK;
+    case CW_TUNE_DEAL_ROUNDS: g_tuning.deal_rounds = value; return CW_OK;
     default: break;
   }
   return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));

@@ -9,15 +9,18 @@
 //
 // Launch order is XCD-aware: the dispatcher hands workgroup i to XCD i % X, and
 // each XCD has its own L2.  All tiles of one (sequence, kv head) read the same
-// keys, so they are kept on one XCD (split into several bundles only when there
-// are fewer bundles than XCDs), bundles are spread over XCDs
-// longest-processing-time first, and the per-XCD queues are interleaved.
+// keys, so the work of a (sequence, kv head) that fills whole rounds of the GPU
+// is dealt round by round across all XCDs (every XCD streams the same keys at
+// the same time), and the rest of it is kept on one XCD (split into several
+// bundles only when there are fewer bundles than XCDs), bundles spread over
+// XCDs longest-processing-time first; the per-XCD queues are interleaved.
 // Queues that run out early are padded with idle items so that later items
 // still land on their XCD.
 #include "planner.h"
 
 #include <algorithm>
 #include <climits>
+#include <iterator>
 #include <numeric>
 
 namespace cw {
@@ -140,8 +143,45 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
     flush();
   }
 
-  // 4. enough bundles to occupy every XCD: halve the largest while possible
+  // 4. Bundles that fill whole rounds of the GPU (R items per XCD, one per
+  // resident workgroup slot): dealt across every XCD a round at a time, so all
+  // XCDs stream the keys of the same (sequence, kv head) at once and what one
+  // XCD's L2 has dropped is still in the memory-side cache for the others (a
+  // bundle kept on one XCD for several rounds has all XCDs streaming different
+  // heads, more than that cache holds).  The items of every other round run in
+  // reverse order, so the slot that drew a short tile draws a long one next and
+  // the slots of an XCD stay close together in the key stream.  Within a round
+  // each XCD takes consecutive items (tiles of about equal length), rotating
+  // over the round's blocks from one round to the next.
   const int32_t X = std::max(1, num_xcds);
+  const int64_t R = std::max<int64_t>(1, int64_t(std::max(1, wgs_per_cu)) * num_cus / X);
+  std::vector<std::vector<WorkItem>> queues(X);
+  if (tuning.deal_rounds != 0) {
+    int64_t round = 0;
+    for (auto& bd : bundles) {
+      const int64_t n_rounds = static_cast<int64_t>(bd.items.size()) / (R * X);
+      for (int64_t r = 0; r < n_rounds; ++r, ++round)
+        for (int32_t x = 0; x < X; ++x) {
+          // XCD x takes block (x + round) % X of the round's X blocks of R
+          // items: blocks later in a bundle hold longer tiles (more keys), and
+          // the rotation gives every XCD each position in turn
+          const auto b0 = bd.items.begin() + (r * X + (x + round) % X) * R;
+          if (round & 1) queues[x].insert(queues[x].end(), std::make_reverse_iterator(b0 + R),
+                                          std::make_reverse_iterator(b0));
+          else queues[x].insert(queues[x].end(), b0, b0 + R);
+        }
+      if (n_rounds > 0) {
+        bd.items.erase(bd.items.begin(), bd.items.begin() + n_rounds * R * X);
+        bd.cost = 0;
+        for (auto& w : bd.items) bd.cost += (w.kv_end - w.kv_begin + BLOCK_N - 1) / BLOCK_N;
+      }
+    }
+    bundles.erase(std::remove_if(bundles.begin(), bundles.end(),
+                                 [](const Bundle& b) { return b.items.empty(); }),
+                  bundles.end());
+  }
+
+  // 5. enough bundles to occupy every XCD: halve the largest while possible
   while (static_cast<int32_t>(bundles.size()) < 2 * X) {
     auto it = std::max_element(bundles.begin(), bundles.end(),
                                [](const Bundle& a, const Bundle& c) { return a.items.size() < c.items.size(); });
@@ -156,10 +196,10 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
     bundles.push_back(std::move(hi));
   }
 
-  // 5. LPT assignment of bundles to XCD queues, then interleave
+  // 6. LPT assignment of the other bundles to XCD queues (after the dealt
+  // rounds, which every queue holds the same number of), then interleave
   std::stable_sort(bundles.begin(), bundles.end(),
                    [](const Bundle& a, const Bundle& c) { return a.cost > c.cost; });
-  std::vector<std::vector<WorkItem>> queues(X);
   std::vector<int64_t> load(X, 0);
   for (auto& bd : bundles) {
     const int32_t x = static_cast<int32_t>(std::min_element(load.begin(), load.end()) - load.begin());
@@ -179,7 +219,7 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
   // trailing idle items launch nothing useful
   while (!plan.items.empty() && plan.items.back().seq < 0) plan.items.pop_back();
 
-  // 6. workspace layout
+  // 7. workspace layout
   plan.part_rows = block_m;
   layout_workspace(plan, head_dim);
   return plan;

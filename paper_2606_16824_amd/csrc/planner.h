@@ -14,6 +14,7 @@ struct Tuning {
   int32_t kv_chunk_tiles = 0;  // 0 = automatic
   int32_t target_wgs = 0;      // 0 = automatic
   int32_t extend_kernel = 0;   // 0 = automatic, 1 = eight waves of 32 rows, 2 = four waves of 64 rows
+  int32_t deal_rounds = 1;     // 1 = deal bundles of whole GPU rounds across XCDs, 0 = keep them on one
 };
 
 struct ExtendPlan {

@@ -41,6 +41,9 @@ SMALL_CASES = {
     "gqa16_d128_fp8": ([200, 17], [24, 3], 1, 16, 128, 16, "fp8"),
     "fp8_p64_d128": ([129, 64, 300], [33, 90, 1], 2, 4, 128, 64, "fp8"),
     "fp8_p16_d64": ([50, 130, 17], [20, 45, 3], 2, 4, 64, 16, "fp8"),
+    # 263 query tiles of one (sequence, kv head): one round dealt across all XCDs,
+    # the rest and the second sequence queued behind it
+    "dealt_round": ([100, 30], [4200, 50], 1, 16, 64, 16, "bf16"),
     # 40 short ragged sequences: many bundles, idle padding in the XCD queues
     "many_seqs": ([(37 * i) % 301 for i in range(40)], [1 + (11 * i) % 40 for i in range(40)],
                   2, 4, 128, 16, "bf16"),

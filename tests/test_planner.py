@@ -48,11 +48,45 @@ def test_turn_plan_fills_every_cu():
         assert len(set(items[x::8, 1].tolist())) == 1
 
 
-def test_long_plan_is_unsplit_and_head_aligned():
+def test_long_plan_is_dealt_round_by_round():
+    """Long: 8 kv heads x 256 tiles, unsplit.  Round r (workgroups 256r ..
+    256r + 255, 32 per XCD) is all of kv head r, every XCD streaming it at once;
+    XCD x gets the 32 consecutive tiles of block (x + r) % 8, in reverse order
+    on odd rounds, so over the eight rounds every XCD does every block once."""
     items = check_plan([131072], [8192], 8, 8, p=64)
     assert len(items) == 2048 and np.all(items[:, 5] == -1)
+    keys = np.zeros(8)
+    for r in range(8):
+        rnd = items[256 * r:256 * (r + 1)]
+        assert set(rnd[:, 1].tolist()) == {r}
+        for x in range(8):
+            tiles = rnd[x::8, 2] // BM  # query tile index, in launch order on XCD x
+            blk = (x + r) % 8
+            want = np.arange(32 * blk, 32 * blk + 32)
+            assert np.array_equal(tiles, want[::-1] if r % 2 else want)
+            keys[x] += (rnd[x::8, 4] - rnd[x::8, 3]).sum()
+    assert keys.max() == keys.min()  # every XCD streams the same number of keys
+
+
+def test_long_plan_without_dealing_keeps_a_head_per_xcd():
+    cwlib.set_tuning(3, 0)
+    try:
+        items = check_plan([131072], [8192], 8, 8, p=64)
+    finally:
+        cwlib.set_tuning(3, 1)
+    assert len(items) == 2048
     for x in range(8):
         assert len(set(items[x::8, 1].tolist())) == 1
+
+
+def test_dealt_rounds_then_bundles():
+    """A bundle of 300 tiles deals one round (256 items) and leaves 44 items
+    that, with a second sequence's bundles, go to the XCD queues after it."""
+    items = check_plan([4000, 500], [300 * 64, 100], 1, 4)
+    real = items[items[:, 0] >= 0]
+    first = items[:256]
+    assert np.all(first[:, 0] == 0) and np.all(first[:, 5] == -1)
+    assert len(real) == 300 + 2
 
 
 @pytest.mark.parametrize("lp,ls,hkv,g", [
