@@ -291,12 +291,19 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           workgroup on every XCD) is dealt across all XCDs a
  *                           round at a time (the default); 0 = it stays on one
  *                           XCD.  Larger values act as 1.
+ *   CW_TUNE_PLAN_DIRECT     0 = the attention calls copy their plan from the
+ *                           pinned staging slot into the workspace with a
+ *                           small kernel before the attention kernels; 1 = the
+ *                           kernels read it from the staging slot over the
+ *                           host link (no copy kernel; cw_extend_attention_noalloc
+ *                           always copies).  Larger values act as 1.
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {
   CW_TUNE_KV_CHUNK_TILES = 0,
   CW_TUNE_TARGET_WGS = 1,
   CW_TUNE_EXTEND_KERNEL = 2,
   CW_TUNE_DEAL_ROUNDS = 3,
+  CW_TUNE_PLAN_DIRECT = 4,
   CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
   CW_TUNE_RANGE_MAX_ = 2147483647
 } cw_tune_key_t;

@@ -175,17 +175,22 @@ cw_status_t current_state(DeviceState** out) {
   return CW_OK;
 }
 
-// Copies `bytes` of host data to `dst` on `stream` through a pinned staging
-// slot, so that the copy is asynchronous and the caller's host buffer can be
-// reused at once.  A slot is reused only after its previous copy completed.
-// `fill(host)` writes the `bytes` bytes into the slot (the plan is packed there
-// directly, without an intermediate buffer).  The ring is set up on the first
-// use on a device when cw_init has not done it, unless `no_alloc` is set, in
-// which case an uninitialised device is an error (CW_ERR_INIT).
-template <class Fill>
-cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
-                        bool no_alloc = false) {
-  if (bytes == 0) return CW_OK;
+// Stages `bytes` of host data for `stream` in a pinned staging slot, so that the
+// caller's host buffer can be reused at once, and enqueues the kernels that read
+// it: `fill(host)` writes the bytes into the slot (the plan is packed there
+// directly, without an intermediate buffer), then `launch(base)` enqueues the
+// kernels, with `base` the device address they read the data at.  Copy mode:
+// a small kernel copies the slot to `dst` (device memory) and base = dst.
+// Direct mode: the kernels read the slot itself over the host link (base = the
+// slot's device address), which saves the copy kernel and its launch gap; the
+// slot is then held until those kernels have run.  A slot is reused only after
+// the event recorded behind its last reader has completed.  The ring is set up
+// on the first use on a device when cw_init has not done it, unless `no_alloc`
+// is set, in which case an uninitialised device is an error (CW_ERR_INIT).
+template <class Fill, class Launch>
+cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
+                             Launch&& launch, bool no_alloc, bool direct) {
+  if (bytes == 0) return launch(static_cast<const uint8_t*>(dst));
   if (bytes > kStagingSlotBytes)
     return fail(CW_ERR_UNSUPPORTED,
                 "the call's plan takes %zu bytes, more than the %zu-byte staging slot "
@@ -210,16 +215,34 @@ cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill
     s.pending = false;
   }
   fill(static_cast<uint8_t*>(s.host));
-  e = launch_stage_copy(s.dev, dst, bytes, stream);
-  if (e != hipSuccess) return hip_fail(e, "plan upload kernel launch");
+  cw_status_t launched = CW_OK;
+  if (direct) {
+    launched = launch(static_cast<const uint8_t*>(s.dev));
+  } else {
+    e = launch_stage_copy(s.dev, dst, bytes, stream);
+    if (e != hipSuccess) return hip_fail(e, "plan upload kernel launch");
+  }
+  // recorded even when a launch failed: whatever was enqueued may read the slot
   e = hipEventRecord(s.ev, stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   s.pending = true;
-  return CW_OK;
+  if (direct) return launched;
+  return launch(static_cast<const uint8_t*>(dst));
+}
+
+template <class Fill>
+cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill) {
+  return stage_and_launch(bytes, dst, stream, fill, [](const uint8_t*) { return CW_OK; }, false, false);
 }
 
 cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
   return upload_fill(bytes, dst, stream, [&](uint8_t* h) { std::memcpy(h, src, bytes); });
+}
+
+// Whether a call's plan is read by its kernels straight from the staging slot
+// (CW_TUNE_PLAN_DIRECT).
+bool plan_direct(bool no_alloc) {
+  return !no_alloc && current_tuning().plan_direct != 0;
 }
 
 // A byte range of one argument, for the aliasing check.
@@ -402,12 +425,13 @@ StepPlan make_step_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, 
   return sp;
 }
 
-// Kernel arguments of a plan whose meta sits at ws + meta and partials at ws + part.
-ExtendParams plan_params(const ExtendPlan& plan, uint8_t* ws, size_t meta, size_t part) {
+// Kernel arguments of a plan whose meta is read at `meta` and whose partials
+// sit at ws + part.
+ExtendParams plan_params(const ExtendPlan& plan, const uint8_t* meta, uint8_t* ws, size_t part) {
   ExtendParams p{};
-  p.seqs = reinterpret_cast<const SeqInfo*>(ws + meta + plan.off_seqs);
-  p.items = reinterpret_cast<const WorkItem*>(ws + meta + plan.off_items);
-  p.groups = reinterpret_cast<const CombineGroup*>(ws + meta + plan.off_groups);
+  p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
+  p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
+  p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
   p.part_o = reinterpret_cast<float*>(ws + part + (plan.off_part_o - plan.meta_bytes));
   p.part_ml = reinterpret_cast<float*>(ws + part + (plan.off_part_ml - plan.meta_bytes));
   p.n_items = static_cast<int32_t>(plan.items.size());
@@ -459,9 +483,6 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   if (s != CW_OK) return s;
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  s = upload_fill(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); }, no_alloc);
-  if (s != CW_OK) return s;
-
   ExtendParams p{};
   p.q = q;
   p.k_new = k_new;
@@ -473,9 +494,6 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   p.block_table = block_table;
   p.out = out;
   p.lse = lse;
-  p.seqs = reinterpret_cast<const SeqInfo*>(ws + plan.off_seqs);
-  p.items = reinterpret_cast<const WorkItem*>(ws + plan.off_items);
-  p.groups = reinterpret_cast<const CombineGroup*>(ws + plan.off_groups);
   p.part_o = reinterpret_cast<float*>(ws + plan.off_part_o);
   p.part_ml = reinterpret_cast<float*>(ws + plan.off_part_ml);
   p.bt_stride = bt_stride;
@@ -494,7 +512,6 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     p.w.k_scale = k_scale;
     p.w.v_scale = v_scale;
     p.w.block_table = block_table;
-    p.w.seqs = p.seqs;
     p.w.bt_stride = bt_stride;
     p.w.num_seqs = num_seqs;
     p.w.num_kv_heads = num_kv_heads;
@@ -506,20 +523,28 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     ev0 = g_ev_start;
     ev1 = g_ev_stop;
   }
-  hipError_t e = hipSuccess;
-  if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
-  if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
-  else e = launch_extend(p, head_dim, page_size, fp8, stream);
-  if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
-  if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if (p.n_groups > 0) {
-    int max_parts = 0;
-    for (const CombineGroup& g : plan.groups) max_parts = std::max(max_parts, g.n_parts);
-    e = launch_combine(p, head_dim, max_parts, stream);
-    if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
-  }
-  return CW_OK;
+  auto launch = [&](const uint8_t* meta) -> cw_status_t {
+    p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
+    p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
+    p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
+    if (write_pages) p.w.seqs = p.seqs;
+    hipError_t e = hipSuccess;
+    if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
+    else e = launch_extend(p, head_dim, page_size, fp8, stream);
+    if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
+    if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (p.n_groups > 0) {
+      int max_parts = 0;
+      for (const CombineGroup& g : plan.groups) max_parts = std::max(max_parts, g.n_parts);
+      e = launch_combine(p, head_dim, max_parts, stream);
+      if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
+    }
+    return CW_OK;
+  };
+  return stage_and_launch(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); },
+                          launch, no_alloc, plan_direct(no_alloc));
 }
 
 // Shared by both swap directions: validates and enqueues block src_ids[i] of
@@ -632,15 +657,6 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
                             page_size, kv_dtype, total, out, lse, workspace, workspace_bytes);
   if (s != CW_OK) return s;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  s = upload_fill(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
-    std::fill(h, h + sp.off_ext_meta, uint8_t(0));
-    std::copy(reinterpret_cast<const uint8_t*>(sp.seqs.data()),
-              reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), h);
-    if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, h + sp.off_ext_meta);
-    if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, h + sp.off_dec_meta);
-  });
-  if (s != CW_OK) return s;
-
   auto common = [&](ExtendParams& p) {
     p.q = q;
     p.k_new = k_new;
@@ -666,7 +682,6 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   w.k_scale = k_scale;
   w.v_scale = v_scale;
   w.block_table = block_table;
-  w.seqs = reinterpret_cast<const SeqInfo*>(ws);
   w.bt_stride = bt_stride;
   w.num_seqs = num_seqs;
   w.num_kv_heads = num_kv_heads;
@@ -679,44 +694,54 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     ev1 = g_ev_stop;
   }
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
-  hipError_t e = hipSuccess;
-  // the timing events bracket the extend kernel, or the decode kernel of a
-  // step without extends
-  if (sp.ext.empty() && ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess)
-    return hip_fail(e, "hipEventRecord");
-  if (!sp.dec.empty()) {
-    ExtendParams pd = plan_params(sp.dec_plan, ws, sp.off_dec_meta, sp.off_dec_part);
-    common(pd);
-    // without extends, the decode launch performs the page write (each
-    // sequence's one new token, stored by the work item holding its key)
-    if (sp.ext.empty()) pd.w = w;
-    if ((e = launch_decode(pd, head_dim, page_size, fp8, stream)) != hipSuccess)
-      return hip_fail(e, "decode kernel launch");
-    if (sp.ext.empty() && ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess)
+  auto launch = [&](const uint8_t* meta) -> cw_status_t {
+    w.seqs = reinterpret_cast<const SeqInfo*>(meta);
+    hipError_t e = hipSuccess;
+    // the timing events bracket the extend kernel, or the decode kernel of a
+    // step without extends
+    if (sp.ext.empty() && ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess)
       return hip_fail(e, "hipEventRecord");
-    if (pd.n_groups > 0) {
-      int max_parts = 0;
-      for (const CombineGroup& g : sp.dec_plan.groups) max_parts = std::max(max_parts, g.n_parts);
-      if ((e = launch_combine(pd, head_dim, max_parts, stream)) != hipSuccess)
-        return hip_fail(e, "combine kernel launch");
+    if (!sp.dec.empty()) {
+      ExtendParams pd = plan_params(sp.dec_plan, meta + sp.off_dec_meta, ws, sp.off_dec_part);
+      common(pd);
+      // without extends, the decode launch performs the page write (each
+      // sequence's one new token, stored by the work item holding its key)
+      if (sp.ext.empty()) pd.w = w;
+      if ((e = launch_decode(pd, head_dim, page_size, fp8, stream)) != hipSuccess)
+        return hip_fail(e, "decode kernel launch");
+      if (sp.ext.empty() && ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+      if (pd.n_groups > 0) {
+        int max_parts = 0;
+        for (const CombineGroup& g : sp.dec_plan.groups) max_parts = std::max(max_parts, g.n_parts);
+        if ((e = launch_combine(pd, head_dim, max_parts, stream)) != hipSuccess)
+          return hip_fail(e, "combine kernel launch");
+      }
     }
-  }
-  if (!sp.ext.empty()) {
-    ExtendParams pe = plan_params(sp.ext_plan, ws, sp.off_ext_meta, sp.off_ext_part);
-    common(pe);
-    pe.w = w;  // every sequence's new K/V, written under the extend's first tiles
-    if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if ((e = launch_extend(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
-      return hip_fail(e, "extend kernel launch");
-    if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if (pe.n_groups > 0) {
-      int max_parts = 0;
-      for (const CombineGroup& g : sp.ext_plan.groups) max_parts = std::max(max_parts, g.n_parts);
-      if ((e = launch_combine(pe, head_dim, max_parts, stream)) != hipSuccess)
-        return hip_fail(e, "combine kernel launch");
+    if (!sp.ext.empty()) {
+      ExtendParams pe = plan_params(sp.ext_plan, meta + sp.off_ext_meta, ws, sp.off_ext_part);
+      common(pe);
+      pe.w = w;  // every sequence's new K/V, written under the extend's first tiles
+      if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+      if ((e = launch_extend(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
+        return hip_fail(e, "extend kernel launch");
+      if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+      if (pe.n_groups > 0) {
+        int max_parts = 0;
+        for (const CombineGroup& g : sp.ext_plan.groups) max_parts = std::max(max_parts, g.n_parts);
+        if ((e = launch_combine(pe, head_dim, max_parts, stream)) != hipSuccess)
+          return hip_fail(e, "combine kernel launch");
+      }
     }
-  }
-  return CW_OK;
+    return CW_OK;
+  };
+  return stage_and_launch(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
+    std::fill(h, h + sp.off_ext_meta, uint8_t(0));
+    std::copy(reinterpret_cast<const uint8_t*>(sp.seqs.data()),
+              reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), h);
+    if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, h + sp.off_ext_meta);
+    if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, h + sp.off_dec_meta);
+  }, launch, false, plan_direct(false));
 }
 
 }  // namespace
@@ -999,6 +1024,7 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
       g_tuning.extend_kernel = value;
       return CW_OK;
     case CW_TUNE_DEAL_ROUNDS: g_tuning.deal_rounds = value; return CW_OK;
+    case CW_TUNE_PLAN_DIRECT: g_tuning.plan_direct = value; return CW_OK;
     default: break;
   }
   return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));

@@ -163,6 +163,8 @@ def test_tuning_keys():
     assert lib().cw_set_tuning(L.CW_TUNE_EXTEND_KERNEL, 0) == L.CW_OK
     assert lib().cw_set_tuning(L.CW_TUNE_DEAL_ROUNDS, 0) == L.CW_OK
     assert lib().cw_set_tuning(L.CW_TUNE_DEAL_ROUNDS, 1) == L.CW_OK
+    assert lib().cw_set_tuning(L.CW_TUNE_PLAN_DIRECT, 1) == L.CW_OK
+    assert lib().cw_set_tuning(L.CW_TUNE_PLAN_DIRECT, 0) == L.CW_OK
 
 
 def _swap(out=True, **over):
