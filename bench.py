@@ -457,7 +457,7 @@ def run_others(names, steps: int, warmup: int = 5):
                          "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
                          "kernel_GB_s": round(nbytes / (kern * 1e-3) / 1e9, 1),
                          "frac_hbm_peak": round(nbytes / (kern * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-                         "algorithmic_bytes": nbytes}
+                         "algorithmic_bytes": nbytes, "traffic": measured_traffic("decode", name)}
         else:
             flops = s.flops()
             out[name] = {"workload": WORKLOAD_DESC[name], "ms_per_step": round(ms, 5),
