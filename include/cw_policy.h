@@ -64,7 +64,7 @@ typedef enum { CW_SCHED_FCFS = 0, CW_SCHED_PREFIX_AWARE = 1 } cw_sched_policy_t;
 typedef enum { CW_EVICT_LRU = 0, CW_EVICT_PREDICTIVE = 1, CW_EVICT_BELADY = 2 } cw_evict_policy_t;
 
 typedef struct {
-  int32_t capacity_blocks;     /* M >= 1 */
+  int32_t capacity_blocks;     /* M, 1 .. 2^26 */
   int32_t block_tokens;        /* >= 1 */
   double prefill_s_per_token;  /* >= 0 */
   double decode_s_per_token;   /* >= 0 */
@@ -108,7 +108,8 @@ typedef struct {
 /* Runs the simulation.  `dispatch` (optional, NULL to skip) receives the
  * session of each dispatched request in order, up to `dispatch_capacity`
  * entries.  CW_ERR_NULL for a missing required pointer, CW_ERR_UNSUPPORTED for
- * an out-of-range configuration, CW_ERR_BAD_LENS for an invalid trace
+ * an out-of-range configuration or exhausted host memory, CW_ERR_BAD_LENS for an
+ * invalid trace
  * (negative values, bad offsets or tool ids, or a turn needing more than
  * capacity_blocks blocks). */
 cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
@@ -157,8 +158,13 @@ cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_t
  * step), with one restriction: while a group's shared blocks are not all
  * resident, admit at most one of its members per step, since the blocks that
  * member allocates are reported as the next member's resident prefix before
- * they hold its K/V.  Errors: CW_ERR_NULL, CW_ERR_BAD_LENS (unknown or running
- * session, negative counts, NaN values), CW_ERR_UNSUPPORTED (sizes). */
+ * they hold its K/V.  Limits: capacity_blocks <= 2^26, session and group ids
+ * below 2^24 (ids index dense tables: use small consecutive integers), token
+ * counts of a request <= 2^40.  Errors: CW_ERR_NULL, CW_ERR_BAD_LENS (unknown or
+ * running session, negative or oversized counts, NaN values),
+ * CW_ERR_UNSUPPORTED (sizes beyond the limits, or host memory exhausted; after
+ * the latter from cw_bm_admit, cw_bm_release or cw_bm_rebuild the manager's
+ * state is undefined and it should only be destroyed).  No call throws. */
 typedef struct cw_block_manager cw_block_manager_t;
 cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out);
 cw_status_t cw_bm_destroy(cw_block_manager_t* bm);

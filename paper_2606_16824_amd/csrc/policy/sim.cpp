@@ -10,6 +10,8 @@
 // unreferenced session every N_rebuild engine iterations).
 #include <cmath>
 #include <cstdarg>
+#include <exception>
+#include <new>
 #include <cstdio>
 #include <limits>
 #include <vector>
@@ -24,6 +26,9 @@ namespace cw {
 namespace {
 
 constexpr double kInf = std::numeric_limits<double>::infinity();
+constexpr int32_t kMaxBlocks = int32_t(1) << 26;  // capacity_blocks (1 GiB of block records)
+constexpr int32_t kMaxIds = int32_t(1) << 24;     // block manager session and group ids
+constexpr int64_t kMaxTokens = int64_t(1) << 40;  // token counts of one request
 
 cw_status_t policy_fail(cw_status_t s, const char* fmt, ...) {
   char buf[512];
@@ -137,8 +142,21 @@ cw_status_t cw_policy_predict(const cw_sim_trace_t* trace, int32_t tool, double 
 
 namespace {
 
+// Runs `f` and turns a failed host allocation (or any other C++ exception)
+// into a status: nothing is thrown across the C ABI.
+template <class F>
+cw_status_t guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return policy_fail(CW_ERR_UNSUPPORTED, "out of host memory");
+  } catch (const std::exception& e) {
+    return policy_fail(CW_ERR_UNSUPPORTED, "%s", e.what());
+  }
+}
+
 cw_status_t check_config(const cw_sim_config_t& c) {
-  if (c.capacity_blocks < 1 || c.block_tokens < 1 || !(c.prefill_s_per_token >= 0.0) ||
+  if (c.capacity_blocks < 1 || c.capacity_blocks > kMaxBlocks || c.block_tokens < 1 || !(c.prefill_s_per_token >= 0.0) ||
       !(c.decode_s_per_token >= 0.0) || !std::isfinite(c.prefill_s_per_token) ||
       !std::isfinite(c.decode_s_per_token) || c.rebuild_every < 1 ||
       (c.sched != CW_SCHED_FCFS && c.sched != CW_SCHED_PREFIX_AWARE) ||
@@ -323,7 +341,7 @@ cw_status_t cw_policy_simulate(const cw_sim_config_t* config, const cw_sim_trace
   st = check_trace(*trace, config);
   if (st != CW_OK) return st;
   if (dispatch_capacity < 0) return policy_fail(CW_ERR_BAD_LENS, "dispatch_capacity < 0");
-  return simulate(*config, *trace, result, dispatch, dispatch_capacity, nullptr);
+  return guarded([&] { return simulate(*config, *trace, result, dispatch, dispatch_capacity, nullptr); });
 }
 
 cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_trace_t* trace,
@@ -338,7 +356,7 @@ cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_t
   if (log->capacity > 0 && (!log->session || !log->cached_tokens || !log->new_tokens || !log->table_off))
     return policy_fail(CW_ERR_NULL, "log arrays are required");
   if (log->table_capacity > 0 && !log->tables) return policy_fail(CW_ERR_NULL, "log tables are required");
-  return simulate(*config, *trace, result, nullptr, 0, log);
+  return guarded([&] { return simulate(*config, *trace, result, nullptr, 0, log); });
 }
 
 struct cw_block_manager {
@@ -350,17 +368,15 @@ struct cw_block_manager {
 cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out) {
   if (!out) return policy_fail(CW_ERR_NULL, "out is required");
   *out = nullptr;
-  if (capacity_blocks < 1 || block_tokens < 1)
-    return policy_fail(CW_ERR_UNSUPPORTED, "capacity_blocks = %d, block_tokens = %d", capacity_blocks, block_tokens);
-  auto* m = new (std::nothrow) cw_block_manager;
-  if (!m) return policy_fail(CW_ERR_UNSUPPORTED, "out of host memory");
-  m->bm.reset(new (std::nothrow) BlockManager(capacity_blocks, block_tokens));
-  if (!m->bm) {
-    delete m;
-    return policy_fail(CW_ERR_UNSUPPORTED, "out of host memory");
-  }
-  *out = m;
-  return CW_OK;
+  if (capacity_blocks < 1 || capacity_blocks > kMaxBlocks || block_tokens < 1)
+    return policy_fail(CW_ERR_UNSUPPORTED, "capacity_blocks = %d (1 .. %d), block_tokens = %d", capacity_blocks,
+                       kMaxBlocks, block_tokens);
+  return guarded([&] {
+    auto m = std::make_unique<cw_block_manager>();
+    m->bm = std::make_unique<BlockManager>(capacity_blocks, block_tokens);
+    *out = m.release();
+    return CW_OK;
+  });
 }
 
 cw_status_t cw_bm_destroy(cw_block_manager_t* m) {
@@ -372,15 +388,19 @@ cw_status_t cw_bm_add_session(cw_block_manager_t* m, int32_t session, int32_t gr
   if (!m) return policy_fail(CW_ERR_NULL, "block manager is NULL");
   if (session < 0 || group < -1 || shared_tokens < 0)
     return policy_fail(CW_ERR_BAD_LENS, "session %d, group %d, shared_tokens %d", session, group, shared_tokens);
+  if (session >= kMaxIds || group >= kMaxIds)
+    return policy_fail(CW_ERR_UNSUPPORTED, "session %d, group %d: ids must be below %d", session, group, kMaxIds);
   if (session < m->sessions && m->known[session])
     return policy_fail(CW_ERR_BAD_LENS, "session %d is already registered", session);
-  if (session >= m->sessions) {
-    m->sessions = session + 1;
-    m->known.resize(session + 1, 0);
-  }
-  m->known[session] = 1;
-  m->bm->add_session(session, group, shared_tokens);
-  return CW_OK;
+  return guarded([&] {
+    if (session >= m->sessions) {
+      m->known.resize(session + 1, 0);
+      m->sessions = session + 1;
+    }
+    m->bm->add_session(session, group, shared_tokens);
+    m->known[session] = 1;
+    return CW_OK;
+  });
 }
 
 cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_tokens, int64_t input_tokens,
@@ -389,22 +409,27 @@ cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_
   if (!m || !blocks || !cached_tokens) return policy_fail(CW_ERR_NULL, "block manager, blocks and cached_tokens are required");
   if (session < 0 || session >= m->sessions || !m->known[session])
     return policy_fail(CW_ERR_BAD_LENS, "session %d is not registered", session);
-  if (context_tokens < 0 || input_tokens < 0 || output_tokens < 0)
-    return policy_fail(CW_ERR_BAD_LENS, "negative token counts");
+  if (context_tokens < 0 || input_tokens < 0 || output_tokens < 0 || context_tokens > kMaxTokens ||
+      input_tokens > kMaxTokens || output_tokens > kMaxTokens)
+    return policy_fail(CW_ERR_BAD_LENS, "token counts must lie in [0, 2^40]");
   if (m->bm->is_running(session)) return policy_fail(CW_ERR_BAD_LENS, "session %d already has a request running", session);
-  BlockManager::Admission adm;
-  if (!m->bm->admit(session, context_tokens, input_tokens, output_tokens, &adm))
-    return policy_fail(CW_ERR_WORKSPACE, "request of session %d does not fit: the referenced blocks would exceed the capacity", session);
-  std::vector<int32_t> ids;
-  m->bm->table(session, &ids);
-  *blocks = adm.blocks;
-  *cached_tokens = adm.cached_tokens;
-  if (evicted_blocks) *evicted_blocks = adm.evicted;
-  if (table) {
-    const int32_t n = std::min<int32_t>(table_capacity, static_cast<int32_t>(ids.size()));
-    for (int32_t q = 0; q < n; ++q) table[q] = ids[q];
-  }
-  return CW_OK;
+  if (table_capacity < 0) return policy_fail(CW_ERR_BAD_LENS, "table_capacity < 0");
+  return guarded([&] {
+    BlockManager::Admission adm;
+    if (!m->bm->admit(session, context_tokens, input_tokens, output_tokens, &adm))
+      return policy_fail(CW_ERR_WORKSPACE,
+                         "request of session %d does not fit: the referenced blocks would exceed the capacity", session);
+    *blocks = adm.blocks;
+    *cached_tokens = adm.cached_tokens;
+    if (evicted_blocks) *evicted_blocks = adm.evicted;
+    if (table) {
+      std::vector<int32_t> ids;
+      m->bm->table(session, &ids);
+      const int32_t n = std::min<int32_t>(table_capacity, static_cast<int32_t>(ids.size()));
+      for (int32_t q = 0; q < n; ++q) table[q] = ids[q];
+    }
+    return CW_OK;
+  });
 }
 
 cw_status_t cw_bm_release(cw_block_manager_t* m, int32_t session, double value) {
@@ -413,8 +438,10 @@ cw_status_t cw_bm_release(cw_block_manager_t* m, int32_t session, double value) 
     return policy_fail(CW_ERR_BAD_LENS, "session %d is not registered", session);
   if (!m->bm->is_running(session)) return policy_fail(CW_ERR_BAD_LENS, "session %d has no request running", session);
   if (std::isnan(value)) return policy_fail(CW_ERR_BAD_LENS, "eviction value is NaN");
-  m->bm->release(session, value);
-  return CW_OK;
+  return guarded([&] {
+    m->bm->release(session, value);
+    return CW_OK;
+  });
 }
 
 cw_status_t cw_bm_rebuild(cw_block_manager_t* m, const int32_t* sessions, const double* values, int32_t n) {
@@ -426,8 +453,10 @@ cw_status_t cw_bm_rebuild(cw_block_manager_t* m, const int32_t* sessions, const 
     if (std::isnan(values[q])) return policy_fail(CW_ERR_BAD_LENS, "eviction value is NaN");
   }
   for (int32_t q = 0; q < n; ++q) m->bm->set_value(sessions[q], values[q]);
-  m->bm->rebuild();
-  return CW_OK;
+  return guarded([&] {
+    m->bm->rebuild();
+    return CW_OK;
+  });
 }
 
 cw_status_t cw_bm_stats(cw_block_manager_t* m, int64_t* free_blocks, int64_t* referenced_blocks) {

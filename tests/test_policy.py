@@ -177,3 +177,51 @@ def test_block_manager_rebuild_reorders_eviction():
     bm.rebuild({0: 3.0, 1: 2.0})  # now session 0's blocks go first
     c, _, ev = bm.admit(2, 0, 8, 0)
     assert ev == 2 and set(c) == set(a)
+
+
+def test_block_manager_limits_are_errors_not_crashes():
+    """Sizes past the documented limits come back as status codes, and a
+    rejected call changes nothing."""
+    lib = L.load()
+    h = C.c_void_p()
+    assert lib.cw_bm_create((1 << 26) + 1, 16, C.byref(h)) == L.CW_ERR_UNSUPPORTED and not h.value
+    assert lib.cw_bm_create(0, 16, C.byref(h)) == L.CW_ERR_UNSUPPORTED
+    assert lib.cw_bm_create(64, 0, C.byref(h)) == L.CW_ERR_UNSUPPORTED
+    assert lib.cw_bm_create(64, 16, None) == L.CW_ERR_NULL
+    assert lib.cw_bm_create(64, 16, C.byref(h)) == L.CW_OK
+    try:
+        assert lib.cw_bm_add_session(h, 1 << 24, -1, 0) == L.CW_ERR_UNSUPPORTED
+        assert lib.cw_bm_add_session(h, 3, 1 << 24, 0) == L.CW_ERR_UNSUPPORTED
+        assert lib.cw_bm_add_session(h, -1, -1, 0) == L.CW_ERR_BAD_LENS
+        blocks, cached, ev = C.c_int32(), C.c_int64(), C.c_int64()
+        table = np.zeros(8, np.int32)
+        # session 3 was not registered by the rejected calls
+        assert lib.cw_bm_admit(h, 3, 0, 10, 0, table.ctypes.data, 8, C.byref(blocks), C.byref(cached),
+                               C.byref(ev)) == L.CW_ERR_BAD_LENS
+        assert lib.cw_bm_add_session(h, 3, -1, 0) == L.CW_OK
+        assert lib.cw_bm_add_session(h, 3, -1, 0) == L.CW_ERR_BAD_LENS  # twice
+        for args in ((1 << 40) + 1, 0, 0), (0, (1 << 40) + 1, 0), (0, 0, -1):
+            assert lib.cw_bm_admit(h, 3, *args, table.ctypes.data, 8, C.byref(blocks), C.byref(cached),
+                                   C.byref(ev)) == L.CW_ERR_BAD_LENS
+        assert lib.cw_bm_admit(h, 3, 0, 10, 0, table.ctypes.data, -1, C.byref(blocks), C.byref(cached),
+                               C.byref(ev)) == L.CW_ERR_BAD_LENS
+        free, ref = C.c_int64(), C.c_int64()
+        assert lib.cw_bm_stats(h, C.byref(free), C.byref(ref)) == L.CW_OK
+        assert (free.value, ref.value) == (64, 0)
+        # a request larger than the node
+        assert lib.cw_bm_admit(h, 3, 0, 65 * 16, 0, table.ctypes.data, 8, C.byref(blocks), C.byref(cached),
+                               C.byref(ev)) == L.CW_ERR_WORKSPACE
+        assert lib.cw_bm_admit(h, 3, 0, 40, 0, table.ctypes.data, 8, C.byref(blocks), C.byref(cached),
+                               C.byref(ev)) == L.CW_OK
+        assert blocks.value == 3 and list(table[:3]) == [0, 1, 2]
+        assert lib.cw_bm_release(h, 3, float("nan")) == L.CW_ERR_BAD_LENS
+        assert lib.cw_bm_release(h, 3, 1.0) == L.CW_OK
+        assert lib.cw_bm_release(h, 3, 1.0) == L.CW_ERR_BAD_LENS  # nothing running
+    finally:
+        lib.cw_bm_destroy(h)
+
+
+def test_simulator_capacity_limit():
+    tr = cw.agent_sessions(num_sessions=2, seed=2000, max_turns=2)
+    with pytest.raises(RuntimeError):
+        policy.simulate(tr.sessions, tr.history, capacity_blocks=(1 << 26) + 1, block_tokens=16)
