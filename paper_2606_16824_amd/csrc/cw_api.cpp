@@ -2,13 +2,15 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <exception>
 #include <initializer_list>
-#include <atomic>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -744,6 +746,27 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   }, launch, false, plan_direct(false));
 }
 
+// Runs an entry point's body: a failed host allocation (or any other C++
+// exception) becomes a status, so nothing is thrown across the C ABI.
+template <class F>
+cw_status_t guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return fail(CW_ERR_UNSUPPORTED, "out of host memory");
+  } catch (const std::exception& e) {
+    return fail(CW_ERR_UNSUPPORTED, "%s", e.what());
+  }
+}
+template <class T, class F>
+T guarded_value(T on_error, F&& f) {
+  try {
+    return f();
+  } catch (...) {
+    return on_error;
+  }
+}
+
 }  // namespace
 }  // namespace cw
 
@@ -763,9 +786,11 @@ cw_status_t cw_kv_swap_out(const void* k_pool, const void* v_pool, const float* 
                            int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
                            cw_kv_dtype_t kv_dtype, void* workspace, size_t workspace_bytes,
                            hipStream_t stream) {
-  return swap_impl(k_pool, v_pool, k_scale, v_scale, num_pages, k_host, v_host, k_scale_host,
-                   v_scale_host, num_host_blocks, pages_h, host_blocks_h, n, num_kv_heads, head_dim,
-                   page_size, kv_dtype, workspace, workspace_bytes, stream);
+  return guarded([&]() -> cw_status_t {
+    return swap_impl(k_pool, v_pool, k_scale, v_scale, num_pages, k_host, v_host, k_scale_host,
+                     v_scale_host, num_host_blocks, pages_h, host_blocks_h, n, num_kv_heads, head_dim,
+                     page_size, kv_dtype, workspace, workspace_bytes, stream);
+  });
 }
 
 cw_status_t cw_kv_swap_in(const void* k_host, const void* v_host, const float* k_scale_host,
@@ -775,9 +800,11 @@ cw_status_t cw_kv_swap_in(const void* k_host, const void* v_host, const float* k
                           int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
                           cw_kv_dtype_t kv_dtype, void* workspace, size_t workspace_bytes,
                           hipStream_t stream) {
-  return swap_impl(k_host, v_host, k_scale_host, v_scale_host, num_host_blocks, k_pool, v_pool,
-                   k_scale, v_scale, num_pages, host_blocks_h, pages_h, n, num_kv_heads, head_dim,
-                   page_size, kv_dtype, workspace, workspace_bytes, stream);
+  return guarded([&]() -> cw_status_t {
+    return swap_impl(k_host, v_host, k_scale_host, v_scale_host, num_host_blocks, k_pool, v_pool,
+                     k_scale, v_scale, num_pages, host_blocks_h, pages_h, n, num_kv_heads, head_dim,
+                     page_size, kv_dtype, workspace, workspace_bytes, stream);
+  });
 }
 
 size_t cw_write_pages_workspace_bytes(int32_t num_seqs) {
@@ -789,31 +816,33 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
                                  const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                  int32_t num_seqs, int32_t page_size, int32_t* bad_per_seq,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  cw_status_t s = check_shape(num_seqs, 1, 1, 64, page_size);
-  if (s != CW_OK) return s;
-  if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
-  s = check_lens(prefix_lens_h, suffix_lens_h, num_seqs, bt_stride, page_size, 1, 1, 64, true);
-  if (s != CW_OK) return s;
-  if (num_seqs == 0) return CW_OK;
-  if (!block_table || !bad_per_seq) return fail(CW_ERR_NULL, "block_table and bad_per_seq are required");
-  if ((reinterpret_cast<uintptr_t>(block_table) & 3u) || (reinterpret_cast<uintptr_t>(bad_per_seq) & 3u))
-    return fail(CW_ERR_ALIGN, "block_table and bad_per_seq must be 4-byte aligned");
-  if (!aligned16(workspace)) return fail(CW_ERR_ALIGN, "workspace must be 16-byte aligned");
-  const size_t need = cw_write_pages_workspace_bytes(num_seqs);
-  if (workspace == nullptr || workspace_bytes < need)
-    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
-  std::vector<SeqInfo> seqs(num_seqs);
-  int64_t cu = 0;
-  for (int32_t b = 0; b < num_seqs; ++b) {
-    seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), b};
-    cu += suffix_lens_h[b];
-  }
-  s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
-  if (s != CW_OK) return s;
-  const hipError_t e = launch_check_table(block_table, bt_stride, num_pages,
-                                          static_cast<const SeqInfo*>(workspace), num_seqs,
-                                          page_size, bad_per_seq, stream);
-  return e == hipSuccess ? CW_OK : hip_fail(e, "check_table kernel launch");
+  return guarded([&]() -> cw_status_t {
+    cw_status_t s = check_shape(num_seqs, 1, 1, 64, page_size);
+    if (s != CW_OK) return s;
+    if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
+    s = check_lens(prefix_lens_h, suffix_lens_h, num_seqs, bt_stride, page_size, 1, 1, 64, true);
+    if (s != CW_OK) return s;
+    if (num_seqs == 0) return CW_OK;
+    if (!block_table || !bad_per_seq) return fail(CW_ERR_NULL, "block_table and bad_per_seq are required");
+    if ((reinterpret_cast<uintptr_t>(block_table) & 3u) || (reinterpret_cast<uintptr_t>(bad_per_seq) & 3u))
+      return fail(CW_ERR_ALIGN, "block_table and bad_per_seq must be 4-byte aligned");
+    if (!aligned16(workspace)) return fail(CW_ERR_ALIGN, "workspace must be 16-byte aligned");
+    const size_t need = cw_write_pages_workspace_bytes(num_seqs);
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    std::vector<SeqInfo> seqs(num_seqs);
+    int64_t cu = 0;
+    for (int32_t b = 0; b < num_seqs; ++b) {
+      seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), b};
+      cu += suffix_lens_h[b];
+    }
+    s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
+    if (s != CW_OK) return s;
+    const hipError_t e = launch_check_table(block_table, bt_stride, num_pages,
+                                            static_cast<const SeqInfo*>(workspace), num_seqs,
+                                            page_size, bad_per_seq, stream);
+    return e == hipSuccess ? CW_OK : hip_fail(e, "check_table kernel launch");
+  });
 }
 
 cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
@@ -823,59 +852,63 @@ cw_status_t cw_kv_write_pages(const void* k_new, const void* v_new, void* k_pool
                               int32_t num_seqs, int32_t num_kv_heads, int32_t head_dim,
                               int32_t page_size, cw_kv_dtype_t kv_dtype, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
-  cw_status_t s = check_shape(num_seqs, num_kv_heads, 1, head_dim, page_size);
-  if (s != CW_OK) return s;
-  s = check_dtype(kv_dtype, k_scale, v_scale);
-  if (s != CW_OK) return s;
-  if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
-  s = check_lens(prefix_lens_h, suffix_lens_h, num_seqs, bt_stride, page_size, num_kv_heads, 1,
-                 head_dim, true);
-  if (s != CW_OK) return s;
-  const int64_t total = sum_suffix(suffix_lens_h, num_seqs);
-  if (total == 0) return CW_OK;
-  if (!k_new || !v_new || !k_pool || !v_pool || !block_table)
-    return fail(CW_ERR_NULL, "k_new, v_new, k_pool, v_pool and block_table are required");
-  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool) ||
-      !aligned16(workspace))
-    return fail(CW_ERR_ALIGN, "tensor and workspace pointers must be 16-byte aligned");
-  const size_t need = cw_write_pages_workspace_bytes(num_seqs);
-  if (workspace == nullptr || workspace_bytes < need)
-    return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
-  std::vector<SeqInfo> seqs(num_seqs);
-  int64_t cu = 0;
-  for (int32_t b = 0; b < num_seqs; ++b) {
-    seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), b};
-    cu += suffix_lens_h[b];
-  }
-  s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
-  if (s != CW_OK) return s;
-  WriteParams p{};
-  p.k_new = k_new;
-  p.v_new = v_new;
-  p.k_pool = k_pool;
-  p.v_pool = v_pool;
-  p.k_scale = k_scale;
-  p.v_scale = v_scale;
-  p.block_table = block_table;
-  p.seqs = static_cast<const SeqInfo*>(workspace);
-  p.bt_stride = bt_stride;
-  p.num_seqs = num_seqs;
-  p.num_kv_heads = num_kv_heads;
-  p.total_tokens = static_cast<int32_t>(total);
-  hipError_t e = launch_write_pages(p, head_dim, page_size, kv_dtype == CW_KV_FP8_E4M3FN, stream);
-  if (e != hipSuccess) return hip_fail(e, "write_pages kernel launch");
-  return CW_OK;
+  return guarded([&]() -> cw_status_t {
+    cw_status_t s = check_shape(num_seqs, num_kv_heads, 1, head_dim, page_size);
+    if (s != CW_OK) return s;
+    s = check_dtype(kv_dtype, k_scale, v_scale);
+    if (s != CW_OK) return s;
+    if (num_pages < 0) return fail(CW_ERR_BAD_LENS, "num_pages = %d is negative", num_pages);
+    s = check_lens(prefix_lens_h, suffix_lens_h, num_seqs, bt_stride, page_size, num_kv_heads, 1,
+                   head_dim, true);
+    if (s != CW_OK) return s;
+    const int64_t total = sum_suffix(suffix_lens_h, num_seqs);
+    if (total == 0) return CW_OK;
+    if (!k_new || !v_new || !k_pool || !v_pool || !block_table)
+      return fail(CW_ERR_NULL, "k_new, v_new, k_pool, v_pool and block_table are required");
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool) ||
+        !aligned16(workspace))
+      return fail(CW_ERR_ALIGN, "tensor and workspace pointers must be 16-byte aligned");
+    const size_t need = cw_write_pages_workspace_bytes(num_seqs);
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(CW_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    std::vector<SeqInfo> seqs(num_seqs);
+    int64_t cu = 0;
+    for (int32_t b = 0; b < num_seqs; ++b) {
+      seqs[b] = SeqInfo{prefix_lens_h[b], suffix_lens_h[b], static_cast<int32_t>(cu), b};
+      cu += suffix_lens_h[b];
+    }
+    s = upload(seqs.data(), seqs.size() * sizeof(SeqInfo), workspace, stream);
+    if (s != CW_OK) return s;
+    WriteParams p{};
+    p.k_new = k_new;
+    p.v_new = v_new;
+    p.k_pool = k_pool;
+    p.v_pool = v_pool;
+    p.k_scale = k_scale;
+    p.v_scale = v_scale;
+    p.block_table = block_table;
+    p.seqs = static_cast<const SeqInfo*>(workspace);
+    p.bt_stride = bt_stride;
+    p.num_seqs = num_seqs;
+    p.num_kv_heads = num_kv_heads;
+    p.total_tokens = static_cast<int32_t>(total);
+    hipError_t e = launch_write_pages(p, head_dim, page_size, kv_dtype == CW_KV_FP8_E4M3FN, stream);
+    if (e != hipSuccess) return hip_fail(e, "write_pages kernel launch");
+    return CW_OK;
+  });
 }
 
 size_t cw_extend_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                  int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
                                  int32_t head_dim, int32_t page_size) {
-  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
-  if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
-                 head_dim, false) != CW_OK)
-    return 0;
-  if (num_seqs == 0) return 256;
-  return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim).total_bytes;
+  return guarded_value<size_t>(0, [&]() -> size_t {
+    if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+    if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                   head_dim, false) != CW_OK)
+      return 0;
+    if (num_seqs == 0) return 256;
+    return make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim).total_bytes;
+  });
 }
 
 cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_new,
@@ -887,10 +920,12 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
                                 int32_t head_dim, int32_t page_size, float softmax_scale,
                                 cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, hipStream_t stream) {
-  return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
-                     v_scale, block_table, bt_stride, num_pages, prefix_lens_h, suffix_lens_h,
-                     num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
-                     out, lse, workspace, workspace_bytes, stream, false, false);
+  return guarded([&]() -> cw_status_t {
+    return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
+                       v_scale, block_table, bt_stride, num_pages, prefix_lens_h, suffix_lens_h,
+                       num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
+                       out, lse, workspace, workspace_bytes, stream, false, false);
+  });
 }
 
 cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const void* v_new,
@@ -902,24 +937,28 @@ cw_status_t cw_write_extend_attention(const void* q, const void* k_new, const vo
                                       int32_t head_dim, int32_t page_size, float softmax_scale,
                                       cw_kv_dtype_t kv_dtype, void* out, float* lse,
                                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
-                     num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
-                     head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
-                     workspace_bytes, stream, false, true);
+  return guarded([&]() -> cw_status_t {
+    return extend_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
+                       num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
+                       head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
+                       workspace_bytes, stream, false, true);
+  });
 }
 
 size_t cw_step_workspace_bytes(const int32_t* prefix_lens_h, const int32_t* suffix_lens_h,
                                int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
                                int32_t head_dim, int32_t page_size, cw_kv_dtype_t kv_dtype) {
-  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
-  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
-  if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
-                 head_dim, false) != CW_OK)
-    return 0;
-  if (num_seqs == 0) return 256;
-  return make_step_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim,
-                        page_size, kv_dtype)
-      .total_bytes;
+  return guarded_value<size_t>(0, [&]() -> size_t {
+    if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+    if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
+    if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                   head_dim, false) != CW_OK)
+      return 0;
+    if (num_seqs == 0) return 256;
+    return make_step_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim,
+                          page_size, kv_dtype)
+        .total_bytes;
+  });
 }
 
 cw_status_t cw_step_attention(const void* q, const void* k_new, const void* v_new, void* k_pool,
@@ -930,25 +969,29 @@ cw_status_t cw_step_attention(const void* q, const void* k_new, const void* v_ne
                               int32_t head_dim, int32_t page_size, float softmax_scale,
                               cw_kv_dtype_t kv_dtype, void* out, float* lse, void* workspace,
                               size_t workspace_bytes, hipStream_t stream) {
-  return step_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
-                   num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
-                   head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
-                   workspace_bytes, stream);
+  return guarded([&]() -> cw_status_t {
+    return step_impl(q, k_new, v_new, k_pool, v_pool, k_scale, v_scale, block_table, bt_stride,
+                     num_pages, prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group,
+                     head_dim, page_size, softmax_scale, kv_dtype, out, lse, workspace,
+                     workspace_bytes, stream);
+  });
 }
 
 size_t cw_decode_workspace_bytes(const int32_t* prefix_lens_h, int32_t num_seqs,
                                  int32_t num_kv_heads, int32_t gqa_group, int32_t head_dim,
                                  int32_t page_size, cw_kv_dtype_t kv_dtype) {
-  if (num_seqs < 0) return 0;
-  if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
-  std::vector<int32_t> ones(num_seqs, 1);
-  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
-  if (check_lens(prefix_lens_h, ones.data(), num_seqs, 0, page_size, num_kv_heads, gqa_group,
-                 head_dim, false) != CW_OK)
-    return 0;
-  if (num_seqs == 0) return 256;
-  return make_decode_plan(prefix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype)
-      .total_bytes;
+  return guarded_value<size_t>(0, [&]() -> size_t {
+    if (num_seqs < 0) return 0;
+    if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return 0;
+    std::vector<int32_t> ones(num_seqs, 1);
+    if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return 0;
+    if (check_lens(prefix_lens_h, ones.data(), num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                   head_dim, false) != CW_OK)
+      return 0;
+    if (num_seqs == 0) return 256;
+    return make_decode_plan(prefix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype)
+        .total_bytes;
+  });
 }
 
 cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_new,
@@ -960,12 +1003,14 @@ cw_status_t cw_decode_attention(const void* q, const void* k_new, const void* v_
                                 int32_t page_size, float softmax_scale, cw_kv_dtype_t kv_dtype,
                                 void* out, float* lse, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream) {
-  if (num_seqs < 0) return fail(CW_ERR_BAD_LENS, "num_seqs = %d is negative", num_seqs);
-  std::vector<int32_t> ones(num_seqs, 1);
-  return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
-                     v_scale, block_table, bt_stride, num_pages, prefix_lens_h, ones.data(),
-                     num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
-                     out, lse, workspace, workspace_bytes, stream, true, false);
+  return guarded([&]() -> cw_status_t {
+    if (num_seqs < 0) return fail(CW_ERR_BAD_LENS, "num_seqs = %d is negative", num_seqs);
+    std::vector<int32_t> ones(num_seqs, 1);
+    return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
+                       v_scale, block_table, bt_stride, num_pages, prefix_lens_h, ones.data(),
+                       num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
+                       out, lse, workspace, workspace_bytes, stream, true, false);
+  });
 }
 
 cw_status_t cw_init(void) {
@@ -995,20 +1040,22 @@ cw_status_t cw_extend_attention_noalloc(const void* q, const void* k_new, const 
                                         int32_t page_size, float softmax_scale,
                                         cw_kv_dtype_t kv_dtype, void* out, float* lse,
                                         hipStream_t stream) {
-  DeviceState* st = nullptr;
-  const cw_status_t s = current_state(&st);
-  if (s != CW_OK) return s;
-  uint8_t* ws = nullptr;
-  {
-    std::lock_guard<std::mutex> g(st->staging_mu);
-    if (!st->ready || st->scratch == nullptr)
-      return fail(CW_ERR_INIT, "cw_init() has not been called on this device");
-    ws = st->scratch;
-  }
-  return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
-                     v_scale, block_table, bt_stride, num_pages, prefix_lens_h, suffix_lens_h,
-                     num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
-                     out, lse, ws, CW_NOALLOC_SCRATCH_BYTES, stream, false, false, true);
+  return guarded([&]() -> cw_status_t {
+    DeviceState* st = nullptr;
+    const cw_status_t s = current_state(&st);
+    if (s != CW_OK) return s;
+    uint8_t* ws = nullptr;
+    {
+      std::lock_guard<std::mutex> g(st->staging_mu);
+      if (!st->ready || st->scratch == nullptr)
+        return fail(CW_ERR_INIT, "cw_init() has not been called on this device");
+      ws = st->scratch;
+    }
+    return extend_impl(q, k_new, v_new, const_cast<void*>(k_pool), const_cast<void*>(v_pool), k_scale,
+                       v_scale, block_table, bt_stride, num_pages, prefix_lens_h, suffix_lens_h,
+                       num_seqs, num_kv_heads, gqa_group, head_dim, page_size, softmax_scale, kv_dtype,
+                       out, lse, ws, CW_NOALLOC_SCRATCH_BYTES, stream, false, false, true);
+  });
 }
 
 int64_t cw_pinned_allocations(void) { return g_pinned_allocs.load(); }
@@ -1041,21 +1088,23 @@ int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
                              int32_t head_dim, int32_t page_size, int32_t* items_out,
                              int64_t capacity) {
-  if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return -1;
-  if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
-                 head_dim, false) != CW_OK)
-    return -1;
-  ExtendPlan plan = make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim);
-  const int64_t n = static_cast<int64_t>(plan.items.size());
-  if (items_out) {
-    for (int64_t i = 0; i < std::min(n, capacity); ++i) {
-      const WorkItem& w = plan.items[i];
-      int32_t* o = items_out + 8 * i;
-      o[0] = w.seq; o[1] = w.kvh; o[2] = w.q_row0; o[3] = w.kv_begin;
-      o[4] = w.kv_end; o[5] = w.part; o[6] = w.rows; o[7] = 0;
+  return guarded_value<int64_t>(-1, [&]() -> int64_t {
+    if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return -1;
+    if (check_lens(prefix_lens_h, suffix_lens_h, num_seqs, 0, page_size, num_kv_heads, gqa_group,
+                   head_dim, false) != CW_OK)
+      return -1;
+    ExtendPlan plan = make_plan(prefix_lens_h, suffix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim);
+    const int64_t n = static_cast<int64_t>(plan.items.size());
+    if (items_out) {
+      for (int64_t i = 0; i < std::min(n, capacity); ++i) {
+        const WorkItem& w = plan.items[i];
+        int32_t* o = items_out + 8 * i;
+        o[0] = w.seq; o[1] = w.kvh; o[2] = w.q_row0; o[3] = w.kv_begin;
+        o[4] = w.kv_end; o[5] = w.part; o[6] = w.rows; o[7] = 0;
+      }
     }
-  }
-  return n;
+    return n;
+  });
 }
 
 const char* cw_status_string(cw_status_t status) {
