@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--plan-direct", type=int, default=0, choices=[0, 1],
                     help="1: kernels read the plan from the pinned staging slot; 0 (default): "
                          "it is copied to the workspace first")
+    ap.add_argument("--suffix-weight", type=int, default=None,
+                    help="split-K cost of a key tile past the cached prefix, percent of a prefix tile "
+                         "(default: the library's)")
     ap.add_argument("--separate-calls", action="store_true",
                     help="time a step as cw_kv_write_pages + cw_extend_attention (or "
                          "cw_decode_attention) instead of cw_step_attention")
@@ -612,6 +615,8 @@ def main():
     cwlib.set_tuning(cwlib._lib.CW_TUNE_EXTEND_KERNEL, args.extend_kernel)
     cwlib.set_tuning(cwlib._lib.CW_TUNE_DEAL_ROUNDS, args.deal_rounds)
     cwlib.set_tuning(cwlib._lib.CW_TUNE_PLAN_DIRECT, args.plan_direct)
+    if args.suffix_weight is not None:
+        cwlib.set_tuning(cwlib._lib.CW_TUNE_SUFFIX_WEIGHT, args.suffix_weight)
     res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,
                        cold_steps=args.cold_steps, power_s=args.power_seconds)
     ceil = measure_ceilings(power_s=args.power_seconds) if args.ceilings else None

@@ -297,6 +297,12 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           kernels read it from the staging slot over the
  *                           host link (no copy kernel; cw_extend_attention_noalloc
  *                           always copies).  Larger values act as 1.
+ *   CW_TUNE_SUFFIX_WEIGHT   split-K chunk boundaries divide a tile's keys into
+ *                           equal shares of cost, where a 64-key tile that
+ *                           reaches past the cached prefix costs value / 100
+ *                           of a prefix tile (1 .. 10000; default 125, the
+ *                           measured cost of the masked tiles; 100: equal
+ *                           key counts).
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {
   CW_TUNE_KV_CHUNK_TILES = 0,
@@ -304,6 +310,7 @@ typedef enum {
   CW_TUNE_EXTEND_KERNEL = 2,
   CW_TUNE_DEAL_ROUNDS = 3,
   CW_TUNE_PLAN_DIRECT = 4,
+  CW_TUNE_SUFFIX_WEIGHT = 5,
   CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
   CW_TUNE_RANGE_MAX_ = 2147483647
 } cw_tune_key_t;

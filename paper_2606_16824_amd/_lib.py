@@ -13,7 +13,7 @@ LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(
 (CW_OK, CW_ERR_NULL, CW_ERR_UNSUPPORTED, CW_ERR_BAD_LENS, CW_ERR_ALIGN, CW_ERR_WORKSPACE, CW_ERR_HIP,
  CW_ERR_ALIAS, CW_ERR_INIT) = range(9)
 CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1
-CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS, CW_TUNE_EXTEND_KERNEL, CW_TUNE_DEAL_ROUNDS, CW_TUNE_PLAN_DIRECT = 0, 1, 2, 3, 4
+CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS, CW_TUNE_EXTEND_KERNEL, CW_TUNE_DEAL_ROUNDS, CW_TUNE_PLAN_DIRECT, CW_TUNE_SUFFIX_WEIGHT = 0, 1, 2, 3, 4, 5
 CW_CEILING_LOW_ENTROPY, CW_CEILING_RANDOM = 0, 1
 
 _i32p = C.POINTER(C.c_int32)

@@ -1072,6 +1072,10 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
       return CW_OK;
     case CW_TUNE_DEAL_ROUNDS: g_tuning.deal_rounds = value; return CW_OK;
     case CW_TUNE_PLAN_DIRECT: g_tuning.plan_direct = value; return CW_OK;
+    case CW_TUNE_SUFFIX_WEIGHT:
+      if (value < 1 || value > 10000) return fail(CW_ERR_UNSUPPORTED, "suffix weight %d is not in 1 .. 10000", value);
+      g_tuning.suffix_weight = value;
+      return CW_OK;
     default: break;
   }
   return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));

@@ -131,8 +131,22 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
                                            static_cast<int32_t>(n_c), 0, 0});
         plan.n_parts += n_c;
       }
+      // chunk boundaries: equal shares of the tile's cost, a key tile that
+      // reaches past the cached prefix (masked, read from the new tokens)
+      // costing suffix_weight / 100 of a prefix tile (forced chunk sizes:
+      // equal key counts)
+      const int64_t n_pre = std::min<int64_t>(t.n_kt, prefix_lens[t.seq] / BLOCK_N);
+      const int64_t wgt = tuning.kv_chunk_tiles > 0 ? 100 : std::max(1, tuning.suffix_weight);
+      const int64_t total_cost = n_pre * 100 + (t.n_kt - n_pre) * wgt;
+      auto boundary = [&](int64_t c) -> int64_t {  // first key tile of chunk c
+        if (c >= n_c) return t.n_kt;
+        const int64_t goal = c * total_cost / n_c;
+        if (goal <= n_pre * 100) return std::min<int64_t>(t.n_kt, (goal + 99) / 100);
+        return std::min<int64_t>(t.n_kt, n_pre + (goal - n_pre * 100 + wgt - 1) / wgt);
+      };
       for (int64_t c = 0; c < n_c; ++c) {
-        const int64_t kt0 = c * t.n_kt / n_c, kt1 = (c + 1) * t.n_kt / n_c;
+        const int64_t kt0 = wgt == 100 ? c * t.n_kt / n_c : boundary(c);
+        const int64_t kt1 = wgt == 100 ? (c + 1) * t.n_kt / n_c : boundary(c + 1);
         WorkItem it{t.seq, t.kvh, t.q_row0, static_cast<int32_t>(kt0 * BLOCK_N),
                     static_cast<int32_t>(std::min<int64_t>(kt1 * BLOCK_N, t.kv_len)),
                     n_c > 1 ? static_cast<int32_t>(part0 + c) : -1, t.rows, 0};

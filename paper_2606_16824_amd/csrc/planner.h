@@ -16,6 +16,7 @@ struct Tuning {
   int32_t extend_kernel = 0;   // 0 = automatic, 1 = eight waves of 32 rows, 2 = four waves of 64 rows
   int32_t deal_rounds = 1;     // 1 = deal bundles of whole GPU rounds across XCDs, 0 = keep them on one
   int32_t plan_direct = 0;     // 1 = kernels read the plan from the pinned staging slot, 0 = copy it first
+  int32_t suffix_weight = 125; // split-K cost of a key tile past the prefix, in percent of a prefix tile
 };
 
 struct ExtendPlan {

@@ -165,6 +165,9 @@ def test_tuning_keys():
     assert lib().cw_set_tuning(L.CW_TUNE_DEAL_ROUNDS, 1) == L.CW_OK
     assert lib().cw_set_tuning(L.CW_TUNE_PLAN_DIRECT, 1) == L.CW_OK
     assert lib().cw_set_tuning(L.CW_TUNE_PLAN_DIRECT, 0) == L.CW_OK
+    assert lib().cw_set_tuning(L.CW_TUNE_SUFFIX_WEIGHT, 0) == L.CW_ERR_UNSUPPORTED
+    assert lib().cw_set_tuning(L.CW_TUNE_SUFFIX_WEIGHT, 10001) == L.CW_ERR_UNSUPPORTED
+    assert lib().cw_set_tuning(L.CW_TUNE_SUFFIX_WEIGHT, 125) == L.CW_OK
 
 
 def _swap(out=True, **over):

@@ -48,6 +48,22 @@ def test_turn_plan_fills_every_cu():
         assert len(set(items[x::8, 1].tolist())) == 1
 
 
+def test_split_boundaries_weight_suffix_tiles():
+    """The turn's tiles split into two chunks of equal cost, a key tile past the
+    prefix costing 1.25 prefix tiles: tile 15 (272 key tiles, 16 past the
+    prefix) splits after 138 tiles (13800 of 27600), not at 136."""
+    items = check_plan([16384], [1024], 8, 4)
+    t15 = items[(items[:, 1] == 0) & (items[:, 2] == 15 * BM)]
+    assert sorted(t15[:, 3:5].tolist()) == [[0, 138 * BN], [138 * BN, 17408]]
+    cwlib.set_tuning(5, 100)
+    try:
+        items = check_plan([16384], [1024], 8, 4)
+        t15 = items[(items[:, 1] == 0) & (items[:, 2] == 15 * BM)]
+        assert sorted(t15[:, 3:5].tolist()) == [[0, 136 * BN], [136 * BN, 17408]]
+    finally:
+        cwlib.set_tuning(5, 125)
+
+
 def test_long_plan_is_dealt_round_by_round():
     """Long: 8 kv heads x 256 tiles, unsplit.  Round r (workgroups 256r ..
     256r + 255, 32 per XCD) is all of kv head r, every XCD streaming it at once;
