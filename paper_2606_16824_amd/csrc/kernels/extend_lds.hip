@@ -361,9 +361,12 @@ void extend_lds_kernel(ExtendParams p) {
   // fp8 pool rows of the tile at j0 into registers (nothing when this wave's
   // rows hold no prefix key; rows of the page past the prefix end are loaded
   // but never stored)
-  auto load8 = [&](int j0, int pg, const uint8_t* pool, bool is_k) __attribute__((always_inline)) -> u32x4 {
+  // (`in_prefix`: the tile lies wholly in the cached prefix, so every row check
+  // below is known to pass)
+  auto load8 = [&](int j0, int pg, const uint8_t* pool, bool is_k,
+                   bool in_prefix) __attribute__((always_inline)) -> u32x4 {
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (j0 + wrow0 < lp) {
+    if (in_prefix || j0 + wrow0 < lp) {
       const auto rs = rsrc_at(pool + (size_t(pg) * hkv + kvh) * page_bytes);
       if constexpr (T::B8 == 16) {
         const u32x2 a = __builtin_amdgcn_raw_buffer_load_b64(rs, is_k ? koff8[0] : voff8[0], 0, 0);
@@ -378,15 +381,16 @@ void extend_lds_kernel(ExtendParams p) {
   };
   // ... dequantised to fp16 with the page's scale and stored at the swizzled
   // positions of their rows
-  auto store8 = [&](int j0, u32x4 v, uint8_t* dst, bool is_k, float scale) __attribute__((always_inline)) {
-    if (j0 + wrow0 >= lp) return;
+  auto store8 = [&](int j0, u32x4 v, uint8_t* dst, bool is_k, float scale,
+                    bool in_prefix) __attribute__((always_inline)) {
+    if (!in_prefix && j0 + wrow0 >= lp) return;
     const PageScale sc = page_scale(scale);
     if constexpr (T::B8 == 16) {
-      if (j0 + r8u[0] < lp)
+      if (in_prefix || j0 + r8u[0] < lp)
         *reinterpret_cast<u32x4*>(dst + wrow0 * T::RB + 16 * lane) = fp8x8_f16x8(v.x, v.y, sc);
-      if (j0 + r8u[1] < lp)
+      if (in_prefix || j0 + r8u[1] < lp)
         *reinterpret_cast<u32x4*>(dst + (wrow0 + 4) * T::RB + 16 * lane) = fp8x8_f16x8(v.z, v.w, sc);
-    } else if (j0 + r8 < lp) {
+    } else if (in_prefix || j0 + r8 < lp) {
       const int swz = is_k ? k_swz<D>(r8) : v_swz<D>(r8);
       *reinterpret_cast<u32x4*>(dst + r8 * T::RB + 16 * (q8 ^ swz)) = fp8x8_f16x8(v.x, v.y, sc);
     }
@@ -587,22 +591,22 @@ void extend_lds_kernel(ExtendParams p) {
       pg_v = pg1;
       if (n_tiles > 2) pg_raw = load_page(tile0(2));
     } else {
-      const u32x4 a = load8(tile0(0), pg0, k_pool, true), b = load8(tile0(0), pg0, v_pool, false);
+      const u32x4 a = load8(tile0(0), pg0, k_pool, true, false), b = load8(tile0(0), pg0, v_pool, false, false);
       u32x4 k1 = {0u, 0u, 0u, 0u};
-      if (n_tiles > 1) k1 = load8(tile0(1), pg1, k_pool, true);
+      if (n_tiles > 1) k1 = load8(tile0(1), pg1, k_pool, true, false);
       const float sk0 = load_scale(ks_s, tile0(0), pg0), sv0 = load_scale(vs_s, tile0(0), pg0);
       const float sk1 = n_tiles > 1 ? load_scale(ks_s, tile0(1), pg1) : 1.f;
       const int pg2 = n_tiles > 2 ? load_page(tile0(2)) : 0;
       __builtin_amdgcn_s_waitcnt(0);
-      store8(tile0(0), a, lds_k0, true, sk0);
-      store8(tile0(0), b, lds_v0, false, sv0);
-      if (n_tiles > 1) store8(tile0(1), k1, lds_k1, true, sk1);
+      store8(tile0(0), a, lds_k0, true, sk0, false);
+      store8(tile0(0), b, lds_v0, false, sv0, false);
+      if (n_tiles > 1) store8(tile0(1), k1, lds_k1, true, sk1, false);
       if (n_tiles > 2) {
-        k8 = load8(tile0(2), pg2, k_pool, true);
+        k8 = load8(tile0(2), pg2, k_pool, true, false);
         sk8 = load_scale(ks_s, tile0(2), pg2);
       }
       if (n_tiles > 1) {
-        v8 = load8(tile0(1), pg1, v_pool, false);
+        v8 = load8(tile0(1), pg1, v_pool, false, false);
         sv8 = load_scale(vs_s, tile0(1), pg1);
       }
       pg_v = pg2;
@@ -668,15 +672,16 @@ void extend_lds_kernel(ExtendParams p) {
   // codes and page scales of K_{j+3} and V_{j+2}
   auto stage8 = [&](int j, uint8_t* k_cur, uint8_t* v_nxt,
                     bool all_prefix) __attribute__((always_inline)) {
-    if (all_prefix || j + 2 < n_tiles) store8(tile0(j + 2), k8, k_cur, true, sk8);
-    if (all_prefix || j + 1 < n_tiles) store8(tile0(j + 1), v8, v_nxt, false, sv8);
+    // all_prefix: tiles j .. j+3 lie wholly in the cached prefix
+    if (all_prefix || j + 2 < n_tiles) store8(tile0(j + 2), k8, k_cur, true, sk8, all_prefix);
+    if (all_prefix || j + 1 < n_tiles) store8(tile0(j + 1), v8, v_nxt, false, sv8, all_prefix);
     const int pg3 = pg_raw;
     if (all_prefix || j + 3 < n_tiles) {
-      k8 = load8(tile0(j + 3), pg3, k_pool, true);
+      k8 = load8(tile0(j + 3), pg3, k_pool, true, all_prefix);
       sk8 = load_scale(ks_s, tile0(j + 3), pg3);
     }
     if (all_prefix || j + 2 < n_tiles) {
-      v8 = load8(tile0(j + 2), pg_v, v_pool, false);
+      v8 = load8(tile0(j + 2), pg_v, v_pool, false, all_prefix);
       sv8 = load_scale(vs_s, tile0(j + 2), pg_v);
     }
     pg_v = pg3;
