@@ -138,15 +138,20 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
       const int64_t n_pre = std::min<int64_t>(t.n_kt, prefix_lens[t.seq] / BLOCK_N);
       const int64_t wgt = tuning.kv_chunk_tiles > 0 ? 100 : std::max(1, tuning.suffix_weight);
       const int64_t total_cost = n_pre * 100 + (t.n_kt - n_pre) * wgt;
-      auto boundary = [&](int64_t c) -> int64_t {  // first key tile of chunk c
-        if (c >= n_c) return t.n_kt;
-        const int64_t goal = c * total_cost / n_c;
-        if (goal <= n_pre * 100) return std::min<int64_t>(t.n_kt, (goal + 99) / 100);
-        return std::min<int64_t>(t.n_kt, n_pre + (goal - n_pre * 100 + wgt - 1) / wgt);
-      };
+      // first key tile of each chunk, every chunk at least one tile long
+      std::vector<int64_t> first(static_cast<size_t>(n_c) + 1);
+      first[0] = 0;
+      first[n_c] = t.n_kt;
+      for (int64_t c = 1; c < n_c; ++c) {
+        int64_t b = c * t.n_kt / n_c;
+        if (wgt != 100) {
+          const int64_t goal = c * total_cost / n_c;
+          b = goal <= n_pre * 100 ? (goal + 99) / 100 : n_pre + (goal - n_pre * 100 + wgt - 1) / wgt;
+        }
+        first[c] = std::min(std::max(b, first[c - 1] + 1), t.n_kt - (n_c - c));
+      }
       for (int64_t c = 0; c < n_c; ++c) {
-        const int64_t kt0 = wgt == 100 ? c * t.n_kt / n_c : boundary(c);
-        const int64_t kt1 = wgt == 100 ? (c + 1) * t.n_kt / n_c : boundary(c + 1);
+        const int64_t kt0 = first[c], kt1 = first[c + 1];
         WorkItem it{t.seq, t.kvh, t.q_row0, static_cast<int32_t>(kt0 * BLOCK_N),
                     static_cast<int32_t>(std::min<int64_t>(kt1 * BLOCK_N, t.kv_len)),
                     n_c > 1 ? static_cast<int32_t>(part0 + c) : -1, t.rows, 0};

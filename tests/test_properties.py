@@ -32,7 +32,7 @@ def plan_case(draw):
     hkv = draw(st.sampled_from([1, 2, 3, 8]))
     g = draw(st.sampled_from([1, 2, 4, 8, 16]))
     chunk = draw(st.sampled_from([0, 0, 0, 1, 3, 7]))
-    weight = draw(st.sampled_from([100, 125, 250]))
+    weight = draw(st.sampled_from([1, 100, 125, 250, 10000]))
     deal = draw(st.sampled_from([0, 1]))
     target = draw(st.sampled_from([0, 0, 16, 1000]))
     return lp, ls, hkv, g, chunk, weight, deal, target
