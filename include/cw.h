@@ -31,7 +31,12 @@
  *
  * Supported: head_dim 64 or 128; page_size 16 or 64; 1 <= gqa_group <= 16;
  * softmax_scale finite and > 0.  In an fp8 pool only the cached prefix is fp8:
- * the suffix keys/values come from the bf16 k_new / v_new.
+ * the suffix keys/values come from the bf16 k_new / v_new.  With an fp8 pool
+ * the extend kernel computes in fp16 on the dequantised values, so every
+ * |code * scale| must lie below 65504 (scales below 146 for codes up to 448)
+ * and so must every k_new / v_new value (beyond it the result is inf or NaN;
+ * the scales are device data, which the calls do not inspect).  The decode
+ * kernel has no such limit.
  *
  * Ownership and ordering: the caller owns every buffer, including the
  * workspace.  Per device the library keeps a cache of device properties, a
