@@ -152,9 +152,10 @@ cw_status_t init_locked(DeviceState& st) {
       return hip_fail(e, "hipHostMalloc of the plan staging ring");
     }
     g_pinned_allocs.fetch_add(1);
-    // The event only tells the host that the upload kernel has finished reading
-    // the slot; it needs no system-scope fence (by default an L2 write-back and
-    // invalidate, which held the next kernel back by ~5 us and left it a cold L2).
+    // The event only tells the host that the kernels reading the slot (the upload
+    // kernel, or with direct plan reads the attention kernels) have finished; it
+    // needs no system-scope fence (by default an L2 write-back and invalidate,
+    // which held the next kernel back by ~5 us and left it a cold L2).
     e = hipHostGetDevicePointer(&s.dev, s.host, 0);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming | hipEventDisableSystemFence);
     if (e != hipSuccess) {
