@@ -201,16 +201,23 @@ def cpu_baseline(w, target_s: float):
         while dt < 0.5 * target_s and n < ls:
             n = min(ls, 2 * n)
             dt = run(n)
+        # the whole suffix fits well inside the target: repeat it (up to the
+        # target's half, at most 20 runs) and take the median run
+        times = [dt]
+        while n == ls and sum(times) < 0.5 * target_s and len(times) < 20:
+            times.append(run(n))
+        dt = float(np.median(times))
     finally:
         if limiter is not None:
             limiter.unregister()
     pairs = n * lp + n * (n + 1) // 2
     flops = 4.0 * s.head_dim * s.num_q_heads * pairs
+    runs = f", median of {len(times)} runs" if len(times) > 1 else ""
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
             "sample": f"first {n} of {ls} suffix tokens of sequence 0, all {s.num_q_heads} query heads "
-                      f"(float32 blocked oracle: page gather, sgemm, mask, softmax, P V), {dt:.1f} s",
+                      f"(float32 blocked oracle: page gather, sgemm, mask, softmax, P V), {dt:.1f} s{runs}",
             "tok_s": n / dt, "cpu_model": cpu_model(), "blas": blas_vendor(),
-            "wall_s": round(dt, 3)}
+            "wall_s": round(sum(times), 3), "runs": len(times)}
 
 
 def _smi_json(args):
