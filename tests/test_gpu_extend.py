@@ -96,6 +96,38 @@ def test_forced_split_matches_unsplit(chunk_tiles):
     assert_close(lse.cpu().double().numpy(), base_lse.cpu().double().numpy(), 2 ** -8, None, "lse")
 
 
+def _max_parts(items):
+    real = items[items[:, 0] >= 0]
+    _, counts = np.unique(real[:, :3], axis=0, return_counts=True)
+    return int(counts.max())
+
+
+def test_merge_of_few_partials():
+    """64 query tiles with a target of 128 workgroups: one to three key chunks per
+    tile, merged by the merge kernel's few-partials path (all loads of a row
+    issued at once); the default plan splits them into more chunks (its
+    many-partials path, slices merged through LDS).  Both against the oracle,
+    and against each other within 2 bf16 ulps."""
+    spec = cw.custom_spec([2000, 300], [1536, 512], num_kv_heads=2, gqa_group=4, head_dim=128,
+                          page_size=16, seed=79)
+    _case("few parts", spec)
+    w = cw.materialize(spec)
+    dw = to_gpu(w)
+    assert _max_parts(cwlib.plan_items(spec.prefix_lens, spec.suffix_lens, 2, 4, 128, 16)) > 4
+    cwlib.set_tuning(1, 128)
+    try:
+        assert _max_parts(cwlib.plan_items(spec.prefix_lens, spec.suffix_lens, 2, 4, 128, 16)) <= 4
+        out, lse = run_extend(dw)
+    finally:
+        cwlib.set_tuning(1, 0)
+    base, base_lse = run_extend(dw)
+    ref, _ = oracle.extend_attention_blocked(paged_inputs(w))
+    assert_close(as_f64(out), ref, BF16_MAX_ABS, BF16_MEAN_ABS, "few parts vs oracle")
+    assert_close(as_f64(base), ref, BF16_MAX_ABS, BF16_MEAN_ABS, "many parts vs oracle")
+    assert_within_bf16_ulps(as_f64(out), as_f64(base), 2, "few parts vs many parts")
+    assert_close(lse.cpu().double().numpy(), base_lse.cpu().double().numpy(), 2 ** -8, None, "lse")
+
+
 def test_page_permutation_bitwise():
     spec = cw.custom_spec([300, 45], [70, 130], num_kv_heads=2, gqa_group=4, head_dim=128,
                           page_size=16, seed=5)
