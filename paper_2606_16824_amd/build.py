@@ -2,7 +2,8 @@
 
 Usage: python -m paper_2606_16824_amd.build [--jobs N] [--sanitize]
 Every .hip / .cpp under csrc/ is compiled to an object in _build/ (in
-parallel), then linked into paper_2606_16824_amd/libcw.so.
+parallel), then linked into paper_2606_16824_amd/libcw.so; the C programs under
+tests/native/ are then compiled against it (build_native_tests).
 
 --sanitize builds the host side of every source with AddressSanitizer and
 UndefinedBehaviorSanitizer (device code is built as usual) into
@@ -100,6 +101,30 @@ def build(jobs: int = 8, verbose: bool = False, sanitize: bool = False) -> str:
     return lib_path
 
 
+NATIVE = os.path.join(ROOT, "tests", "native")
+
+
+def build_native_tests() -> list:
+    """Compiles the C programs under tests/native/ (host code that drives the C
+    ABI with no Python) against libcw.so into tests/native/<name>.bin."""
+    cc = shutil.which("gcc") or "gcc"
+    out = []
+    for f in sorted(os.listdir(NATIVE)) if os.path.isdir(NATIVE) else []:
+        if not f.endswith(".c"):
+            continue
+        exe = os.path.join(NATIVE, f[:-2] + ".bin")
+        cmd = [cc, "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+               "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+               os.path.join(NATIVE, f), "-L", PKG, "-lcw", "-L", "/opt/rocm/lib", "-lamdhip64", "-lm",
+               "-Wl,-rpath,$ORIGIN/../../paper_2606_16824_amd", "-Wl,-rpath,/opt/rocm/lib", "-o", exe]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            print(" ".join(cmd), "\n", r.stdout, r.stderr, file=sys.stderr)
+            raise RuntimeError(f"build of {f} failed")
+        out.append(exe)
+    return out
+
+
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=8)
@@ -108,3 +133,5 @@ if __name__ == "__main__":
                     help="host-side ASan + UBSan build into _build/sanitize/libcw.so")
     a = ap.parse_args()
     print(build(a.jobs, a.verbose, a.sanitize))
+    if not a.sanitize:
+        print("\n".join(build_native_tests()))

@@ -328,3 +328,23 @@ def test_plan_larger_than_a_staging_slot_is_rejected_before_any_gpu_work():
                                    16, 0.088, 0, FAKE + 6 * gb, None, FAKE + 7 * gb, 1 << 29, None)
     assert st == L.CW_ERR_UNSUPPORTED
     assert "staging slot" in lib().cw_last_error_message().decode()
+
+
+@pytest.mark.parametrize("header", ["cw.h", "cw_policy.h", "cw_ceiling.h"])
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_header_compiles_alone(header, lang, tmp_path):
+    """Each public header compiles on its own as C11 and as C++17 (plain host
+    compilers, no HIP compiler), so a C caller can use the boundary directly."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc" if lang == "c" else "g++")
+    if cc is None:
+        pytest.skip("no host compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = tmp_path / "use.c"
+    src.write_text(f'#include "{header}"\nint main(void) {{ return 0; }}\n')
+    std = "-std=c11" if lang == "c" else "-std=c++17"
+    r = subprocess.run([cc, std, "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I",
+                        os.path.join(root, "include"), "-I", "/opt/rocm/include", "-fsyntax-only",
+                        "-x", lang, str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
