@@ -48,6 +48,8 @@ class Config:
     sched: str = "prefix"      # "fcfs" | "prefix"
     evict: str = "predictive"  # "lru" | "predictive" | "belady"
     n_rebuild: int = 3
+    host_blocks: int = 0       # offload: blocks of the host pool evicted blocks go to (0: none)
+    swap_s_per_block: float = 0.0  # engine time of one block's transfer either way
 
 
 @dataclass
@@ -61,6 +63,8 @@ class Result:
     recomputed_tokens: int = 0
     prefilled_tokens: int = 0
     heap_rebuilds: int = 0
+    swapped_out_blocks: int = 0
+    swapped_in_blocks: int = 0
     dispatch: List[int] = field(default_factory=list)
 
 
@@ -207,7 +211,19 @@ def simulate(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Seq
 #    that value.  So every sharer's private blocks (positions after it) leave
 #    first: resident blocks stay a leading run of every context.  The
 #    dispatching session's resident run is never a candidate.
-# With no groups this is exactly simulate() above (pinned by a test).
+# Offload (the paper's Sec. 6.4 configuration: evicted blocks go to CPU memory
+# and are swapped back when the session resumes), with host_blocks > 0:
+#  * an evicted block goes to the host pool while it has a free block (a swap
+#    out); the host-held blocks of a context follow its resident run.  When the
+#    pool is full the block is dropped instead, and with it the owner's host-held
+#    blocks (past it, so no longer part of a leading run); a dropped shared block
+#    also drops the sharers' host-held private blocks.
+#  * a request first swaps its host-held blocks back in (shared ones, then its
+#    private ones once the shared run is complete), after the evictions that make
+#    room for them; they count as found (no prefill).  Every swap, out or in,
+#    costs swap_s_per_block of engine time.
+# With no groups this is exactly simulate() above (pinned by a test), and with a
+# host pool of 0 blocks exactly the model without offload.
 # ---------------------------------------------------------------------------
 
 @dataclass
@@ -216,6 +232,8 @@ class Dispatch:
     cached_tokens: int     # prompt tokens whose K/V are resident (attention prefix)
     new_tokens: int        # tokens prefilled (context + input - cached)
     blocks: int            # blocks of the request (context + input + output)
+    swapped_in: int = 0    # of them, blocks brought back from the host pool
+    swapped_out: int = 0   # blocks of other sessions moved to the host pool to make room
 
 
 def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Sequence[float]],
@@ -236,6 +254,8 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
     attached = [False] * n
     res_private = [0] * n               # resident private blocks (positions G .. G + r - 1)
     res_shared = [0] * len(shared_tokens)  # resident shared blocks of each group (leading)
+    host_private = [0] * n              # host-held private blocks, following the resident ones
+    host_shared = [0] * len(shared_tokens)
     for i, s in enumerate(sessions):
         if not s.turns:
             state[i], done_at[i], prio[i] = "done", s.start, INF
@@ -320,23 +340,52 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
                     r.faults += 1
                 a = d - k
                 free = cfg.M - sum(res_private) - sum(res_shared)
+                swapped_out = 0
                 while free < a:
                     kind, x = victim(i)
+                    to_host = sum(host_private) + sum(host_shared) < cfg.host_blocks
                     if kind == "p":
                         res_private[x] -= 1
+                        if to_host:
+                            host_private[x] += 1
+                        else:
+                            host_private[x] = 0
                     else:
                         res_shared[x] -= 1
                         # the key order keeps every sharer's private blocks out first
                         assert all(res_private[j] == 0 for j in range(n) if sessions[j].group == x)
+                        if to_host:
+                            host_shared[x] += 1
+                        else:
+                            host_shared[x] = 0
+                            for j in range(n):
+                                if sessions[j].group == x:
+                                    host_private[j] = 0
+                    swapped_out += 1 if to_host else 0
                     free += 1
                     r.evicted_blocks += 1
+                # swap the host-held run back in, in position order
+                swapped_in = 0
+                g = sessions[i].group
+                if g >= 0 and res_shared[g] < G[i]:
+                    take = host_shared[g]
+                    host_shared[g] -= take
+                    res_shared[g] += take
+                    swapped_in += take
+                if g < 0 or res_shared[g] >= G[i]:
+                    take = host_private[i]
+                    host_private[i] = 0
+                    res_private[i] += take
+                    swapped_in += take
+                r.swapped_out_blocks += swapped_out
+                r.swapped_in_blocks += swapped_in
                 k = resident_run(i)
                 known = max(ctx[i], G[i] * B)
                 hit = min(k * B, known)
                 recompute = max(0, ctx[i] - hit)
                 r.recomputed_tokens += recompute
                 r.prefilled_tokens += ctx[i] + tr.in_tokens - hit
-                log.append(Dispatch(i, hit, ctx[i] + tr.in_tokens - hit, d))
+                log.append(Dispatch(i, hit, ctx[i] + tr.in_tokens - hit, d, swapped_in, swapped_out))
                 g = sessions[i].group
                 if g >= 0:
                     res_shared[g] = max(res_shared[g], min(d, G[i]))
@@ -345,7 +394,8 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
                 state[i] = "running"
                 running = i
                 run_end = t + (cfg.prefill_s_per_token * (ctx[i] + tr.in_tokens - hit)
-                               + cfg.decode_s_per_token * tr.out_tokens)
+                               + cfg.decode_s_per_token * tr.out_tokens
+                               + cfg.swap_s_per_block * (swapped_in + swapped_out))
                 r.dispatch.append(i)
                 continue
         nexts = [arrival[i] for i in range(n) if state[i] == "wait"]

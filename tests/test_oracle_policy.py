@@ -235,3 +235,100 @@ def test_block_model_with_groups_accounting(seed, sched, evict):
     # the same sessions without the groups prefill at least as much
     r0, _ = cp.simulate_blocks(cfg, _to_oracle_sessions(tr.sessions), tr.history)
     assert r0.prefilled_tokens >= r.prefilled_tokens
+
+
+# ---- offload (evicted blocks to a host pool, swapped back when the session resumes)
+
+def test_offload_worked_example():
+    """M = 4 blocks of 4 tokens, prefill 1 s/token, swaps 1 s/block, FCFS + LRU.
+    A (t=0): 8 tokens, tool 10 s, then 4.  B (t=1): 8 tokens, tool 20 s, then 4.
+    A runs 0-8, B 8-16.  A's second turn (t=18) needs a third block: B's tail goes
+    to the host (1 swap out), A prefills its 4 new tokens: ends 18 + 4 + 1 = 23.
+    B's second turn (t=36) needs 3 blocks with 1 resident: A's two tail blocks go
+    out (2 swaps), B's host block comes back (1 swap in), B prefills 4 tokens:
+    ends 36 + 4 + 3 = 43.  Without the host pool B recomputes its dropped 4 tokens
+    instead: ends 36 + 8 = 44."""
+    sess = [cp.SessionSpec(0.0, [cp.Turn(8, 0, 0, 10.0), cp.Turn(4, 0)]),
+            cp.SessionSpec(1.0, [cp.Turn(8, 0, 0, 20.0), cp.Turn(4, 0)])]
+    kw = dict(M=4, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict="lru",
+              swap_s_per_block=1.0)
+    r, log = cp.simulate_blocks(cp.Config(host_blocks=8, **kw), sess, [[1.0]])
+    assert r.dispatch == [0, 1, 0, 1]
+    assert [(d.cached_tokens, d.new_tokens, d.blocks, d.swapped_in, d.swapped_out) for d in log] == \
+        [(0, 8, 2, 0, 0), (0, 8, 2, 0, 0), (8, 4, 3, 0, 1), (8, 4, 3, 1, 2)]
+    assert (r.evicted_blocks, r.swapped_out_blocks, r.swapped_in_blocks, r.recomputed_tokens,
+            r.prefilled_tokens, r.makespan_s) == (3, 3, 1, 0, 24, 43.0)
+    r0, log0 = cp.simulate_blocks(cp.Config(host_blocks=0, **kw), sess, [[1.0]])
+    assert [(d.cached_tokens, d.new_tokens) for d in log0] == [(0, 8), (0, 8), (8, 4), (4, 8)]
+    assert (r0.evicted_blocks, r0.swapped_out_blocks, r0.swapped_in_blocks, r0.recomputed_tokens,
+            r0.prefilled_tokens, r0.makespan_s) == (3, 0, 0, 4, 28, 44.0)
+
+
+def test_offload_full_host_pool_drops_the_tail_worked_example():
+    """A host pool of 1 block: an evicted block goes out while the pool has room;
+    the next finds it full and is dropped together with the host-held block behind
+    it, which frees the pool again.  A (t=0): 12 tokens (3 blocks), tool 50 s, then
+    4.  B (t=1, runs 12-25): 12 tokens in a 4-block node: A's tail (position 2)
+    goes out, A's position 1 is dropped and takes position 2 with it (1 swap out).
+    A's second turn (t=62) keeps position 0 (4 tokens found) and needs 3 more
+    blocks: B's position 2 goes out, position 1 is dropped (freeing the pool),
+    position 0 goes out (2 swaps out); A recomputes 8 context tokens."""
+    sess = [cp.SessionSpec(0.0, [cp.Turn(12, 0, 0, 50.0), cp.Turn(4, 0)]),
+            cp.SessionSpec(1.0, [cp.Turn(12, 0)])]
+    cfg = cp.Config(M=4, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict="lru",
+                    host_blocks=1, swap_s_per_block=1.0)
+    r, log = cp.simulate_blocks(cfg, sess, [[1.0]])
+    assert r.dispatch == [0, 1, 0]
+    assert [(d.cached_tokens, d.new_tokens, d.swapped_in, d.swapped_out) for d in log] == \
+        [(0, 12, 0, 0), (0, 12, 0, 1), (4, 12, 0, 2)]
+    assert (r.evicted_blocks, r.swapped_out_blocks, r.swapped_in_blocks, r.recomputed_tokens) == (5, 3, 0, 8)
+    assert r.makespan_s == 62.0 + 12 + 2
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_free_unbounded_offload_is_a_node_that_never_evicts(seed):
+    """FCFS with an unbounded host pool and free swaps gives the dispatch order,
+    times and prefill of FCFS on a node large enough never to evict: with FCFS
+    the order depends only on times, and no request recomputes or pays a swap."""
+    import cw_workloads as cw
+    tr = cw.agent_sessions(num_sessions=10, seed=2200 + seed, max_turns=8, shared_groups=2,
+                           shared_prefix_tokens=512)
+    sess = _to_oracle_sessions(tr.sessions, tr.groups)
+    kw = dict(block_tokens=tr.block_tokens, prefill_s_per_token=1e-4, decode_s_per_token=1e-3,
+              sched="fcfs", evict="lru")
+    off, _ = cp.simulate_blocks(cp.Config(M=tr.capacity_blocks, host_blocks=10 ** 9, **kw), sess,
+                                tr.history, shared_tokens=tr.shared_tokens)
+    big, _ = cp.simulate_blocks(cp.Config(M=10 ** 9, **kw), sess, tr.history, shared_tokens=tr.shared_tokens)
+    assert off.evicted_blocks > 0 and big.evicted_blocks == 0
+    assert off.dispatch == big.dispatch
+    assert off.recomputed_tokens == 0 and off.prefilled_tokens == big.prefilled_tokens
+    assert off.makespan_s == pytest.approx(big.makespan_s, rel=1e-12)
+    assert 0 < off.swapped_in_blocks <= off.swapped_out_blocks == off.evicted_blocks
+
+
+@pytest.mark.parametrize("seed", range(2))
+@pytest.mark.parametrize("sched,evict", list(itertools.product(("fcfs", "prefix"),
+                                                               ("lru", "predictive", "belady"))))
+def test_offload_accounting(seed, sched, evict):
+    """With groups: a host pool of 0 is the model without offload; with a bounded
+    pool every block swapped in was swapped out before, and the log's counts add
+    up to the totals; an unbounded pool never recomputes."""
+    import cw_workloads as cw
+    tr = cw.agent_sessions(num_sessions=10, seed=2300 + seed, max_turns=8, shared_groups=2,
+                           shared_prefix_tokens=1024)
+    sess = _to_oracle_sessions(tr.sessions, tr.groups)
+    kw = dict(M=tr.capacity_blocks, block_tokens=tr.block_tokens, prefill_s_per_token=1e-5,
+              decode_s_per_token=1e-3, sched=sched, evict=evict, n_rebuild=3, swap_s_per_block=1e-3)
+    base, blog = cp.simulate_blocks(cp.Config(**kw), sess, tr.history, shared_tokens=tr.shared_tokens)
+    zero, zlog = cp.simulate_blocks(cp.Config(host_blocks=0, **kw), sess, tr.history,
+                                    shared_tokens=tr.shared_tokens)
+    assert zero == base and zlog == blog
+    for host in (40, 10 ** 9):
+        r, log = cp.simulate_blocks(cp.Config(host_blocks=host, **kw), sess, tr.history,
+                                    shared_tokens=tr.shared_tokens)
+        assert r.swapped_in_blocks <= r.swapped_out_blocks <= r.evicted_blocks
+        assert sum(d.swapped_in for d in log) == r.swapped_in_blocks
+        assert sum(d.swapped_out for d in log) == r.swapped_out_blocks
+        assert sum(d.new_tokens for d in log) == r.prefilled_tokens
+        if host == 10 ** 9:
+            assert r.recomputed_tokens == 0 and r.swapped_out_blocks == r.evicted_blocks
