@@ -29,7 +29,13 @@
  *    become unreferenced and recomputed for every session each rebuild_every
  *    engine iterations (dispatches); Belady = largest true time to next use.
  *  - A request takes prefill_s_per_token x (context tokens not resident +
- *    in_tokens) + decode_s_per_token x out_tokens seconds.
+ *    in_tokens) + decode_s_per_token x out_tokens seconds (+ swap_s_per_block
+ *    per block swapped out or in for it, with offload).
+ *  - Offload (host_blocks > 0; CacheWise Sec. 6.4): an evicted block is copied
+ *    to the host pool while it has a free block, else dropped together with the
+ *    owner's host-held blocks past it (and, for a shared block, the sharers'
+ *    host-held private blocks); a request first swaps its context's host-held
+ *    blocks back in, after the evictions that make room for them.
  *  - The predictor estimates E[tau | tau > e] of a tool type as the mean of
  *    (x - e) over its history samples x > e, and e when no sample exceeds e.
  *
@@ -71,6 +77,8 @@ typedef struct {
   int32_t sched;               /* cw_sched_policy_t */
   int32_t evict;               /* cw_evict_policy_t */
   int32_t rebuild_every;       /* >= 1; predictive eviction only */
+  int32_t host_blocks;         /* 0 .. 2^26: offload host pool (0: evicted blocks are dropped) */
+  double swap_s_per_block;     /* >= 0: engine time of one block swapped out or in */
 } cw_sim_config_t;
 
 /* Sessions and their turns, flattened (host arrays, read during the call):
@@ -103,6 +111,8 @@ typedef struct {
   int64_t recomputed_tokens;   /* context tokens prefilled again because their blocks were evicted */
   int64_t prefilled_tokens;    /* all prefilled tokens (recomputed + new input) */
   int64_t heap_rebuilds;
+  int64_t swapped_out_blocks;  /* evicted blocks copied to the host pool */
+  int64_t swapped_in_blocks;   /* blocks brought back from it */
 } cw_sim_result_t;
 
 /* Runs the simulation.  `dispatch` (optional, NULL to skip) receives the
@@ -133,6 +143,8 @@ typedef struct {
   int32_t* tables;         /* [table_capacity] */
   int64_t table_capacity;
   int64_t written;         /* out */
+  int32_t* swapped_in;     /* [capacity] or NULL: blocks of the request swapped in */
+  int32_t* swapped_out;    /* [capacity] or NULL: blocks of others swapped out for it */
 } cw_sim_log_t;
 
 /* cw_policy_simulate with the per-dispatch log instead of the dispatch order. */
@@ -161,7 +173,9 @@ cw_status_t cw_policy_simulate_log(const cw_sim_config_t* config, const cw_sim_t
  * they hold its K/V.  Limits: capacity_blocks <= 2^26, session and group ids
  * below 2^24 (ids index dense tables: use small consecutive integers), token
  * counts of a request <= 2^40.  Errors: CW_ERR_NULL, CW_ERR_BAD_LENS (unknown or
- * running session, negative or oversized counts, NaN values),
+ * running session, negative or oversized counts, NaN values, a request whose
+ * blocks do not cover its group's shared blocks and the private blocks its
+ * session already holds: a context only grows),
  * CW_ERR_UNSUPPORTED (sizes beyond the limits, or host memory exhausted; after
  * the latter from cw_bm_admit, cw_bm_release or cw_bm_rebuild the manager's
  * state is undefined and it should only be destroyed).  No call throws. */
@@ -178,6 +192,41 @@ cw_status_t cw_bm_release(cw_block_manager_t* bm, int32_t session, double value)
 cw_status_t cw_bm_rebuild(cw_block_manager_t* bm, const int32_t* sessions, const double* values,
                           int32_t n);
 cw_status_t cw_bm_stats(cw_block_manager_t* bm, int64_t* free_blocks, int64_t* referenced_blocks);
+
+/* The block manager with offload (CacheWise Sec. 6.4): evicted blocks move to a
+ * host pool of host_blocks blocks (1 .. 2^26) while it has room, else they are
+ * dropped with the owner's host-held blocks past them (for a shared block, also
+ * the sharers' host-held private blocks), and a request's host-held context
+ * blocks are swapped back in when it is admitted.  The manager decides; the
+ * caller moves the data (cw_kv_swap_out / cw_kv_swap_in of cw.h).  Admissions of
+ * such a manager go through cw_bm_admit_swaps, which also returns the swaps:
+ * out_device[i] -> out_host[i] (copy device page to host block) for the blocks
+ * evicted to the host pool, then in_host[i] -> in_device[i] for the blocks of
+ * the request brought back.  Apply every admission's swaps in admission order,
+ * its swap-outs before its swap-ins (a swap-in may fill a page just swapped out,
+ * and a later admission may reuse a host block just swapped in), all before the
+ * step that reads the pages.  The four arrays hold `capacity` entries each;
+ * capacity must be at least the request's blocks (both counts are bounded by
+ * it), else CW_ERR_WORKSPACE with nothing changed.  cw_bm_admit on such a
+ * manager is CW_ERR_UNSUPPORTED (it would lose the swap lists).
+ * cw_bm_host_stats reports the free and held host blocks. */
+typedef struct {
+  int32_t* out_device;  /* [capacity] */
+  int32_t* out_host;    /* [capacity] */
+  int32_t* in_host;     /* [capacity] */
+  int32_t* in_device;   /* [capacity] */
+  int32_t capacity;
+  int32_t n_out;        /* out: swap-outs written */
+  int32_t n_in;         /* out: swap-ins written */
+} cw_bm_swaps_t;
+cw_status_t cw_bm_create_with_host_pool(int32_t capacity_blocks, int32_t block_tokens,
+                                        int32_t host_blocks, cw_block_manager_t** out);
+cw_status_t cw_bm_admit_swaps(cw_block_manager_t* bm, int32_t session, int64_t context_tokens,
+                              int64_t input_tokens, int64_t output_tokens, int32_t* table,
+                              int32_t table_capacity, int32_t* blocks, int64_t* cached_tokens,
+                              int64_t* evicted_blocks, cw_bm_swaps_t* swaps);
+cw_status_t cw_bm_host_stats(cw_block_manager_t* bm, int64_t* free_host_blocks,
+                             int64_t* held_host_blocks);
 
 /* The predictor alone: the expected remaining time of a tool call of type
  * `tool` that has run for elapsed_s seconds, from the trace's history samples

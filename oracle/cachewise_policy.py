@@ -217,7 +217,9 @@ def simulate(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Seq
 #    out); the host-held blocks of a context follow its resident run.  When the
 #    pool is full the block is dropped instead, and with it the owner's host-held
 #    blocks (past it, so no longer part of a leading run); a dropped shared block
-#    also drops the sharers' host-held private blocks.
+#    also drops the sharers' host-held private blocks.  A copy to the host pool
+#    that a drop in the same admission discards is not made (its data would
+#    never be read) and is not counted.
 #  * a request first swaps its host-held blocks back in (shared ones, then its
 #    private ones once the shared run is complete), after the evictions that make
 #    room for them; they count as found (no prefill).  Every swap, out or in,
@@ -341,6 +343,9 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
                 a = d - k
                 free = cfg.M - sum(res_private) - sum(res_shared)
                 swapped_out = 0
+                # copies to the host pool made by this admission and still held
+                new_private = [0] * n
+                new_shared = [0] * len(shared_tokens)
                 while free < a:
                     kind, x = victim(i)
                     to_host = sum(host_private) + sum(host_shared) < cfg.host_blocks
@@ -348,19 +353,27 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
                         res_private[x] -= 1
                         if to_host:
                             host_private[x] += 1
+                            new_private[x] += 1
                         else:
                             host_private[x] = 0
+                            swapped_out -= new_private[x]
+                            new_private[x] = 0
                     else:
                         res_shared[x] -= 1
                         # the key order keeps every sharer's private blocks out first
                         assert all(res_private[j] == 0 for j in range(n) if sessions[j].group == x)
                         if to_host:
                             host_shared[x] += 1
+                            new_shared[x] += 1
                         else:
                             host_shared[x] = 0
+                            swapped_out -= new_shared[x]
+                            new_shared[x] = 0
                             for j in range(n):
                                 if sessions[j].group == x:
                                     host_private[j] = 0
+                                    swapped_out -= new_private[j]
+                                    new_private[j] = 0
                     swapped_out += 1 if to_host else 0
                     free += 1
                     r.evicted_blocks += 1

@@ -74,6 +74,10 @@ SIGNATURES = {
     "cw_bm_release": (C.c_int, [_vp, _i32, C.c_double]),
     "cw_bm_rebuild": (C.c_int, [_vp, _vp, _vp, _i32]),
     "cw_bm_stats": (C.c_int, [_vp, _vp, _vp]),
+    "cw_bm_create_with_host_pool": (C.c_int, [_i32, _i32, _i32, _vp]),
+    "cw_bm_admit_swaps": (C.c_int, [_vp, _i32, C.c_int64, C.c_int64, C.c_int64, _vp, _i32, _vp, _vp, _vp,
+                                    _vp]),
+    "cw_bm_host_stats": (C.c_int, [_vp, _vp, _vp]),
 }
 
 _lib = None

@@ -5,10 +5,13 @@
 
 namespace cw {
 
-BlockManager::BlockManager(int32_t capacity_blocks, int32_t block_tokens)
-    : capacity_(capacity_blocks), block_tokens_(block_tokens), blocks_(capacity_blocks) {
+BlockManager::BlockManager(int32_t capacity_blocks, int32_t block_tokens, int32_t host_blocks)
+    : capacity_(capacity_blocks), block_tokens_(block_tokens), blocks_(capacity_blocks),
+      host_capacity_(host_blocks), host_out_(host_blocks, -1) {
   free_.reserve(capacity_blocks);
   for (int32_t b = capacity_blocks - 1; b >= 0; --b) free_.push_back(b);  // hands out 0, 1, 2, ...
+  host_free_.reserve(host_blocks);
+  for (int32_t b = host_blocks - 1; b >= 0; --b) host_free_.push_back(b);
 }
 
 void BlockManager::add_session(int32_t s, int32_t group, int32_t shared_tokens) {
@@ -76,6 +79,51 @@ std::vector<int32_t>& BlockManager::run_of(int32_t owner) {
   return owner >= 0 ? sess_[owner].priv : groups_[-1 - owner].blocks;
 }
 
+std::vector<int32_t>& BlockManager::host_run_of(int32_t owner) {
+  return owner >= 0 ? sess_[owner].hpriv : groups_[-1 - owner].hblocks;
+}
+
+// Frees the owner's host-held run (and, for a group, its sharers' host-held
+// private runs): they no longer follow a leading run.  Copies into them that
+// the current admission listed are cancelled: their data is never read.
+void BlockManager::drop_host_run(int32_t owner) {
+  auto release = [&](std::vector<int32_t>& run) {
+    for (auto it = run.rbegin(); it != run.rend(); ++it) {
+      const int32_t hb = *it;
+      if (host_out_[hb] >= 0) {
+        swap_out_[host_out_[hb]].host = -1;
+        host_out_[hb] = -1;
+      }
+      host_free_.push_back(hb);
+    }
+    run.clear();
+  };
+  release(host_run_of(owner));
+  if (owner < 0)
+    for (int32_t m : groups_[-1 - owner].members) release(sess_[m].hpriv);
+}
+
+// Moves the whole host-held run back to device blocks (lowest position first),
+// referenced by the admitting request, recording the swaps.
+void BlockManager::swap_in_run(std::vector<int32_t>& host_run, std::vector<int32_t>& run, Kind kind,
+                               int32_t owner, int32_t* pos) {
+  while (!host_run.empty()) {
+    const int32_t hb = host_run.back();
+    host_run.pop_back();
+    const int32_t b = free_.back();
+    free_.pop_back();
+    Block& bl = blocks_[b];
+    bl.kind = kind;
+    bl.owner = owner;
+    bl.pos = (*pos)++;
+    bl.ref = 1;
+    ++referenced_;
+    run.push_back(b);
+    host_free_.push_back(hb);
+    swap_in_.push_back(Swap{b, hb});
+  }
+}
+
 // (Re)enters the run's tail block into the heap; older entries of the run are
 // stale from now on.  A referenced run has no entry.
 void BlockManager::push(int32_t owner) {
@@ -112,6 +160,17 @@ bool BlockManager::evict_one() {
     blocks_[b].kind = kFree;
     blocks_[b].owner = -1;
     free_.push_back(b);
+    if (host_capacity_ > 0) {
+      if (!host_free_.empty()) {  // to the host pool: the block now leads the host-held run
+        const int32_t hb = host_free_.back();
+        host_free_.pop_back();
+        host_run_of(e.owner).push_back(hb);
+        host_out_[hb] = static_cast<int32_t>(swap_out_.size());
+        swap_out_.push_back(Swap{b, hb});
+      } else {
+        drop_host_run(e.owner);
+      }
+    }
     push(e.owner);  // the run's new tail
     return true;
   }
@@ -132,11 +191,31 @@ bool BlockManager::admit(int32_t s, int64_t context_tokens, int64_t input_tokens
     return false;
   }
   int64_t evicted = 0;
+  swap_out_.clear();
+  swap_in_.clear();
   while (static_cast<int64_t>(free_.size()) < a) {
     if (!evict_one()) return false;  // unreachable: the heap holds every evictable block
     ++evicted;
   }
-  for (int64_t p = k; p < d; ++p) {
+  // the copies that still matter (each host block written at most once)
+  size_t kept = 0;
+  for (const Swap& w : swap_out_) {
+    if (w.host < 0) continue;
+    host_out_[w.host] = -1;
+    swap_out_[kept++] = w;
+  }
+  swap_out_.resize(kept);
+  // the host-held run comes back first, in position order
+  int32_t pos = k;
+  if (host_capacity_ > 0) {
+    if (x.group >= 0 && static_cast<int32_t>(groups_[x.group].blocks.size()) < x.shared) {
+      Group& g = groups_[x.group];
+      swap_in_run(g.hblocks, g.blocks, kShared, x.group, &pos);
+    }
+    if (x.group < 0 || static_cast<int32_t>(groups_[x.group].blocks.size()) >= x.shared)
+      swap_in_run(x.hpriv, x.priv, kPrivate, s, &pos);
+  }
+  for (int64_t p = pos; p < d; ++p) {
     const int32_t b = free_.back();
     free_.pop_back();
     Block& bl = blocks_[b];
@@ -159,8 +238,10 @@ bool BlockManager::admit(int32_t s, int64_t context_tokens, int64_t input_tokens
   x.run_blocks = static_cast<int32_t>(d);
   out->resident_before = k;
   out->blocks = static_cast<int32_t>(d);
-  out->cached_tokens = std::min<int64_t>(int64_t(k) * B, std::max<int64_t>(context_tokens, int64_t(x.shared) * B));
+  out->cached_tokens = std::min<int64_t>(int64_t(pos) * B, std::max<int64_t>(context_tokens, int64_t(x.shared) * B));
   out->evicted = evicted;
+  out->swapped_out = static_cast<int32_t>(swap_out_.size());
+  out->swapped_in = static_cast<int32_t>(swap_in_.size());
   return true;
 }
 

@@ -20,6 +20,16 @@
 // referenced as a whole (a running request references all of it), so the heap
 // holds one entry per run, for its tail block: the block order above at
 // O(log runs) per eviction.
+//
+// Offload (a host pool of host_blocks > 0 blocks; CacheWise Sec. 6.4): an
+// evicted block is copied to a free host block (a swap out) and joins its
+// owner's host-held run, which follows the resident run; with no free host
+// block it is dropped, and with it the owner's host-held run (past it, so no
+// longer part of a leading run; for a shared block also the sharers' host-held
+// private runs).  An admission swaps the requesting context's host-held run
+// back in (shared blocks, then private ones once the shared run is complete)
+// after the evictions that make room.  Each admission records its swaps, outs
+// before ins: a caller copies them in that order before the request's kernels.
 #pragma once
 
 #include <stdint.h>
@@ -34,11 +44,17 @@ class BlockManager {
   struct Admission {
     int32_t resident_before = 0;  // leading resident blocks found (k)
     int32_t blocks = 0;           // blocks of the request (d)
-    int64_t cached_tokens = 0;    // prompt tokens whose K/V were resident
+    int64_t cached_tokens = 0;    // prompt tokens whose K/V were resident or swapped in
     int64_t evicted = 0;          // blocks evicted to make room
+    int32_t swapped_out = 0;      // of them, copied to the host pool
+    int32_t swapped_in = 0;       // blocks of the request brought back from the host pool
+  };
+  struct Swap {
+    int32_t device;  // page of the device pool
+    int32_t host;    // block of the host pool
   };
 
-  BlockManager(int32_t capacity_blocks, int32_t block_tokens);
+  BlockManager(int32_t capacity_blocks, int32_t block_tokens, int32_t host_blocks = 0);
 
   // Registers session s (ids 0, 1, ...) in shared-prefix group g (-1: none)
   // whose members share their first shared_tokens tokens.  Sessions are
@@ -53,6 +69,15 @@ class BlockManager {
   int64_t free_blocks() const { return static_cast<int64_t>(free_.size()); }
   int64_t resident_blocks() const { return capacity_ - free_blocks(); }
   int64_t referenced_blocks() const;
+  // Blocks of a request of `tokens` context + input + output tokens.
+  int64_t blocks_for(int64_t tokens) const { return (tokens + block_tokens_ - 1) / block_tokens_; }
+  // The fewest blocks a request of session s may have: its group's shared
+  // blocks and every private block it holds, resident or on the host (a
+  // context only grows).
+  int64_t min_blocks(int32_t s) const {
+    const Session& x = sess_[s];
+    return int64_t(x.shared) + int64_t(x.priv.size()) + int64_t(x.hpriv.size());
+  }
 
   // Admits a request of session s: its context holds context_tokens tokens,
   // the request adds input_tokens and output_tokens.  References the resident
@@ -72,6 +97,11 @@ class BlockManager {
   // Rebuilds the eviction heap from the current values.
   void rebuild();
   bool is_running(int32_t s) const { return sess_[s].running; }
+  // Swaps of the last admission: device -> host (before the ins), host -> device.
+  const std::vector<Swap>& swaps_out() const { return swap_out_; }
+  const std::vector<Swap>& swaps_in() const { return swap_in_; }
+  int32_t host_capacity() const { return host_capacity_; }
+  int64_t free_host_blocks() const { return static_cast<int64_t>(host_free_.size()); }
 
  private:
   enum Kind : uint8_t { kFree = 0, kPrivate = 1, kShared = 2 };
@@ -85,6 +115,7 @@ class BlockManager {
     int32_t group = -1;
     int32_t shared = 0;            // whole shared blocks (G)
     std::vector<int32_t> priv;     // resident private blocks, positions shared ..
+    std::vector<int32_t> hpriv;    // host-held private blocks after them (back(): lowest position)
     double value = 0.0;
     bool attached = false;         // has run at least one request
     bool running = false;
@@ -94,6 +125,7 @@ class BlockManager {
   struct Group {
     int32_t shared = 0;
     std::vector<int32_t> blocks;   // resident shared blocks, positions 0 ..
+    std::vector<int32_t> hblocks;  // host-held shared blocks after them (back(): lowest position)
     std::vector<int32_t> members;  // attached sessions
     uint32_t version = 0;
   };
@@ -113,6 +145,10 @@ class BlockManager {
 
   void push(int32_t owner);
   std::vector<int32_t>& run_of(int32_t owner);
+  std::vector<int32_t>& host_run_of(int32_t owner);
+  void drop_host_run(int32_t owner);
+  void swap_in_run(std::vector<int32_t>& host_run, std::vector<int32_t>& run, Kind kind, int32_t owner,
+                   int32_t* pos);
   void ref(int32_t b);
   void unref(int32_t b);
   bool group_key(int32_t g, double* v, int32_t* s) const;
@@ -126,6 +162,12 @@ class BlockManager {
   std::vector<Group> groups_;
   std::priority_queue<Entry> heap_;
   int64_t referenced_ = 0;  // resident blocks with a reference
+  int32_t host_capacity_;
+  std::vector<int32_t> host_free_;  // stack of free host block ids
+  std::vector<Swap> swap_out_, swap_in_;
+  // per host block: its entry in swap_out_ while the admission that wrote it
+  // runs its evictions (-1 otherwise); a drop cancels that copy
+  std::vector<int32_t> host_out_;
 };
 
 }  // namespace cw

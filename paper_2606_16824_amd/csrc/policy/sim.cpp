@@ -160,7 +160,9 @@ cw_status_t check_config(const cw_sim_config_t& c) {
       !(c.decode_s_per_token >= 0.0) || !std::isfinite(c.prefill_s_per_token) ||
       !std::isfinite(c.decode_s_per_token) || c.rebuild_every < 1 ||
       (c.sched != CW_SCHED_FCFS && c.sched != CW_SCHED_PREFIX_AWARE) ||
-      (c.evict != CW_EVICT_LRU && c.evict != CW_EVICT_PREDICTIVE && c.evict != CW_EVICT_BELADY))
+      (c.evict != CW_EVICT_LRU && c.evict != CW_EVICT_PREDICTIVE && c.evict != CW_EVICT_BELADY) ||
+      c.host_blocks < 0 || c.host_blocks > kMaxBlocks || !(c.swap_s_per_block >= 0.0) ||
+      !std::isfinite(c.swap_s_per_block))
     return policy_fail(CW_ERR_UNSUPPORTED, "invalid simulation configuration");
   return CW_OK;
 }
@@ -171,7 +173,7 @@ cw_status_t simulate(const cw_sim_config_t& c, const cw_sim_trace_t& tr, cw_sim_
   const int32_t S = tr.num_sessions;
   const int64_t B = c.block_tokens;
   std::vector<Session> ss(S);
-  BlockManager bm(c.capacity_blocks, c.block_tokens);
+  BlockManager bm(c.capacity_blocks, c.block_tokens, c.host_blocks);
   int64_t total_tokens = 0;
   for (int32_t s = 0; s < S; ++s) {
     ss[s].first = tr.turn_off[s];
@@ -228,6 +230,8 @@ cw_status_t simulate(const cw_sim_config_t& c, const cw_sim_trace_t& tr, cw_sim_
     if (!bm.admit(i, s.ctx, tr.in_tokens[j], tr.out_tokens[j], &adm))
       return policy_fail(CW_ERR_HIP, "block manager: request of session %d did not fit", i);
     r.evicted_blocks += adm.evicted;
+    r.swapped_out_blocks += adm.swapped_out;
+    r.swapped_in_blocks += adm.swapped_in;
     const int64_t hit = adm.cached_tokens;
     const int64_t prefill = s.ctx + tr.in_tokens[j] - hit;
     r.recomputed_tokens += std::max<int64_t>(0, s.ctx - hit);
@@ -239,6 +243,8 @@ cw_status_t simulate(const cw_sim_config_t& c, const cw_sim_trace_t& tr, cw_sim_
       log->session[w] = i;
       log->cached_tokens[w] = static_cast<int32_t>(hit);
       log->new_tokens[w] = static_cast<int32_t>(prefill);
+      if (log->swapped_in) log->swapped_in[w] = adm.swapped_in;
+      if (log->swapped_out) log->swapped_out[w] = adm.swapped_out;
       const int64_t n = std::min<int64_t>(int64_t(ids.size()), std::max<int64_t>(0, log->table_capacity - table_used));
       for (int64_t q = 0; q < n; ++q) log->tables[table_used + q] = ids[q];
       table_used += n;
@@ -247,7 +253,8 @@ cw_status_t simulate(const cw_sim_config_t& c, const cw_sim_trace_t& tr, cw_sim_
     }
     s.state = kRunning;
     running = i;
-    run_end = t + c.prefill_s_per_token * double(prefill) + c.decode_s_per_token * double(tr.out_tokens[j]);
+    run_end = t + (c.prefill_s_per_token * double(prefill) + c.decode_s_per_token * double(tr.out_tokens[j]) +
+                   c.swap_s_per_block * double(adm.swapped_out + adm.swapped_in));
     if (dispatch && r.requests < dispatch_capacity) dispatch[r.requests] = i;
     ++r.requests;
     return CW_OK;
@@ -365,18 +372,33 @@ struct cw_block_manager {
   std::vector<uint8_t> known;
 };
 
-cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out) {
+static cw_status_t bm_create(int32_t capacity_blocks, int32_t block_tokens, int32_t host_blocks,
+                             cw_block_manager_t** out) {
   if (!out) return policy_fail(CW_ERR_NULL, "out is required");
   *out = nullptr;
-  if (capacity_blocks < 1 || capacity_blocks > kMaxBlocks || block_tokens < 1)
-    return policy_fail(CW_ERR_UNSUPPORTED, "capacity_blocks = %d (1 .. %d), block_tokens = %d", capacity_blocks,
-                       kMaxBlocks, block_tokens);
+  if (capacity_blocks < 1 || capacity_blocks > kMaxBlocks || block_tokens < 1 || host_blocks < 0 ||
+      host_blocks > kMaxBlocks)
+    return policy_fail(CW_ERR_UNSUPPORTED, "capacity_blocks = %d (1 .. %d), block_tokens = %d, host_blocks = %d",
+                       capacity_blocks, kMaxBlocks, block_tokens, host_blocks);
   return guarded([&] {
     auto m = std::make_unique<cw_block_manager>();
-    m->bm = std::make_unique<BlockManager>(capacity_blocks, block_tokens);
+    m->bm = std::make_unique<BlockManager>(capacity_blocks, block_tokens, host_blocks);
     *out = m.release();
     return CW_OK;
   });
+}
+
+cw_status_t cw_bm_create(int32_t capacity_blocks, int32_t block_tokens, cw_block_manager_t** out) {
+  return bm_create(capacity_blocks, block_tokens, 0, out);
+}
+
+cw_status_t cw_bm_create_with_host_pool(int32_t capacity_blocks, int32_t block_tokens, int32_t host_blocks,
+                                        cw_block_manager_t** out) {
+  if (host_blocks < 1) {
+    if (out) *out = nullptr;
+    return policy_fail(CW_ERR_UNSUPPORTED, "host_blocks = %d: a host pool holds at least one block", host_blocks);
+  }
+  return bm_create(capacity_blocks, block_tokens, host_blocks, out);
 }
 
 cw_status_t cw_bm_destroy(cw_block_manager_t* m) {
@@ -403,10 +425,10 @@ cw_status_t cw_bm_add_session(cw_block_manager_t* m, int32_t session, int32_t gr
   });
 }
 
-cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_tokens, int64_t input_tokens,
-                        int64_t output_tokens, int32_t* table, int32_t table_capacity, int32_t* blocks,
-                        int64_t* cached_tokens, int64_t* evicted_blocks) {
-  if (!m || !blocks || !cached_tokens) return policy_fail(CW_ERR_NULL, "block manager, blocks and cached_tokens are required");
+static cw_status_t bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_tokens, int64_t input_tokens,
+                            int64_t output_tokens, int32_t* table, int32_t table_capacity, int32_t* blocks,
+                            int64_t* cached_tokens, int64_t* evicted_blocks, cw_bm_swaps_t* swaps) {
+  if (!blocks || !cached_tokens) return policy_fail(CW_ERR_NULL, "blocks and cached_tokens are required");
   if (session < 0 || session >= m->sessions || !m->known[session])
     return policy_fail(CW_ERR_BAD_LENS, "session %d is not registered", session);
   if (context_tokens < 0 || input_tokens < 0 || output_tokens < 0 || context_tokens > kMaxTokens ||
@@ -414,6 +436,21 @@ cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_
     return policy_fail(CW_ERR_BAD_LENS, "token counts must lie in [0, 2^40]");
   if (m->bm->is_running(session)) return policy_fail(CW_ERR_BAD_LENS, "session %d already has a request running", session);
   if (table_capacity < 0) return policy_fail(CW_ERR_BAD_LENS, "table_capacity < 0");
+  if (m->bm->blocks_for(context_tokens + input_tokens + output_tokens) < m->bm->min_blocks(session))
+    return policy_fail(CW_ERR_BAD_LENS,
+                       "session %d: the request's %lld blocks do not cover its shared prefix and held blocks (%lld)",
+                       session, static_cast<long long>(m->bm->blocks_for(context_tokens + input_tokens + output_tokens)),
+                       static_cast<long long>(m->bm->min_blocks(session)));
+  if (swaps) {
+    if (swaps->capacity < 0) return policy_fail(CW_ERR_BAD_LENS, "swap capacity < 0");
+    if (swaps->capacity > 0 && (!swaps->out_device || !swaps->out_host || !swaps->in_host || !swaps->in_device))
+      return policy_fail(CW_ERR_NULL, "the four swap arrays are required");
+    // every swap of the admission is one of the request's blocks: its block count bounds both lists
+    const int64_t need = m->bm->blocks_for(context_tokens + input_tokens + output_tokens);
+    if (need > swaps->capacity)
+      return policy_fail(CW_ERR_WORKSPACE, "swap lists hold %d entries; the request has %lld blocks", swaps->capacity,
+                         static_cast<long long>(need));
+  }
   return guarded([&] {
     BlockManager::Admission adm;
     if (!m->bm->admit(session, context_tokens, input_tokens, output_tokens, &adm))
@@ -428,8 +465,42 @@ cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_
       const int32_t n = std::min<int32_t>(table_capacity, static_cast<int32_t>(ids.size()));
       for (int32_t q = 0; q < n; ++q) table[q] = ids[q];
     }
+    if (swaps) {
+      const auto& so = m->bm->swaps_out();
+      const auto& si = m->bm->swaps_in();
+      for (size_t q = 0; q < so.size(); ++q) {
+        swaps->out_device[q] = so[q].device;
+        swaps->out_host[q] = so[q].host;
+      }
+      for (size_t q = 0; q < si.size(); ++q) {
+        swaps->in_host[q] = si[q].host;
+        swaps->in_device[q] = si[q].device;
+      }
+      swaps->n_out = static_cast<int32_t>(so.size());
+      swaps->n_in = static_cast<int32_t>(si.size());
+    }
     return CW_OK;
   });
+}
+
+cw_status_t cw_bm_admit(cw_block_manager_t* m, int32_t session, int64_t context_tokens, int64_t input_tokens,
+                        int64_t output_tokens, int32_t* table, int32_t table_capacity, int32_t* blocks,
+                        int64_t* cached_tokens, int64_t* evicted_blocks) {
+  if (!m) return policy_fail(CW_ERR_NULL, "block manager is NULL");
+  if (m->bm->host_capacity() > 0)
+    return policy_fail(CW_ERR_UNSUPPORTED, "a manager with a host pool admits through cw_bm_admit_swaps");
+  return bm_admit(m, session, context_tokens, input_tokens, output_tokens, table, table_capacity, blocks,
+                  cached_tokens, evicted_blocks, nullptr);
+}
+
+cw_status_t cw_bm_admit_swaps(cw_block_manager_t* m, int32_t session, int64_t context_tokens, int64_t input_tokens,
+                              int64_t output_tokens, int32_t* table, int32_t table_capacity, int32_t* blocks,
+                              int64_t* cached_tokens, int64_t* evicted_blocks, cw_bm_swaps_t* swaps) {
+  if (!m || !swaps) return policy_fail(CW_ERR_NULL, "block manager and swaps are required");
+  swaps->n_out = 0;
+  swaps->n_in = 0;
+  return bm_admit(m, session, context_tokens, input_tokens, output_tokens, table, table_capacity, blocks,
+                  cached_tokens, evicted_blocks, swaps);
 }
 
 cw_status_t cw_bm_release(cw_block_manager_t* m, int32_t session, double value) {
@@ -463,6 +534,13 @@ cw_status_t cw_bm_stats(cw_block_manager_t* m, int64_t* free_blocks, int64_t* re
   if (!m || !free_blocks || !referenced_blocks) return policy_fail(CW_ERR_NULL, "arguments are required");
   *free_blocks = m->bm->free_blocks();
   *referenced_blocks = m->bm->referenced_blocks();
+  return CW_OK;
+}
+
+cw_status_t cw_bm_host_stats(cw_block_manager_t* m, int64_t* free_host_blocks, int64_t* held_host_blocks) {
+  if (!m || !free_host_blocks || !held_host_blocks) return policy_fail(CW_ERR_NULL, "arguments are required");
+  *free_host_blocks = m->bm->free_host_blocks();
+  *held_host_blocks = m->bm->host_capacity() - m->bm->free_host_blocks();
   return CW_OK;
 }
 

@@ -1,0 +1,228 @@
+"""Offload in the KV block manager (CacheWise Sec. 6.4): evicted blocks go to a
+host pool and come back when their session resumes.
+
+- A hand-worked trace fixes the physical device and host blocks of every swap.
+- The ABI's error cases change nothing.
+- A serving loop moves page contents by the manager's swap lists (a numpy
+  model of the device pool and the host pool, copies in the documented order:
+  each admission's swap-outs, then its swap-ins, admissions in order) and checks
+  after every step that each admitted request's prefix pages hold that
+  session's K/V, token by token.  The GPU test of the same loop runs the copies
+  with cw_kv_swap_out / cw_kv_swap_in and the attention with
+  cw_step_attention."""
+import ctypes as C
+
+import numpy as np
+import pytest
+
+from paper_2606_16824_amd import _lib as L
+from paper_2606_16824_amd import policy
+
+
+def test_offload_worked_example():
+    # 4 device blocks of 4 tokens, 4 host blocks; blocks are handed out lowest id first
+    bm = policy.BlockManager(capacity_blocks=4, block_tokens=4, host_blocks=4)
+    for s in range(2):
+        bm.add_session(s)
+    t, cached, ev, outs, ins = bm.admit_swaps(0, 0, 8, 0)
+    assert (list(t), cached, ev, outs, ins) == ([0, 1], 0, 0, [], [])
+    bm.release(0, 1.0)
+    # 3 blocks, 2 free: session 0's tail block (1) goes to host block 0
+    t, cached, ev, outs, ins = bm.admit_swaps(1, 0, 12, 0)
+    assert (list(t), cached, ev, outs, ins) == ([1, 2, 3], 0, 1, [(1, 0)], [])
+    bm.release(1, 5.0)  # larger value: evicted first
+    # session 0 resumes with 3 blocks: its head (0) is resident, 2 are missing.
+    # Session 1's tail blocks 3 then 2 go to host blocks 1 and 2; then host
+    # block 0 comes back into device block 2 (just swapped out: the swap-outs'
+    # copies come first), and the third block is new (3).
+    t, cached, ev, outs, ins = bm.admit_swaps(0, 8, 4, 0)
+    assert (list(t), cached, ev) == ([0, 2, 3], 8, 2)
+    assert outs == [(3, 1), (2, 2)] and ins == [(0, 2)]
+    assert bm.host_stats() == {"free_host_blocks": 2, "held_host_blocks": 2}
+    bm.release(0, 2.0)
+    # session 1 resumes: its head block (1) is resident; its host-held blocks
+    # (positions 1, 2 in host blocks 2, 1) come back after session 0's blocks
+    # make room (tail first: 3 and 2 to host blocks 0 and 3)
+    t, cached, ev, outs, ins = bm.admit_swaps(1, 12, 0, 0)
+    assert (list(t), cached, ev) == ([1, 2, 3], 12, 2)
+    assert outs == [(3, 0), (2, 3)] and ins == [(2, 2), (1, 3)]
+    assert bm.host_stats() == {"free_host_blocks": 2, "held_host_blocks": 2}
+    bm.close()
+
+
+def test_full_host_pool_drops_the_owners_host_run():
+    bm = policy.BlockManager(capacity_blocks=3, block_tokens=4, host_blocks=1)
+    for s in range(2):
+        bm.add_session(s)
+    bm.admit_swaps(0, 0, 12, 0)
+    bm.release(0, 1.0)
+    # 3 evictions from session 0's tail: block 2 goes to the host block; block 1
+    # finds the pool full and is dropped with the host-held block past it (the
+    # context must stay a leading run), which cancels that copy; block 0 then
+    # goes to the freed host block.  One copy remains.
+    t, cached, ev, outs, ins = bm.admit_swaps(1, 0, 12, 0)
+    assert (list(t), ev, outs, ins) == ([0, 1, 2], 3, [(0, 0)], [])
+    assert bm.host_stats() == {"free_host_blocks": 0, "held_host_blocks": 1}
+    bm.release(1, 9.0)
+    # session 0 resumes (3 blocks, none resident, position 0 on the host): session
+    # 1's blocks 2, 1, 0 find the pool full and are dropped; host block 0 comes
+    # back into block 0 (position 0, 4 tokens found) and blocks 1, 2 are new
+    t, cached, ev, outs, ins = bm.admit_swaps(0, 12, 0, 0)
+    assert (list(t), cached, ev, outs, ins) == ([0, 1, 2], 4, 3, [], [(0, 0)])
+    assert bm.host_stats() == {"free_host_blocks": 1, "held_host_blocks": 0}
+    bm.close()
+
+
+def test_offload_abi_errors_change_nothing():
+    lib = L.load()
+    h = C.c_void_p()
+    assert lib.cw_bm_create_with_host_pool(8, 4, 0, C.byref(h)) == L.CW_ERR_UNSUPPORTED and not h.value
+    assert lib.cw_bm_create_with_host_pool(8, 4, (1 << 26) + 1, C.byref(h)) == L.CW_ERR_UNSUPPORTED
+    assert lib.cw_bm_create_with_host_pool(8, 4, 4, None) == L.CW_ERR_NULL
+    assert lib.cw_bm_create_with_host_pool(8, 4, 4, C.byref(h)) == L.CW_OK
+    try:
+        assert lib.cw_bm_add_session(h, 0, -1, 0) == L.CW_OK
+        blocks, cached, ev = C.c_int32(), C.c_int64(), C.c_int64()
+        table = np.zeros(8, np.int32)
+        # a host-pool manager admits only with the swap lists
+        assert lib.cw_bm_admit(h, 0, 0, 8, 0, table.ctypes.data, 8, C.byref(blocks), C.byref(cached),
+                               C.byref(ev)) == L.CW_ERR_UNSUPPORTED
+        lists = [np.zeros(8, np.int32) for _ in range(4)]
+        sw = policy._Swaps(*(x.ctypes.data for x in lists), 1, 7, 7)
+        args = (table.ctypes.data, 8, C.byref(blocks), C.byref(cached), C.byref(ev))
+        # 2 blocks, lists of 1 entry
+        assert lib.cw_bm_admit_swaps(h, 0, 0, 8, 0, *args, C.byref(sw)) == L.CW_ERR_WORKSPACE
+        assert (sw.n_out, sw.n_in) == (0, 0)
+        assert lib.cw_bm_admit_swaps(h, 0, 0, 8, 0, *args, None) == L.CW_ERR_NULL
+        sw.capacity = -1
+        assert lib.cw_bm_admit_swaps(h, 0, 0, 8, 0, *args, C.byref(sw)) == L.CW_ERR_BAD_LENS
+        sw = policy._Swaps(lists[0].ctypes.data, None, lists[2].ctypes.data, lists[3].ctypes.data, 8, 0, 0)
+        assert lib.cw_bm_admit_swaps(h, 0, 0, 8, 0, *args, C.byref(sw)) == L.CW_ERR_NULL
+        free, ref = C.c_int64(), C.c_int64()
+        assert lib.cw_bm_stats(h, C.byref(free), C.byref(ref)) == L.CW_OK and (free.value, ref.value) == (8, 0)
+        sw = policy._Swaps(*(x.ctypes.data for x in lists), 8, 0, 0)
+        assert lib.cw_bm_admit_swaps(h, 0, 0, 8, 0, *args, C.byref(sw)) == L.CW_OK
+        assert blocks.value == 2 and (sw.n_out, sw.n_in) == (0, 0)
+        assert lib.cw_bm_release(h, 0, 1.0) == L.CW_OK
+        # a context only grows: fewer blocks than the session holds is an error
+        assert lib.cw_bm_admit_swaps(h, 0, 4, 0, 0, *args, C.byref(sw)) == L.CW_ERR_BAD_LENS
+        assert lib.cw_bm_stats(h, C.byref(free), C.byref(ref)) == L.CW_OK and (free.value, ref.value) == (6, 0)
+        fh, hh = C.c_int64(), C.c_int64()
+        assert lib.cw_bm_host_stats(h, C.byref(fh), C.byref(hh)) == L.CW_OK and (fh.value, hh.value) == (4, 0)
+        assert lib.cw_bm_host_stats(h, None, C.byref(hh)) == L.CW_ERR_NULL
+    finally:
+        lib.cw_bm_destroy(h)
+
+
+def test_shared_prefix_must_be_covered():
+    bm = policy.BlockManager(capacity_blocks=8, block_tokens=4)
+    bm.add_session(0, group=0, shared_tokens=16)
+    with pytest.raises(RuntimeError):
+        bm.admit(0, 0, 12, 0)  # 3 blocks, the group shares 4
+    t, cached, _ = bm.admit(0, 0, 16, 0)
+    assert len(t) == 4 and cached == 0
+
+
+# --- the serving loop -------------------------------------------------------
+
+BLOCK = 16
+DEVICE_BLOCKS, HOST_BLOCKS = 20, 10
+GROUPS = [-1, -1, -1, -1, -1, 0, 0]  # sessions 5 and 6 share a prefix
+SHARED = 48                          # 3 blocks
+MAX_CTX = 9 * BLOCK
+
+
+def serving_steps(seed, n_steps=40):
+    """Steps of a serving loop: each a list of (session, input tokens); two
+    private sessions or one session per step; contexts grow to MAX_CTX tokens.
+    Also returns the eviction value of each release (larger evicts first)."""
+    rng = np.random.default_rng(seed)
+    ctx = [0] * len(GROUPS)
+    steps = []
+    for _ in range(n_steps):
+        live = [s for s in range(len(GROUPS)) if ctx[s] < MAX_CTX]
+        if not live:
+            break
+        k = 2 if len([s for s in live if GROUPS[s] < 0]) >= 2 and rng.random() < 0.4 else 1
+        pick = list(rng.choice([s for s in live if GROUPS[s] < 0], size=2, replace=False)) if k == 2 \
+            else [int(rng.choice(live))]
+        step = []
+        for s in pick:
+            lo = SHARED + 1 if (GROUPS[s] >= 0 and ctx[s] == 0) else 1
+            tin = int(min(MAX_CTX - ctx[s], rng.integers(lo, lo + 60)))
+            step.append((int(s), tin))
+            ctx[s] += tin
+        steps.append((step, [float(rng.random()) for _ in step]))
+    return steps
+
+
+def logical_kv(seed, width):
+    """K/V rows of every session's positions (the group's rows for its shared
+    prefix): [session][position] -> row of `width` values."""
+    rng = np.random.default_rng(seed + 1)
+    own = rng.standard_normal((len(GROUPS), MAX_CTX, width)).astype(np.float32)
+    grp = rng.standard_normal((max(GROUPS) + 1, SHARED, width)).astype(np.float32)
+    for s, g in enumerate(GROUPS):
+        if g >= 0:
+            own[s, :SHARED] = grp[g]
+    return own
+
+
+def run_loop(seed, apply_swaps, after_step):
+    """Drives the manager through serving_steps(seed).  apply_swaps(outs, ins)
+    moves page contents for one admission; after_step(rows) gets per admitted
+    request (session, block table, cached tokens, tokens after the request)."""
+    bm = policy.BlockManager(DEVICE_BLOCKS, BLOCK, host_blocks=HOST_BLOCKS)
+    for s, g in enumerate(GROUPS):
+        bm.add_session(s, g, SHARED if g >= 0 else 0)
+    ctx = [0] * len(GROUPS)
+    totals = {"out": 0, "in": 0, "evicted": 0, "hit": 0}
+    for step, values in serving_steps(seed):
+        rows = []
+        for s, tin in step:
+            table, cached, ev, outs, ins = bm.admit_swaps(s, ctx[s], tin, 0)
+            apply_swaps(outs, ins)
+            rows.append((s, table, cached, ctx[s] + tin))
+            totals["out"] += len(outs)
+            totals["in"] += len(ins)
+            totals["evicted"] += ev
+            totals["hit"] += cached
+        after_step(rows)
+        for (s, tin), v in zip(step, values):
+            ctx[s] += tin
+            bm.release(s, v)
+    bm.close()
+    return totals
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_swap_lists_keep_every_prefix_intact(seed):
+    W = 4
+    kv = logical_kv(seed, W)
+    dev = np.full((DEVICE_BLOCKS, BLOCK, W), np.nan, np.float32)
+    host = np.full((HOST_BLOCKS, BLOCK, W), np.nan, np.float32)
+
+    def apply_swaps(outs, ins):
+        # the copies of one list run in parallel on the GPU: no destination
+        # twice, and none read by another entry of the list
+        for lst in (outs, ins):
+            src, dst = [x for x, _ in lst], [y for _, y in lst]
+            assert len(set(src)) == len(src) and len(set(dst)) == len(dst)
+        for d, h in outs:
+            host[h] = dev[d]
+        for h, d in ins:
+            dev[d] = host[h]
+            host[h] = np.nan  # a freed host block holds nothing from now on
+
+    def after_step(rows):
+        for s, table, cached, end in rows:
+            assert len(table) == -(-end // BLOCK)
+            for p in range(cached):  # the prefix the attention reads
+                assert np.array_equal(dev[table[p // BLOCK], p % BLOCK], kv[s, p]), (s, p)
+        for s, table, cached, end in rows:  # the step writes the rest
+            for p in range(cached, end):
+                dev[table[p // BLOCK], p % BLOCK] = kv[s, p]
+
+    totals = run_loop(seed, apply_swaps, after_step)
+    # the loop exercises swap-outs, swap-ins, drops and cache hits
+    assert totals["out"] > 0 and totals["in"] > 0 and totals["evicted"] > totals["out"] and totals["hit"] > 0

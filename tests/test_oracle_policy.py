@@ -267,12 +267,14 @@ def test_offload_worked_example():
 def test_offload_full_host_pool_drops_the_tail_worked_example():
     """A host pool of 1 block: an evicted block goes out while the pool has room;
     the next finds it full and is dropped together with the host-held block behind
-    it, which frees the pool again.  A (t=0): 12 tokens (3 blocks), tool 50 s, then
-    4.  B (t=1, runs 12-25): 12 tokens in a 4-block node: A's tail (position 2)
-    goes out, A's position 1 is dropped and takes position 2 with it (1 swap out).
+    it, which frees the pool again; the copy of that block is then not made (nor
+    charged).  A (t=0): 12 tokens (3 blocks), tool 50 s, then 4.  B (t=1, runs
+    12-24): 12 tokens in a 4-block node: A's tail (position 2) goes out, A's
+    position 1 is dropped and takes position 2 with it (no swap out remains).
     A's second turn (t=62) keeps position 0 (4 tokens found) and needs 3 more
-    blocks: B's position 2 goes out, position 1 is dropped (freeing the pool),
-    position 0 goes out (2 swaps out); A recomputes 8 context tokens."""
+    blocks: B's position 2 goes out, position 1 is dropped (freeing the pool and
+    cancelling that copy), position 0 goes out (1 swap out); A recomputes 8
+    context tokens."""
     sess = [cp.SessionSpec(0.0, [cp.Turn(12, 0, 0, 50.0), cp.Turn(4, 0)]),
             cp.SessionSpec(1.0, [cp.Turn(12, 0)])]
     cfg = cp.Config(M=4, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict="lru",
@@ -280,9 +282,9 @@ def test_offload_full_host_pool_drops_the_tail_worked_example():
     r, log = cp.simulate_blocks(cfg, sess, [[1.0]])
     assert r.dispatch == [0, 1, 0]
     assert [(d.cached_tokens, d.new_tokens, d.swapped_in, d.swapped_out) for d in log] == \
-        [(0, 12, 0, 0), (0, 12, 0, 1), (4, 12, 0, 2)]
-    assert (r.evicted_blocks, r.swapped_out_blocks, r.swapped_in_blocks, r.recomputed_tokens) == (5, 3, 0, 8)
-    assert r.makespan_s == 62.0 + 12 + 2
+        [(0, 12, 0, 0), (0, 12, 0, 0), (4, 12, 0, 1)]
+    assert (r.evicted_blocks, r.swapped_out_blocks, r.swapped_in_blocks, r.recomputed_tokens) == (5, 1, 0, 8)
+    assert r.makespan_s == 62.0 + 12 + 1
 
 
 @pytest.mark.parametrize("seed", range(3))

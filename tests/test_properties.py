@@ -6,7 +6,8 @@
 - The policy: the library's simulator and block manager give exactly the
   oracle's block-level model (dispatch order, counters, block counts and cached
   tokens of every dispatch) on small random traces with random shared-prefix
-  groups, for every scheduling x eviction pair."""
+  groups, for every scheduling x eviction pair, with and without offload to a
+  host pool (sizes from none to more than every evicted block)."""
 import os
 
 import numpy as np
@@ -90,30 +91,34 @@ def trace(draw):
     sched = draw(st.sampled_from(["fcfs", "prefix"]))
     evict = draw(st.sampled_from(["lru", "predictive", "belady"]))
     rebuild = draw(st.integers(1, 4))
-    return sessions, groups, shared, history, cap, sched, evict, rebuild
+    host = draw(st.sampled_from([0, 0, 1, 2, 5, 40]))
+    swap_s = draw(st.sampled_from([0.0, 0.03]))
+    return sessions, groups, shared, history, cap, sched, evict, rebuild, host, swap_s
 
 
 @SETTINGS
 @given(trace())
 def test_simulator_matches_the_block_level_oracle(case):
-    sessions, groups, shared, history, cap, sched, evict, rebuild = case
+    sessions, groups, shared, history, cap, sched, evict, rebuild, host, swap_s = case
     kw = dict(capacity_blocks=cap, block_tokens=B, prefill_s_per_token=0.01, decode_s_per_token=0.05)
     got = policy.simulate(sessions, history, sched=sched, evict=evict, rebuild_every=rebuild,
                           groups=groups if shared else None, shared_tokens=shared if shared else None,
-                          log=True, **kw)
+                          log=True, host_blocks=host, swap_s_per_block=swap_s, **kw)
     want, wlog = cp.simulate_blocks(
         cp.Config(M=cap, block_tokens=B, prefill_s_per_token=0.01, decode_s_per_token=0.05,
-                  sched=sched, evict=evict, n_rebuild=rebuild),
+                  sched=sched, evict=evict, n_rebuild=rebuild, host_blocks=host,
+                  swap_s_per_block=swap_s),
         [cp.SessionSpec(st_, [cp.Turn(*t) for t in turns], group=groups[i] if shared else -1)
          for i, (st_, turns) in enumerate(sessions)],
         history, shared_tokens=shared)
     assert got["dispatch"] == want.dispatch
     for f in ("requests", "faults", "evicted_blocks", "recomputed_tokens", "prefilled_tokens",
-              "heap_rebuilds"):
+              "heap_rebuilds", "swapped_out_blocks", "swapped_in_blocks"):
         assert got[f] == getattr(want, f), f
     for f in ("makespan_s", "mean_session_s"):
         assert got[f] == pytest.approx(getattr(want, f), rel=1e-12), f
     assert [(s, c, n, len(t)) for s, c, n, t in got["log"]] == \
         [(d.session, d.cached_tokens, d.new_tokens, d.blocks) for d in wlog]
+    assert got["log_swaps"] == [(d.swapped_in, d.swapped_out) for d in wlog]
     for _, _, _, t in got["log"]:
         assert len(set(t)) == len(t) and all(0 <= x < cap for x in t)
