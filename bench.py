@@ -724,7 +724,7 @@ def main():
         result["workloads"] = run_others(OTHER_WORKLOADS, args.other_steps)
     if not decode and args.policy:
         from paper_2606_16824_amd import policy_bench
-        result["policy"] = policy_bench.run()
+        result["policy"] = policy_bench.run(host_fraction=1.0)
         result["policy_shared_prefix"] = policy_bench.run(shared_groups=4, shared_prefix_tokens=2000)
         print("[bench] policy simulation done", file=sys.stderr, flush=True)
     if not decode and args.swap:

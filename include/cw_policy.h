@@ -34,8 +34,11 @@
  *  - Offload (host_blocks > 0; CacheWise Sec. 6.4): an evicted block is copied
  *    to the host pool while it has a free block, else dropped together with the
  *    owner's host-held blocks past it (and, for a shared block, the sharers'
- *    host-held private blocks); a request first swaps its context's host-held
- *    blocks back in, after the evictions that make room for them.
+ *    host-held private blocks); a block of value +inf (no one uses it again:
+ *    a finished session under predictive or Belady eviction) is dropped the
+ *    same way.  A copy that a drop in the same admission discards is not made
+ *    nor charged.  A request first swaps its context's host-held blocks back
+ *    in, after the evictions that make room for them.
  *  - The predictor estimates E[tau | tau > e] of a tool type as the mean of
  *    (x - e) over its history samples x > e, and e when no sample exceeds e.
  *
@@ -197,7 +200,9 @@ cw_status_t cw_bm_stats(cw_block_manager_t* bm, int64_t* free_blocks, int64_t* r
  * host pool of host_blocks blocks (1 .. 2^26) while it has room, else they are
  * dropped with the owner's host-held blocks past them (for a shared block, also
  * the sharers' host-held private blocks), and a request's host-held context
- * blocks are swapped back in when it is admitted.  The manager decides; the
+ * blocks are swapped back in when it is admitted (a block released with value
+ * +inf is never copied out, and copies a later drop of the same admission
+ * discards are not listed).  The manager decides; the
  * caller moves the data (cw_kv_swap_out / cw_kv_swap_in of cw.h).  Admissions of
  * such a manager go through cw_bm_admit_swaps, which also returns the swaps:
  * out_device[i] -> out_host[i] (copy device page to host block) for the blocks

@@ -217,7 +217,9 @@ def simulate(cfg: Config, sessions: Sequence[SessionSpec], history: Sequence[Seq
 #    out); the host-held blocks of a context follow its resident run.  When the
 #    pool is full the block is dropped instead, and with it the owner's host-held
 #    blocks (past it, so no longer part of a leading run); a dropped shared block
-#    also drops the sharers' host-held private blocks.  A copy to the host pool
+#    also drops the sharers' host-held private blocks.  A block whose value is
+#    +inf (predictive: its session has finished; Belady: never used again) is
+#    dropped the same way rather than copied.  A copy to the host pool
 #    that a drop in the same admission discards is not made (its data would
 #    never be read) and is not counted.
 #  * a request first swaps its host-held blocks back in (shared ones, then its
@@ -294,13 +296,13 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
 
     def victim(i):
         """Largest key among the tail blocks of other sessions' private runs and of
-        the groups' shared runs: ('p', session) or ('g', group)."""
+        the groups' shared runs: ('p', session, value) or ('g', group, value)."""
         best, best_key = None, None
         for j in range(n):
             if j != i and res_private[j] > 0:
                 key = (value(j), -j, G[j] + res_private[j] - 1)
                 if best_key is None or key > best_key:
-                    best, best_key = ("p", j), key
+                    best, best_key = ("p", j, key[0]), key
         for g in range(len(shared_tokens)):
             if res_shared[g] == 0:
                 continue
@@ -311,7 +313,7 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
             jsel = max(j for j in sharers if value(j) == v)
             key = (v, -jsel, res_shared[g] - 1)
             if best_key is None or key > best_key:
-                best, best_key = ("g", g), key
+                best, best_key = ("g", g, v), key
         return best
 
     while True:
@@ -347,8 +349,9 @@ def simulate_blocks(cfg: Config, sessions: Sequence[SessionSpec], history: Seque
                 new_private = [0] * n
                 new_shared = [0] * len(shared_tokens)
                 while free < a:
-                    kind, x = victim(i)
-                    to_host = sum(host_private) + sum(host_shared) < cfg.host_blocks
+                    kind, x, v = victim(i)
+                    # a block no one will use again (value +inf) is not worth a copy
+                    to_host = v != INF and sum(host_private) + sum(host_shared) < cfg.host_blocks
                     if kind == "p":
                         res_private[x] -= 1
                         if to_host:

@@ -2,6 +2,7 @@
 #include "block_manager.h"
 
 #include <algorithm>
+#include <limits>
 
 namespace cw {
 
@@ -161,7 +162,9 @@ bool BlockManager::evict_one() {
     blocks_[b].owner = -1;
     free_.push_back(b);
     if (host_capacity_ > 0) {
-      if (!host_free_.empty()) {  // to the host pool: the block now leads the host-held run
+      // to the host pool while it has room, unless no one will use the block
+      // again (value +inf): it then leads the owner's host-held run
+      if (!host_free_.empty() && e.v != std::numeric_limits<double>::infinity()) {
         const int32_t hb = host_free_.back();
         host_free_.pop_back();
         host_run_of(e.owner).push_back(hb);

@@ -73,6 +73,21 @@ def test_full_host_pool_drops_the_owners_host_run():
     bm.close()
 
 
+def test_blocks_no_one_uses_again_are_dropped_not_copied():
+    bm = policy.BlockManager(capacity_blocks=4, block_tokens=4, host_blocks=4)
+    for s in range(3):
+        bm.add_session(s)
+    bm.admit_swaps(0, 0, 8, 0)
+    bm.release(0, float("inf"))  # finished
+    bm.admit_swaps(1, 0, 8, 0)
+    bm.release(1, 1.0)
+    # 3 blocks, 0 free: session 0's two blocks (value +inf) are dropped, then
+    # session 1's tail goes to the host pool
+    t, cached, ev, outs, ins = bm.admit_swaps(2, 0, 12, 0)
+    assert (ev, outs, ins) == (3, [(3, 0)], [])
+    bm.close()
+
+
 def test_offload_abi_errors_change_nothing():
     lib = L.load()
     h = C.c_void_p()

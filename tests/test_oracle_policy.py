@@ -333,4 +333,24 @@ def test_offload_accounting(seed, sched, evict):
         assert sum(d.swapped_out for d in log) == r.swapped_out_blocks
         assert sum(d.new_tokens for d in log) == r.prefilled_tokens
         if host == 10 ** 9:
-            assert r.recomputed_tokens == 0 and r.swapped_out_blocks == r.evicted_blocks
+            # every evicted block goes out, but those no one uses again
+            # (predictive and Belady know them: value +inf)
+            assert r.recomputed_tokens == 0
+            if evict == "lru":
+                assert r.swapped_out_blocks == r.evicted_blocks
+            else:
+                assert r.swapped_out_blocks < r.evicted_blocks
+
+
+def test_offload_skips_blocks_no_one_uses_again():
+    """A (t=0) runs one 8-token turn (2 blocks) and finishes at t=8; B (t=1) needs
+    3 blocks of a 4-block node after it and evicts one of A's.  Predictive and
+    Belady give a finished session's blocks the value +inf: the block is dropped,
+    not copied; LRU cannot tell and copies it."""
+    sess = [cp.SessionSpec(0.0, [cp.Turn(8, 0)]), cp.SessionSpec(1.0, [cp.Turn(12, 0)])]
+    for evict, out in (("lru", 1), ("predictive", 0), ("belady", 0)):
+        cfg = cp.Config(M=4, block_tokens=4, prefill_s_per_token=1.0, sched="fcfs", evict=evict,
+                        host_blocks=8, swap_s_per_block=1.0)
+        r, log = cp.simulate_blocks(cfg, sess, [[1.0]])
+        assert (r.evicted_blocks, r.swapped_out_blocks, r.swapped_in_blocks) == (1, out, 0), evict
+        assert r.makespan_s == 8.0 + 12 + out, evict
