@@ -49,6 +49,17 @@
  * must stay valid until the stream has passed the work.  Calls on one stream
  * may share one workspace; calls that may run concurrently need separate ones.
  *
+ * Graph capture: every call that runs kernels may be captured into a HIP graph
+ * (hipStreamBeginCapture on `stream`).  A captured call carries its plan in
+ * the arguments of small copy kernels (2 KiB each) instead of the staging
+ * ring, so each replay writes the plan it was captured with into its
+ * workspace; the lengths are those of capture time.  cw_init() must have been
+ * called on the device first (CW_ERR_INIT), and a captured call's plan may
+ * take at most 256 KiB (CW_ERR_UNSUPPORTED beyond).  The buffers of a captured
+ * call must stay valid while the graph may be replayed, and a replay shares
+ * its workspace (or the no-alloc scratch) with every other call using it, as
+ * any call on the graph's stream would.
+ *
  * Errors: every argument is checked before anything is enqueued, so a call
  * that returns an error has enqueued nothing.  A HIP failure while enqueuing
  * returns CW_ERR_HIP; faults inside kernels surface, as usual with HIP, at a

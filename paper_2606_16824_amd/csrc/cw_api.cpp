@@ -74,6 +74,9 @@ constexpr int kStagingSlots = 8;
 // Every staging slot has this fixed size, allocated once per device (cw_init or
 // the first call that uploads a plan); a plan larger than a slot is rejected.
 constexpr size_t kStagingSlotBytes = size_t(4) << 20;
+// A call captured into a graph carries its plan in kernel arguments (2 KiB per
+// copy launch); its plan may take at most this many bytes.
+constexpr size_t kCaptureMaxBytes = size_t(256) << 10;
 
 struct StagingSlot {
   void* host = nullptr;
@@ -90,6 +93,7 @@ struct DeviceState {
   bool ready = false;     // staging ring allocated
   StagingSlot slots[kStagingSlots];
   int next_slot = 0;
+  uint8_t* capture_buf = nullptr;  // kCaptureMaxBytes of host memory: plans of captured calls
   uint8_t* scratch = nullptr;  // this device's copy of the static scratch array (cw_init)
 };
 
@@ -142,7 +146,11 @@ cw_status_t init_locked(DeviceState& st) {
       if (st.slots[i].ev) (void)hipEventDestroy(st.slots[i].ev);
       st.slots[i] = StagingSlot{};
     }
+    delete[] st.capture_buf;
+    st.capture_buf = nullptr;
   };
+  st.capture_buf = new (std::nothrow) uint8_t[kCaptureMaxBytes];
+  if (st.capture_buf == nullptr) return fail(CW_ERR_UNSUPPORTED, "host memory for captured plans");
   for (; made < kStagingSlots; ++made) {
     StagingSlot& s = st.slots[made];
     e = hipHostMalloc(&s.host, kStagingSlotBytes, hipHostMallocDefault);
@@ -190,6 +198,9 @@ cw_status_t current_state(DeviceState** out) {
 // the event recorded behind its last reader has completed.  The ring is set up
 // on the first use on a device when cw_init has not done it, unless `no_alloc`
 // is set, in which case an uninitialised device is an error (CW_ERR_INIT).
+// A stream being captured into a graph gets the plan in the arguments of copy
+// kernels instead (each replay writes the captured plan again; no slot, no
+// event, no wait), and the ring must exist already (CW_ERR_INIT otherwise).
 template <class Fill, class Launch>
 cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
                              Launch&& launch, bool no_alloc, bool direct) {
@@ -199,11 +210,25 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
                 "the call's plan takes %zu bytes, more than the %zu-byte staging slot "
                 "(too many sequences or work items for one call)",
                 bytes, kStagingSlotBytes);
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  hipError_t ce = hipStreamIsCapturing(stream, &capture);
+  if (ce != hipSuccess) return hip_fail(ce, "hipStreamIsCapturing");
   DeviceState* stp = nullptr;
   cw_status_t s0 = current_state(&stp);
   if (s0 != CW_OK) return s0;
   DeviceState& st = *stp;
   std::lock_guard<std::mutex> g(st.staging_mu);
+  if (capture != hipStreamCaptureStatusNone) {
+    if (capture != hipStreamCaptureStatusActive) return fail(CW_ERR_HIP, "the stream's capture has been invalidated");
+    if (!st.ready) return fail(CW_ERR_INIT, "cw_init() must be called on this device before capturing a call");
+    if (bytes > kCaptureMaxBytes || bytes % 4 != 0)
+      return fail(CW_ERR_UNSUPPORTED, "a captured call's plan takes %zu bytes, more than %zu", bytes,
+                  kCaptureMaxBytes);
+    fill(st.capture_buf);
+    ce = launch_arg_copy(st.capture_buf, dst, bytes, stream);
+    if (ce != hipSuccess) return hip_fail(ce, "plan upload kernel launch");
+    return launch(static_cast<const uint8_t*>(dst));
+  }
   if (!st.ready) {
     if (no_alloc) return fail(CW_ERR_INIT, "cw_init() has not been called on this device");
     s0 = init_locked(st);

@@ -132,6 +132,10 @@ hipError_t launch_swap(const SwapParams& p, hipStream_t stream);
 // Copies `bytes` from device-visible pinned host memory to device memory on
 // `stream` with a kernel (the plan upload).
 hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+// Plan bytes carried in kernel arguments, kArgChunkBytes per launch (bytes a
+// multiple of 4; for calls captured into a graph).
+constexpr size_t kArgChunkBytes = 2048;
+hipError_t launch_arg_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 hipError_t launch_check_table(const int32_t* bt, int32_t bt_stride, int32_t num_pages,
                               const SeqInfo* seqs, int32_t num_seqs, int32_t page_size,
                               int32_t* bad, hipStream_t stream);

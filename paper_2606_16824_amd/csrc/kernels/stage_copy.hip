@@ -5,6 +5,9 @@
 // attention kernels (a copy engine would cost a hand-off between queues).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cstring>
+
 #include "../cw_internal.h"
 
 namespace cw {
@@ -24,7 +27,37 @@ __global__ __launch_bounds__(kThreads) void stage_copy_kernel(const uint8_t* src
   if (first < bytes - n16 * 16) dst[n16 * 16 + first] = src[n16 * 16 + first];
 }
 
+// Plan upload under stream capture: the bytes travel in the kernel's own
+// arguments, which a captured launch keeps by value, so every replay of the
+// graph writes the plan the call was captured with (a staging slot would be
+// read at replay time, after later calls may have refilled it).
+struct ArgChunk {
+  uint32_t* dst;
+  uint32_t words;
+  uint32_t data[kArgChunkBytes / 4];
+};
+
+__global__ __launch_bounds__(kThreads) void arg_copy_kernel(ArgChunk a) {
+  for (uint32_t i = threadIdx.x; i < a.words; i += kThreads) a.dst[i] = a.data[i];
+}
+
 }  // namespace
+
+hipError_t launch_arg_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+  const uint8_t* s = static_cast<const uint8_t*>(src);
+  uint8_t* d = static_cast<uint8_t*>(dst);
+  for (size_t off = 0; off < bytes; off += kArgChunkBytes) {
+    ArgChunk a;
+    const size_t n = std::min(bytes - off, kArgChunkBytes);
+    a.dst = reinterpret_cast<uint32_t*>(d + off);
+    a.words = static_cast<uint32_t>(n / 4);
+    std::memcpy(a.data, s + off, n);
+    hipLaunchKernelGGL(arg_copy_kernel, dim3(1), dim3(kThreads), 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
 
 hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
   if (bytes == 0) return hipSuccess;
