@@ -197,7 +197,11 @@ bool BlockManager::admit(int32_t s, int64_t context_tokens, int64_t input_tokens
   swap_out_.clear();
   swap_in_.clear();
   while (static_cast<int64_t>(free_.size()) < a) {
-    if (!evict_one()) return false;  // unreachable: the heap holds every evictable block
+    if (!evict_one()) {  // unreachable: the heap holds every evictable block
+      for (const Swap& w : swap_out_)
+        if (w.host >= 0) host_out_[w.host] = -1;
+      return false;
+    }
     ++evicted;
   }
   // the copies that still matter (each host block written at most once)
