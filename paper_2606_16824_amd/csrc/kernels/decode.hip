@@ -450,7 +450,7 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
     if (p.lse != nullptr && h == 0)
       p.lse[size_t(tok) * hq + size_t(kvh) * G + col] = (m_run + __log2f(l_tot)) * kLn2;
   } else {
-    float* po = p.part_o + (size_t(it.part) * p.part_rows + col) * D;
+    float* po = static_cast<float*>(p.part_o) + (size_t(it.part) * p.part_rows + col) * D;
 #pragma unroll
     for (int b = 0; b < T::DB; ++b) {
 #pragma unroll

@@ -630,15 +630,18 @@ void extend_w64_kernel(ExtendParams p) {
       }
       if (p.lse != nullptr && h == 0) p.lse[orow_idx] = (m_run[rb] + __log2f(l_tot)) * kLn2;
     } else {
-      float* po = p.part_o + (size_t(it.part) * p.part_rows + r_local[rb]) * D;
+      // the unnormalised partial O in bf16
+      uint16_t* po = static_cast<uint16_t*>(p.part_o) + (size_t(it.part) * p.part_rows + r_local[rb]) * D;
 #pragma unroll
       for (int b = 0; b < T::DB; ++b) {
         __builtin_amdgcn_sched_barrier(0);  // one accumulator at a time
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const int d = 32 * b + 8 * q4 + 4 * h;
-          *reinterpret_cast<float4*>(po + d) =
-              make_float4(o[rb][b][4 * q4], o[rb][b][4 * q4 + 1], o[rb][b][4 * q4 + 2], o[rb][b][4 * q4 + 3]);
+          bf16x4 v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v4[e] = static_cast<__bf16>(o[rb][b][4 * q4 + e]);
+          *reinterpret_cast<u32x2*>(po + d) = __builtin_bit_cast(u32x2, v4);
         }
       }
       if (h == 0) {

@@ -69,7 +69,7 @@ def test_noalloc_rejects_a_plan_larger_than_the_scratch():
     dw = to_gpu(w)
     print("\n[case] noalloc over the scratch size (turn, one-tile split-K chunks)", flush=True)
     out = torch.full_like(dw.q, float("nan"))
-    cwlib.set_tuning(0, 1)  # about 35k partial slots of 128 KiB: far above the cap
+    cwlib.set_tuning(0, 1)  # about 35k partial slots of 64 KiB: far above the cap
     try:
         need = cwlib.extend_workspace_bytes(s.prefix_lens, s.suffix_lens, s.num_kv_heads,
                                             s.gqa_group, s.head_dim, s.page_size)
