@@ -460,12 +460,11 @@ ExtendParams plan_params(const ExtendPlan& plan, const uint8_t* meta, uint8_t* w
   p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
   p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
   p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
-  p.part_o = ws + part + (plan.off_part_o - plan.meta_bytes);
+  p.part_o = reinterpret_cast<uint16_t*>(ws + part + (plan.off_part_o - plan.meta_bytes));
   p.part_ml = reinterpret_cast<float*>(ws + part + (plan.off_part_ml - plan.meta_bytes));
   p.n_items = static_cast<int32_t>(plan.items.size());
   p.n_groups = static_cast<int32_t>(plan.groups.size());
   p.part_rows = plan.part_rows;
-  p.part_bf16 = plan.part_elem_bytes == 2 ? 1 : 0;
   return p;
 }
 
@@ -523,9 +522,8 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   p.block_table = block_table;
   p.out = out;
   p.lse = lse;
-  p.part_o = ws + plan.off_part_o;
+  p.part_o = reinterpret_cast<uint16_t*>(ws + plan.off_part_o);
   p.part_ml = reinterpret_cast<float*>(ws + plan.off_part_ml);
-  p.part_bf16 = plan.part_elem_bytes == 2 ? 1 : 0;
   p.bt_stride = bt_stride;
   p.num_kv_heads = num_kv_heads;
   p.gqa_group = gqa_group;

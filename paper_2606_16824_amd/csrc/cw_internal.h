@@ -81,7 +81,7 @@ struct ExtendParams {
   const SeqInfo* seqs;
   const WorkItem* items;
   const CombineGroup* groups;
-  void* part_o;    // [n_parts, part_rows, D]: bf16 for extend plans, fp32 for decode plans
+  uint16_t* part_o;  // [n_parts, part_rows, D] bf16: the unnormalised partial O
   float* part_ml;  // [n_parts, part_rows, 2]  (running max in log2 units, sum)
   int32_t bt_stride;
   int32_t num_kv_heads;
@@ -91,7 +91,6 @@ struct ExtendParams {
   int32_t n_items;
   int32_t n_groups;
   int32_t part_rows;  // rows per split-K partial slot (the row block for extend, G for decode)
-  int32_t part_bf16;  // 1: part_o holds bf16 (extend), 0: fp32 (decode)
   WriteParams w;      // extend: also scatter the new K/V into the pools when w.total_tokens > 0
 };
 

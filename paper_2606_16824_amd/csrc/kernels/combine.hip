@@ -10,31 +10,22 @@ constexpr float kLn2 = 0.69314718055994531f;
 constexpr int kFewParts = 4;  // the one-slice merge loads up to this many partials at once
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// PER consecutive elements of a partial's O row as fp32: bf16 partials (the
-// extend's) or fp32 partials (the decode's).
-template <bool BF16, int PER>
-__device__ __forceinline__ void load_part(const void* base, size_t elem, float (&v)[PER]) {
-  if constexpr (BF16) {
-    static_assert(PER == 2 || PER == 4, "two or four bf16 per lane");
-    const uint16_t* src = static_cast<const uint16_t*>(base) + elem;
-    if constexpr (PER == 4) {
-      const u32x2 w = *reinterpret_cast<const u32x2*>(src);
+// PER consecutive bf16 elements of a partial's O row, as fp32.
+template <int PER>
+__device__ __forceinline__ void load_part(const uint16_t* base, size_t elem, float (&v)[PER]) {
+  static_assert(PER == 2 || PER == 4, "two or four elements per lane");
+  if constexpr (PER == 4) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(base + elem);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        v[2 * i] = __uint_as_float(w[i] << 16);
-        v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
-      }
-    } else {
-      const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
-      v[0] = __uint_as_float(w << 16);
-      v[1] = __uint_as_float(w & 0xFFFF0000u);
+    for (int i = 0; i < 2; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
     }
   } else {
-    const float* src = static_cast<const float*>(base) + elem;
-#pragma unroll
-    for (int e = 0; e < PER; ++e) v[e] = src[e];
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(base + elem);
+    v[0] = __uint_as_float(w << 16);
+    v[1] = __uint_as_float(w & 0xFFFF0000u);
   }
 }
 
@@ -43,7 +34,7 @@ __device__ __forceinline__ void load_part(const void* base, size_t elem, float (
 // each row's SLICES slices of 32 lanes fold every SLICES-th partial with an
 // online merge, then the slices are merged through LDS (SLICES = 1 for a few
 // partials per row, 8 for many).  Fixed order, no atomics.
-template <int D, int SLICES, bool BF16>
+template <int D, int SLICES>
 __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
   constexpr int ROWS = 8 / SLICES;
   constexpr int PER = D / 32;  // dims per lane
@@ -75,7 +66,7 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
         const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + pr * 2);
         mc[c] = ml.x;
         lc[c] = ml.y;
-        load_part<BF16, PER>(p.part_o, pr * D + d0, oc[c]);
+        load_part<PER>(p.part_o, pr * D + d0, oc[c]);
       }
     }
 #pragma unroll
@@ -104,7 +95,7 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
           const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + pr * 2);
           mc[k] = ml.x;
           lc[k] = ml.y;
-          load_part<BF16, PER>(p.part_o, pr * D + d0, oc[k]);
+          load_part<PER>(p.part_o, pr * D + d0, oc[k]);
         }
       }
       float m_new = m;
@@ -176,21 +167,15 @@ hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hi
   const bool many = max_parts > 4;
   const int rows_per_wg = many ? 1 : 8;
   const dim3 grid(p.n_groups * ((p.part_rows + rows_per_wg - 1) / rows_per_wg));
-#define CW_COMBINE(D_, S_)                                                              \
-  do {                                                                                  \
-    if (p.part_bf16) hipLaunchKernelGGL((combine_kernel<D_, S_, true>), grid, dim3(256), 0, stream, p); \
-    else hipLaunchKernelGGL((combine_kernel<D_, S_, false>), grid, dim3(256), 0, stream, p);          \
-  } while (0)
   if (head_dim == 64) {
-    if (many) CW_COMBINE(64, 8);
-    else CW_COMBINE(64, 1);
+    if (many) hipLaunchKernelGGL((combine_kernel<64, 8>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((combine_kernel<64, 1>), grid, dim3(256), 0, stream, p);
   } else if (head_dim == 128) {
-    if (many) CW_COMBINE(128, 8);
-    else CW_COMBINE(128, 1);
+    if (many) hipLaunchKernelGGL((combine_kernel<128, 8>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((combine_kernel<128, 1>), grid, dim3(256), 0, stream, p);
   } else {
     return hipErrorInvalidValue;
   }
-#undef CW_COMBINE
   return hipGetLastError();
 }
 

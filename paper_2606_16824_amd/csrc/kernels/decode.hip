@@ -450,13 +450,16 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
     if (p.lse != nullptr && h == 0)
       p.lse[size_t(tok) * hq + size_t(kvh) * G + col] = (m_run + __log2f(l_tot)) * kLn2;
   } else {
-    float* po = static_cast<float*>(p.part_o) + (size_t(it.part) * p.part_rows + col) * D;
+    // the unnormalised partial O in bf16 (relative rounding 2^-9, the range of fp32)
+    uint16_t* po = p.part_o + (size_t(it.part) * p.part_rows + col) * D;
 #pragma unroll
     for (int b = 0; b < T::DB; ++b) {
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        float4 v = make_float4(o[b][4 * q4], o[b][4 * q4 + 1], o[b][4 * q4 + 2], o[b][4 * q4 + 3]);
-        *reinterpret_cast<float4*>(po + 32 * b + 8 * q4 + 4 * h) = v;
+        bf16x4 v4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = static_cast<__bf16>(o[b][4 * q4 + e]);
+        *reinterpret_cast<u32x2*>(po + 32 * b + 8 * q4 + 4 * h) = __builtin_bit_cast(u32x2, v4);
       }
     }
     if (h == 0) {

@@ -785,7 +785,7 @@ void extend_lds_kernel(ExtendParams p) {
       p.lse[size_t(sq.cu + t) * hq + size_t(kvh) * G + g] = (m_run + __log2f(l_tot)) * kLn2;
   } else {
     // the unnormalised partial O in bf16 (relative rounding 2^-9, the range of fp32)
-    uint16_t* po = static_cast<uint16_t*>(p.part_o) + (size_t(it.part) * p.part_rows + r_local) * D;
+    uint16_t* po = p.part_o + (size_t(it.part) * p.part_rows + r_local) * D;
 #pragma unroll
     for (int b = 0; b < T::DB; ++b) {
 #pragma unroll

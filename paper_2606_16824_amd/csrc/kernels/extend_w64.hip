@@ -631,7 +631,7 @@ void extend_w64_kernel(ExtendParams p) {
       if (p.lse != nullptr && h == 0) p.lse[orow_idx] = (m_run[rb] + __log2f(l_tot)) * kLn2;
     } else {
       // the unnormalised partial O in bf16
-      uint16_t* po = static_cast<uint16_t*>(p.part_o) + (size_t(it.part) * p.part_rows + r_local[rb]) * D;
+      uint16_t* po = p.part_o + (size_t(it.part) * p.part_rows + r_local[rb]) * D;
 #pragma unroll
       for (int b = 0; b < T::DB; ++b) {
         __builtin_amdgcn_sched_barrier(0);  // one accumulator at a time

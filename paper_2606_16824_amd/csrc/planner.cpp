@@ -238,9 +238,8 @@ ExtendPlan build_extend_plan(const int32_t* prefix_lens, const int32_t* suffix_l
   // trailing idle items launch nothing useful
   while (!plan.items.empty() && plan.items.back().seq < 0) plan.items.pop_back();
 
-  // 7. workspace layout (the extend's partial O in bf16)
+  // 7. workspace layout
   plan.part_rows = block_m;
-  plan.part_elem_bytes = 2;
   layout_workspace(plan, head_dim);
   return plan;
 }
@@ -252,8 +251,8 @@ void layout_workspace(ExtendPlan& plan, int32_t head_dim) {
   plan.off_groups = align256(plan.off_items + plan.items.size() * sizeof(WorkItem));
   plan.meta_bytes = align256(plan.off_groups + plan.groups.size() * sizeof(CombineGroup));
   plan.off_part_o = plan.meta_bytes;
-  plan.off_part_ml =
-      align256(plan.off_part_o + size_t(plan.n_parts) * plan.part_rows * head_dim * size_t(plan.part_elem_bytes));
+  // the partial O is stored in bf16 (2 bytes), the running max and sum in fp32
+  plan.off_part_ml = align256(plan.off_part_o + size_t(plan.n_parts) * plan.part_rows * head_dim * 2);
   plan.total_bytes = align256(plan.off_part_ml + size_t(plan.n_parts) * plan.part_rows * 2 * sizeof(float));
 }
 }  // namespace

@@ -29,7 +29,6 @@ struct ExtendPlan {
   size_t meta_bytes = 0;  // seqs + items + groups: the part uploaded per call
   size_t total_bytes = 0;
   int32_t part_rows = 0;  // rows per partial slot
-  int32_t part_elem_bytes = 4;  // bytes per element of a partial's O: 2 (bf16, extend) or 4 (fp32, decode)
 };
 
 // Builds the plan for a kernel whose workgroups own `block_m` rows and of
