@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--plan-direct", type=int, default=0, choices=[0, 1],
                     help="1: kernels read the plan from the pinned staging slot; 0 (default): "
                          "it is copied to the workspace first")
+    ap.add_argument("--compact-decode", type=int, default=1, choices=[0, 1],
+                    help="1 (default): decode plans are uploaded in compact form and rebuilt on "
+                         "the device; 0: their work items are uploaded as they are")
     ap.add_argument("--suffix-weight", type=int, default=None,
                     help="split-K cost of a key tile past the cached prefix, percent of a prefix tile "
                          "(default: the library's)")
@@ -622,6 +625,7 @@ def main():
     cwlib.set_tuning(cwlib._lib.CW_TUNE_EXTEND_KERNEL, args.extend_kernel)
     cwlib.set_tuning(cwlib._lib.CW_TUNE_DEAL_ROUNDS, args.deal_rounds)
     cwlib.set_tuning(cwlib._lib.CW_TUNE_PLAN_DIRECT, args.plan_direct)
+    cwlib.set_tuning(cwlib._lib.CW_TUNE_COMPACT_DECODE, args.compact_decode)
     if args.suffix_weight is not None:
         cwlib.set_tuning(cwlib._lib.CW_TUNE_SUFFIX_WEIGHT, args.suffix_weight)
     res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,

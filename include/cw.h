@@ -319,6 +319,12 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           of a prefix tile (1 .. 10000; default 125, the
  *                           measured cost of the masked tiles; 100: equal
  *                           key counts).
+ *   CW_TUNE_COMPACT_DECODE  1 = a decode plan (of cw_decode_attention or of a
+ *                           step's decodes) is uploaded in compact form, one
+ *                           record per sequence, and rebuilt on the device by
+ *                           the upload kernel (the default; up to 2048
+ *                           sequences, beyond that as 0); 0 = its work items
+ *                           are uploaded as they are.  Larger values act as 1.
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {
   CW_TUNE_KV_CHUNK_TILES = 0,
@@ -327,6 +333,7 @@ typedef enum {
   CW_TUNE_DEAL_ROUNDS = 3,
   CW_TUNE_PLAN_DIRECT = 4,
   CW_TUNE_SUFFIX_WEIGHT = 5,
+  CW_TUNE_COMPACT_DECODE = 6,
   CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
   CW_TUNE_RANGE_MAX_ = 2147483647
 } cw_tune_key_t;
@@ -352,6 +359,21 @@ int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix
                              int32_t num_seqs, int32_t num_kv_heads, int32_t gqa_group,
                              int32_t head_dim, int32_t page_size, int32_t* items_out,
                              int64_t capacity);
+
+/* Host-only view of the decode plan (cw_decode_attention's), for tests: its
+ * work items (8 int32 each, as cw_extend_plan_items) and merge groups (8 int32
+ * each: {seq, kv_head, first row, rows, first partial slot, partial slots, 0,
+ * 0}), as the planner builds them (rebuilt = 0) or as the plan-upload kernel
+ * rebuilds them from the compact form (rebuilt = 1, the same function run on
+ * the host).  Writes up to items_capacity items and groups_capacity groups;
+ * returns the number of items and sets *num_groups, or returns -1 if the
+ * arguments are invalid or (rebuilt = 1) the plan has no compact form.  Works
+ * without a GPU. */
+int64_t cw_decode_plan_items(const int32_t* prefix_lens_h, int32_t num_seqs, int32_t num_kv_heads,
+                             int32_t gqa_group, int32_t head_dim, int32_t page_size,
+                             cw_kv_dtype_t kv_dtype, int32_t rebuilt, int32_t* items_out,
+                             int64_t items_capacity, int32_t* groups_out, int64_t groups_capacity,
+                             int64_t* num_groups);
 
 /* One-time set-up of the current device: allocates the pinned plan staging
  * ring (which every other call otherwise does on first use) and resolves this

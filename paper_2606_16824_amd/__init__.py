@@ -35,7 +35,7 @@ from . import _lib as L
 
 __all__ = ["CWError", "init", "pinned_allocations", "extend_attention", "extend_attention_noalloc", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
-           "set_tuning", "plan_items", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
+           "set_tuning", "plan_items", "decode_plan", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
            "step_attention", "step_workspace_bytes", "check_block_table", "ceiling_mfma_bf16", "ceiling_stream_read",
            "ceiling_stream_copy"]
 
@@ -212,6 +212,25 @@ def plan_items(prefix_lens, suffix_lens, num_kv_heads, gqa_group, head_dim, page
     lib.cw_extend_plan_items(_ptr(lp), _ptr(ls), len(lp), num_kv_heads, gqa_group, head_dim,
                              page_size, out.ctypes.data, n)
     return out[:n]
+
+
+def decode_plan(prefix_lens, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype="bf16",
+                rebuilt=False):
+    """The decode work list and merge groups, int32 [n, 8] each (see
+    cw_decode_plan_items): as planned, or as rebuilt from the compact form."""
+    lp = _lens(prefix_lens)
+    lib = library()
+    ng = C.c_int64()
+    dt = {"bf16": L.CW_KV_BF16, "fp8": L.CW_KV_FP8_E4M3FN}[kv_dtype]
+    n = lib.cw_decode_plan_items(_ptr(lp), len(lp), num_kv_heads, gqa_group, head_dim, page_size, dt,
+                                 int(rebuilt), None, 0, None, 0, C.byref(ng))
+    if n < 0:
+        raise CWError(L.CW_ERR_UNSUPPORTED, "invalid plan arguments")
+    items = np.zeros((max(n, 1), 8), dtype=np.int32)
+    groups = np.zeros((max(ng.value, 1), 8), dtype=np.int32)
+    lib.cw_decode_plan_items(_ptr(lp), len(lp), num_kv_heads, gqa_group, head_dim, page_size, dt,
+                             int(rebuilt), items.ctypes.data, n, groups.ctypes.data, ng.value, C.byref(ng))
+    return items[:n], groups[:ng.value]
 
 
 def kv_write_pages(k_new, v_new, k_pool, v_pool, block_table, prefix_lens, suffix_lens,

@@ -201,9 +201,37 @@ cw_status_t current_state(DeviceState** out) {
 // A stream being captured into a graph gets the plan in the arguments of copy
 // kernels instead (each replay writes the captured plan again; no slot, no
 // event, no wait), and the ring must exist already (CW_ERR_INIT otherwise).
-template <class Fill, class Launch>
+// With `compact` (a decode plan in compact form, copy mode only) the slot gets
+// the meta's first compact->verbatim bytes (fill_head) and the plan's records,
+// and the upload kernel rebuilds the decode items and groups on the device.
+struct CompactUpload {
+  const ExtendPlan* plan = nullptr;  // nullptr: upload the meta as it is
+  size_t verbatim = 0;               // bytes of the meta before the decode items
+  size_t bytes = 0;                  // bytes of the compact blob
+  ExpandDesc desc{};
+};
+
+// The compact upload of decode plan `plan` whose meta starts at byte `at` of a
+// call's meta; false when the plan has no compact form or it is switched off.
+bool compact_upload(const ExtendPlan& plan, size_t at, CompactUpload* cu) {
+  if (!plan.compact || current_tuning().compact_decode == 0 || plan.recs.empty() ||
+      plan.recs.size() > size_t(kMaxExpandSeqs))
+    return false;
+  cu->plan = &plan;
+  cu->verbatim = at + plan.off_items;
+  cu->desc = plan.desc;
+  cu->desc.rec_off = static_cast<uint32_t>(cu->verbatim);
+  cu->desc.tail_off = static_cast<uint32_t>(cu->verbatim + plan.recs.size() * sizeof(DecodeRec));
+  cu->desc.items_off = static_cast<uint32_t>(at + plan.off_items);
+  cu->desc.groups_off = static_cast<uint32_t>(at + plan.off_groups);
+  cu->bytes = (size_t(cu->desc.tail_off) + plan.tails.size() * sizeof(int32_t) + 15) & ~size_t(15);
+  return true;
+}
+
+template <class Fill, class Launch, class FillHead>
 cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
-                             Launch&& launch, bool no_alloc, bool direct) {
+                             Launch&& launch, bool no_alloc, bool direct,
+                             const CompactUpload* compact, FillHead&& fill_head) {
   if (bytes == 0) return launch(static_cast<const uint8_t*>(dst));
   if (bytes > kStagingSlotBytes)
     return fail(CW_ERR_UNSUPPORTED,
@@ -242,12 +270,23 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
     s.pending = false;
   }
-  fill(static_cast<uint8_t*>(s.host));
+  const bool use_compact = compact != nullptr && compact->plan != nullptr && !direct &&
+                           compact->bytes <= kStagingSlotBytes && compact->bytes < bytes;
+  uint8_t* h = static_cast<uint8_t*>(s.host);
+  if (use_compact) {
+    const ExtendPlan& cp = *compact->plan;
+    fill_head(h);
+    std::memcpy(h + compact->desc.rec_off, cp.recs.data(), cp.recs.size() * sizeof(DecodeRec));
+    std::memcpy(h + compact->desc.tail_off, cp.tails.data(), cp.tails.size() * sizeof(int32_t));
+  } else {
+    fill(h);
+  }
   cw_status_t launched = CW_OK;
   if (direct) {
     launched = launch(static_cast<const uint8_t*>(s.dev));
   } else {
-    e = launch_stage_copy(s.dev, dst, bytes, stream);
+    e = use_compact ? launch_plan_expand(s.dev, dst, compact->verbatim, compact->desc, stream)
+                    : launch_stage_copy(s.dev, dst, bytes, stream);
     if (e != hipSuccess) return hip_fail(e, "plan upload kernel launch");
   }
   // recorded even when a launch failed: whatever was enqueued may read the slot
@@ -260,7 +299,8 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
 
 template <class Fill>
 cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill) {
-  return stage_and_launch(bytes, dst, stream, fill, [](const uint8_t*) { return CW_OK; }, false, false);
+  return stage_and_launch(bytes, dst, stream, fill, [](const uint8_t*) { return CW_OK; }, false, false,
+                          nullptr, fill);
 }
 
 cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
@@ -571,8 +611,11 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     }
     return CW_OK;
   };
+  CompactUpload cu;
+  const bool compact = decode && compact_upload(plan, 0, &cu);
   return stage_and_launch(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); },
-                          launch, no_alloc, plan_direct(no_alloc));
+                          launch, no_alloc, plan_direct(no_alloc), compact ? &cu : nullptr,
+                          [&](uint8_t* h) { pack_plan_head(plan, h); });
 }
 
 // Shared by both swap directions: validates and enqueues block src_ids[i] of
@@ -763,13 +806,23 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     }
     return CW_OK;
   };
-  return stage_and_launch(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
+  // the step's sequences and the extend meta, then the decode meta (in full or
+  // in compact form, rebuilt by the upload kernel)
+  auto head = [&](uint8_t* h) {
     std::fill(h, h + sp.off_ext_meta, uint8_t(0));
     std::copy(reinterpret_cast<const uint8_t*>(sp.seqs.data()),
               reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), h);
     if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, h + sp.off_ext_meta);
+  };
+  CompactUpload cu;
+  const bool compact = !sp.dec.empty() && compact_upload(sp.dec_plan, sp.off_dec_meta, &cu);
+  return stage_and_launch(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
+    head(h);
     if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, h + sp.off_dec_meta);
-  }, launch, false, plan_direct(false));
+  }, launch, false, plan_direct(false), compact ? &cu : nullptr, [&](uint8_t* h) {
+    head(h);
+    pack_plan_head(sp.dec_plan, h + sp.off_dec_meta);
+  });
 }
 
 // Runs an entry point's body: a failed host allocation (or any other C++
@@ -1102,6 +1155,9 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
       if (value < 1 || value > 10000) return fail(CW_ERR_UNSUPPORTED, "suffix weight %d is not in 1 .. 10000", value);
       g_tuning.suffix_weight = value;
       return CW_OK;
+    case CW_TUNE_COMPACT_DECODE:
+      g_tuning.compact_decode = value;
+      return CW_OK;
     default: break;
   }
   return fail(CW_ERR_UNSUPPORTED, "unknown tuning key %d", int(key));
@@ -1133,6 +1189,41 @@ int64_t cw_extend_plan_items(const int32_t* prefix_lens_h, const int32_t* suffix
         o[4] = w.kv_end; o[5] = w.part; o[6] = w.rows; o[7] = 0;
       }
     }
+    return n;
+  });
+}
+
+int64_t cw_decode_plan_items(const int32_t* prefix_lens_h, int32_t num_seqs, int32_t num_kv_heads,
+                             int32_t gqa_group, int32_t head_dim, int32_t page_size,
+                             cw_kv_dtype_t kv_dtype, int32_t rebuilt, int32_t* items_out,
+                             int64_t items_capacity, int32_t* groups_out, int64_t groups_capacity,
+                             int64_t* num_groups) {
+  return guarded_value<int64_t>(-1, [&]() -> int64_t {
+    if (check_shape(num_seqs, num_kv_heads, gqa_group, head_dim, page_size) != CW_OK) return -1;
+    if (kv_dtype != CW_KV_BF16 && kv_dtype != CW_KV_FP8_E4M3FN) return -1;
+    if (!prefix_lens_h && num_seqs > 0) return -1;
+    std::vector<int32_t> ones(size_t(std::max(num_seqs, 0)), 1);
+    if (check_lens(prefix_lens_h, ones.data(), num_seqs, 0, page_size, num_kv_heads, gqa_group, head_dim,
+                   false) != CW_OK)
+      return -1;
+    const ExtendPlan plan =
+        make_decode_plan(prefix_lens_h, num_seqs, num_kv_heads, gqa_group, head_dim, page_size, kv_dtype);
+    if (rebuilt && (!plan.compact || plan.recs.empty())) return -1;
+    const int64_t n = static_cast<int64_t>(plan.items.size()), ng = static_cast<int64_t>(plan.groups.size());
+    for (int64_t i = 0; items_out && i < std::min(n, items_capacity); ++i) {
+      const WorkItem w = rebuilt ? expand_item(plan.recs.data(), plan.tails.data(), plan.desc, int32_t(i))
+                                 : plan.items[i];
+      int32_t* o = items_out + 8 * i;
+      o[0] = w.seq; o[1] = w.kvh; o[2] = w.q_row0; o[3] = w.kv_begin;
+      o[4] = w.kv_end; o[5] = w.part; o[6] = w.rows; o[7] = w.pad;
+    }
+    for (int64_t g = 0; groups_out && g < std::min(ng, groups_capacity); ++g) {
+      const CombineGroup c = rebuilt ? expand_group(plan.recs.data(), plan.desc, int32_t(g)) : plan.groups[g];
+      int32_t* o = groups_out + 8 * g;
+      o[0] = c.seq; o[1] = c.kvh; o[2] = c.q_row0; o[3] = c.rows;
+      o[4] = c.part0; o[5] = c.n_parts; o[6] = c.pad0; o[7] = c.pad1;
+    }
+    if (num_groups) *num_groups = ng;
     return n;
   });
 }

@@ -9,6 +9,7 @@
 #include <cstring>
 
 #include "../cw_internal.h"
+#include "../plan_expand.h"
 
 namespace cw {
 namespace {
@@ -41,7 +42,44 @@ __global__ __launch_bounds__(kThreads) void arg_copy_kernel(ArgChunk a) {
   for (uint32_t i = threadIdx.x; i < a.words; i += kThreads) a.dst[i] = a.data[i];
 }
 
+// Upload of a compact plan blob: the first `verbatim` bytes are copied as they
+// are (16 bytes per lane), then every workgroup reads the decode records and
+// the tail order into LDS and rebuilds its share of the work items and merge
+// groups (expand_item / expand_group, the functions the host checks them with).
+__global__ __launch_bounds__(kThreads) void plan_expand_kernel(const uint8_t* src, uint8_t* dst,
+                                                              int64_t verbatim, ExpandDesc d) {
+  __shared__ DecodeRec rec[kMaxExpandSeqs];
+  __shared__ int32_t tails[kMaxExpandSeqs];
+  const int64_t stride = int64_t(gridDim.x) * kThreads;
+  const int64_t first = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  const int64_t n16 = verbatim / 16;
+  for (int64_t i = first; i < n16; i += stride)
+    reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
+  const DecodeRec* rs = reinterpret_cast<const DecodeRec*>(src + d.rec_off);
+  const int32_t* ts = reinterpret_cast<const int32_t*>(src + d.tail_off);
+  for (int32_t i = threadIdx.x; i < d.n_seqs; i += kThreads) rec[i] = rs[i];
+  for (int32_t i = threadIdx.x; i < d.n_tails; i += kThreads) tails[i] = ts[i];
+  __syncthreads();
+  WorkItem* items = reinterpret_cast<WorkItem*>(dst + d.items_off);
+  CombineGroup* groups = reinterpret_cast<CombineGroup*>(dst + d.groups_off);
+  for (int64_t i = first; i < d.n_items + d.n_groups; i += stride) {
+    if (i < d.n_items) items[i] = expand_item(rec, tails, d, static_cast<int32_t>(i));
+    else groups[i - d.n_items] = expand_group(rec, d, static_cast<int32_t>(i - d.n_items));
+  }
+}
+
 }  // namespace
+
+hipError_t launch_plan_expand(const void* src, void* dst, size_t verbatim, const ExpandDesc& d,
+                              hipStream_t stream) {
+  if (d.n_seqs < 1 || d.n_seqs > kMaxExpandSeqs || d.n_tails > d.n_seqs || verbatim % 16 != 0)
+    return hipErrorInvalidValue;
+  const int64_t work = std::max<int64_t>(int64_t(verbatim / 16), int64_t(d.n_items) + d.n_groups);
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((work + kThreads - 1) / kThreads, 1024));
+  hipLaunchKernelGGL(plan_expand_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream,
+                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), int64_t(verbatim), d);
+  return hipGetLastError();
+}
 
 hipError_t launch_arg_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
   const uint8_t* s = static_cast<const uint8_t*>(src);

@@ -319,7 +319,47 @@ ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32
   });
   plan.items.insert(plan.items.end(), tails.begin(), tails.end());
   layout_workspace(plan, head_dim);
+
+  // the compact form: one record per sequence, the order of the last chunks
+  plan.compact = true;
+  plan.recs.resize(num_seqs);
+  int32_t full_off = 0, part_off = 0, group_off = 0;
+  std::vector<std::pair<int64_t, int32_t>> tail_len;  // (length, sequence)
+  for (int32_t b = 0; b < num_seqs; ++b) {
+    const int64_t n = int64_t(prefix_lens[b]) + 1;
+    const int32_t nc = static_cast<int32_t>((n + chunk - 1) / chunk);
+    const int32_t full = n % chunk == 0 ? nc : nc - 1;
+    plan.recs[b] = DecodeRec{full_off, full, nc, static_cast<int32_t>(n), part_off, group_off};
+    full_off += full * num_kv_heads;
+    if (nc > 1) {
+      part_off += nc * num_kv_heads;
+      group_off += num_kv_heads;
+    }
+    if (full < nc) tail_len.emplace_back(n - int64_t(full) * chunk, b);
+  }
+  std::stable_sort(tail_len.begin(), tail_len.end(),
+                   [](const std::pair<int64_t, int32_t>& a, const std::pair<int64_t, int32_t>& c) {
+                     return a.first > c.first;
+                   });
+  for (const auto& t : tail_len) plan.tails.push_back(t.second);
+  ExpandDesc& d = plan.desc;
+  d.n_seqs = num_seqs;
+  d.n_full = full_off;
+  d.n_items = static_cast<int32_t>(plan.items.size());
+  d.n_groups = static_cast<int32_t>(plan.groups.size());
+  d.n_tails = static_cast<int32_t>(plan.tails.size());
+  d.chunk = static_cast<int32_t>(chunk);
+  d.hkv = num_kv_heads;
+  d.rows = gqa_group;
+  d.items_off = static_cast<uint32_t>(plan.off_items);
+  d.groups_off = static_cast<uint32_t>(plan.off_groups);
   return plan;
+}
+
+void pack_plan_head(const ExtendPlan& plan, uint8_t* dst) {
+  std::fill(dst, dst + plan.off_items, uint8_t(0));
+  std::copy(reinterpret_cast<const uint8_t*>(plan.seqs.data()),
+            reinterpret_cast<const uint8_t*>(plan.seqs.data() + plan.seqs.size()), dst + plan.off_seqs);
 }
 
 void pack_plan_meta(const ExtendPlan& plan, uint8_t* dst) {

@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "cw_internal.h"
+#include "plan_expand.h"
 
 namespace cw {
 
@@ -17,6 +18,7 @@ struct Tuning {
   int32_t deal_rounds = 1;     // 1 = deal bundles of whole GPU rounds across XCDs, 0 = keep them on one
   int32_t plan_direct = 0;     // 1 = kernels read the plan from the pinned staging slot, 0 = copy it first
   int32_t suffix_weight = 125; // split-K cost of a key tile past the prefix, in percent of a prefix tile
+  int32_t compact_decode = 1;  // 1 = decode plans are uploaded in compact form
 };
 
 struct ExtendPlan {
@@ -29,6 +31,11 @@ struct ExtendPlan {
   size_t meta_bytes = 0;  // seqs + items + groups: the part uploaded per call
   size_t total_bytes = 0;
   int32_t part_rows = 0;  // rows per partial slot
+  // decode plans: the same items and groups in compact form (see plan_expand.h)
+  bool compact = false;
+  std::vector<DecodeRec> recs;
+  std::vector<int32_t> tails;
+  ExpandDesc desc{};  // offsets relative to the plan's own meta
 };
 
 // Builds the plan for a kernel whose workgroups own `block_m` rows and of
@@ -52,5 +59,7 @@ ExtendPlan build_decode_plan(const int32_t* prefix_lens, int32_t num_seqs, int32
 
 // Serialises seqs, items and groups into `dst` (meta_bytes long) at their offsets.
 void pack_plan_meta(const ExtendPlan& plan, uint8_t* dst);
+// Only the meta's first off_items bytes (the sequences).
+void pack_plan_head(const ExtendPlan& plan, uint8_t* dst);
 
 }  // namespace cw

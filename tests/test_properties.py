@@ -3,6 +3,8 @@
 - The extend planner: for any lengths, head counts and tunings, every
   (sequence, kv head, query tile) key range is covered exactly once, partial
   slots are unique and consecutive per tile, and idle items carry no work.
+- The decode plan: rebuilt from its compact form (what the upload kernel does
+  on the device), it is exactly the planner's work list and merge groups.
 - The policy: the library's simulator and block manager give exactly the
   oracle's block-level model (dispatch order, counters, block counts and cached
   tokens of every dispatch) on small random traces with random shared-prefix
@@ -58,6 +60,47 @@ def test_planner_covers_every_key_range_once(case):
     assert np.all(idle[:, 4] == idle[:, 3])  # no keys
     if len(items):
         assert items[-1, 0] >= 0  # no trailing idle items
+
+
+@st.composite
+def decode_case(draw):
+    b = draw(st.integers(1, 40))
+    lp = draw(st.lists(st.sampled_from([0, 1, 15, 16, 17, 63, 64, 65, 255, 256, 257, 1000, 4095, 4096,
+                                        4097, 20000, 65536, 131071]), min_size=b, max_size=b))
+    hkv = draw(st.sampled_from([1, 2, 8]))
+    g = draw(st.sampled_from([1, 4, 8, 16]))
+    d = draw(st.sampled_from([64, 128]))
+    p = draw(st.sampled_from([16, 64]))
+    dt = draw(st.sampled_from(["bf16", "fp8"]))
+    chunk = draw(st.sampled_from([0, 0, 1, 2, 5, 64]))
+    target = draw(st.sampled_from([0, 0, 16, 1000, 100000]))
+    return lp, hkv, g, d, p, dt, chunk, target
+
+
+@SETTINGS
+@given(decode_case())
+def test_decode_plan_rebuilt_from_compact_form_is_the_plan(case):
+    """The upload kernel's rebuild of a decode plan from its compact form (the
+    same function, run on the host) gives exactly the planner's items and merge
+    groups, for any lengths, head counts, tile shapes and tunings."""
+    lp, hkv, g, d, p, dt, chunk, target = case
+    cwlib.set_tuning(0, chunk)
+    cwlib.set_tuning(1, target)
+    try:
+        items, groups = cwlib.decode_plan(lp, hkv, g, d, p, dt, rebuilt=False)
+        r_items, r_groups = cwlib.decode_plan(lp, hkv, g, d, p, dt, rebuilt=True)
+    finally:
+        cwlib.set_tuning(0, 0)
+        cwlib.set_tuning(1, 0)
+    assert np.array_equal(items, r_items)
+    assert np.array_equal(groups, r_groups)
+    # and the plan covers every (sequence, kv head) key range [0, Lp + 1) once
+    for b in range(len(lp)):
+        for h in range(hkv):
+            rows = items[(items[:, 0] == b) & (items[:, 1] == h)]
+            spans = sorted((int(x[3]), int(x[4])) for x in rows)
+            assert spans[0][0] == 0 and spans[-1][1] == lp[b] + 1
+            assert all(spans[i][1] == spans[i + 1][0] for i in range(len(spans) - 1))
 
 
 B = 4  # block tokens of the random traces
