@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -12,6 +13,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "../../include/cw.h"
@@ -74,6 +76,10 @@ constexpr int kStagingSlots = 8;
 // Every staging slot has this fixed size, allocated once per device (cw_init or
 // the first call that uploads a plan); a plan larger than a slot is rejected.
 constexpr size_t kStagingSlotBytes = size_t(4) << 20;
+// The last bytes of a slot are the words its upload kernel's workgroups write
+// once they have read the slot (one per workgroup); the plan gets the rest.
+constexpr size_t kDoneBytes = size_t(kMaxUploadWorkgroups) * sizeof(uint32_t);
+constexpr size_t kPlanSlotBytes = kStagingSlotBytes - kDoneBytes;
 // A call captured into a graph carries its plan in kernel arguments (2 KiB per
 // copy launch); its plan may take at most this many bytes.
 constexpr size_t kCaptureMaxBytes = size_t(256) << 10;
@@ -82,7 +88,10 @@ struct StagingSlot {
   void* host = nullptr;
   void* dev = nullptr;  // the same pinned memory as the device addresses it
   hipEvent_t ev = nullptr;
-  bool pending = false;
+  bool pending = false;        // `ev` recorded behind kernels that read the slot (direct mode)
+  bool reads_pending = false;  // an upload kernel reads the slot: wait for its done words
+  uint32_t seq = 0;            // the value its workgroups write
+  int32_t workgroups = 0;
 };
 
 struct DeviceState {
@@ -94,6 +103,7 @@ struct DeviceState {
   StagingSlot slots[kStagingSlots];
   int next_slot = 0;
   uint8_t* capture_buf = nullptr;  // kCaptureMaxBytes of host memory: plans of captured calls
+  uint32_t upload_seq = 0;         // the last value handed to an upload kernel
   uint8_t* scratch = nullptr;  // this device's copy of the static scratch array (cw_init)
 };
 
@@ -228,16 +238,49 @@ bool compact_upload(const ExtendPlan& plan, size_t at, CompactUpload* cu) {
   return true;
 }
 
+// Waits until every workgroup of the upload kernel that last read `s` has
+// reported its reads (the done words at the slot's end).  The host runs up to
+// kStagingSlots calls ahead of the device, so this waits for the device to
+// reach an upload issued that many calls ago.  If the words have not all
+// arrived after two seconds (calls of hundreds of milliseconds each, or an
+// upload that never ran), the device is synchronised once, which also surfaces
+// a fault, and they are checked again.
+cw_status_t wait_slot_reads(StagingSlot& s) {
+  if (!s.reads_pending) return CW_OK;
+  const volatile uint32_t* done =
+      reinterpret_cast<const volatile uint32_t*>(static_cast<uint8_t*>(s.host) + kPlanSlotBytes);
+  auto all_read = [&]() {
+    for (int32_t w = 0; w < s.workgroups; ++w)
+      if (done[w] != s.seq) return false;
+    return true;
+  };
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint32_t spin = 1; !all_read(); ++spin) {
+    if ((spin & 1023u) == 0) {
+      if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) {
+        const hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize while waiting for a staging slot");
+        if (!all_read()) return fail(CW_ERR_HIP, "the upload kernel of a staging slot never reported its reads");
+        break;
+      }
+      std::this_thread::yield();
+    }
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
+  s.reads_pending = false;
+  return CW_OK;
+}
+
 template <class Fill, class Launch, class FillHead>
 cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
                              Launch&& launch, bool no_alloc, bool direct,
                              const CompactUpload* compact, FillHead&& fill_head) {
   if (bytes == 0) return launch(static_cast<const uint8_t*>(dst));
-  if (bytes > kStagingSlotBytes)
+  if (bytes > kPlanSlotBytes)
     return fail(CW_ERR_UNSUPPORTED,
                 "the call's plan takes %zu bytes, more than the %zu-byte staging slot "
                 "(too many sequences or work items for one call)",
-                bytes, kStagingSlotBytes);
+                bytes, kPlanSlotBytes);
   hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
   hipError_t ce = hipStreamIsCapturing(stream, &capture);
   if (ce != hipSuccess) return hip_fail(ce, "hipStreamIsCapturing");
@@ -270,8 +313,10 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
     s.pending = false;
   }
+  s0 = wait_slot_reads(s);
+  if (s0 != CW_OK) return s0;
   const bool use_compact = compact != nullptr && compact->plan != nullptr && !direct &&
-                           compact->bytes <= kStagingSlotBytes && compact->bytes < bytes;
+                           compact->bytes <= kPlanSlotBytes && compact->bytes < bytes;
   uint8_t* h = static_cast<uint8_t*>(s.host);
   if (use_compact) {
     const ExtendPlan& cp = *compact->plan;
@@ -281,19 +326,27 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
   } else {
     fill(h);
   }
-  cw_status_t launched = CW_OK;
   if (direct) {
-    launched = launch(static_cast<const uint8_t*>(s.dev));
-  } else {
-    e = use_compact ? launch_plan_expand(s.dev, dst, compact->verbatim, compact->desc, stream)
-                    : launch_stage_copy(s.dev, dst, bytes, stream);
-    if (e != hipSuccess) return hip_fail(e, "plan upload kernel launch");
+    const cw_status_t launched = launch(static_cast<const uint8_t*>(s.dev));
+    // recorded even when a launch failed: whatever was enqueued may read the slot
+    e = hipEventRecord(s.ev, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    s.pending = true;
+    return launched;
   }
-  // recorded even when a launch failed: whatever was enqueued may read the slot
-  e = hipEventRecord(s.ev, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-  s.pending = true;
-  if (direct) return launched;
+  // copy mode: only the upload kernel reads the slot, and it reports its reads
+  // itself (no event in the stream: a marker between two kernels costs ~4 us)
+  uint32_t* done = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(s.dev) + kPlanSlotBytes);
+  st.upload_seq = st.upload_seq == 0xFFFFFFFFu ? 1u : st.upload_seq + 1u;
+  std::memset(static_cast<uint8_t*>(s.host) + kPlanSlotBytes, 0, kDoneBytes);
+  int32_t workgroups = 0;
+  e = use_compact
+          ? launch_plan_expand(s.dev, dst, compact->verbatim, compact->desc, stream, done, st.upload_seq, &workgroups)
+          : launch_stage_copy(s.dev, dst, bytes, stream, done, st.upload_seq, &workgroups);
+  if (e != hipSuccess) return hip_fail(e, "plan upload kernel launch");
+  s.seq = st.upload_seq;
+  s.workgroups = workgroups;
+  s.reads_pending = true;
   return launch(static_cast<const uint8_t*>(dst));
 }
 

@@ -130,8 +130,12 @@ hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size,
                               hipStream_t stream);
 hipError_t launch_swap(const SwapParams& p, hipStream_t stream);
 // Copies `bytes` from device-visible pinned host memory to device memory on
-// `stream` with a kernel (the plan upload).
-hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+// `stream` with a kernel (the plan upload).  With `done` (device address of
+// pinned host words), each of its *workgroups (at most kMaxUploadWorkgroups)
+// writes `seq` into done[its index] once it has read its share.
+constexpr int32_t kMaxUploadWorkgroups = 1024;
+hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream,
+                             uint32_t* done = nullptr, uint32_t seq = 0, int32_t* workgroups = nullptr);
 // Plan bytes carried in kernel arguments, kArgChunkBytes per launch (bytes a
 // multiple of 4; for calls captured into a graph).
 constexpr size_t kArgChunkBytes = 2048;

@@ -18,14 +18,25 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 
+// Once a workgroup has read its share of the slot it writes `seq` into its
+// word of `done` (pinned host memory, a system-scope store), so the host knows
+// when the slot may be refilled without an event in the stream.
+__device__ __forceinline__ void report_read(uint32_t* done, uint32_t seq) {
+  __syncthreads();  // every lane's reads of the slot have returned
+  if (done != nullptr && threadIdx.x == 0)
+    __hip_atomic_store(done + blockIdx.x, seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 __global__ __launch_bounds__(kThreads) void stage_copy_kernel(const uint8_t* src, uint8_t* dst,
-                                                              int64_t bytes) {
+                                                              int64_t bytes, uint32_t* done,
+                                                              uint32_t seq) {
   const int64_t n16 = bytes / 16;
   const int64_t stride = int64_t(gridDim.x) * kThreads;
   const int64_t first = int64_t(blockIdx.x) * kThreads + threadIdx.x;
   for (int64_t i = first; i < n16; i += stride)
     reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
   if (first < bytes - n16 * 16) dst[n16 * 16 + first] = src[n16 * 16 + first];
+  report_read(done, seq);
 }
 
 // Plan upload under stream capture: the bytes travel in the kernel's own
@@ -47,7 +58,8 @@ __global__ __launch_bounds__(kThreads) void arg_copy_kernel(ArgChunk a) {
 // the tail order into LDS and rebuilds its share of the work items and merge
 // groups (expand_item / expand_group, the functions the host checks them with).
 __global__ __launch_bounds__(kThreads) void plan_expand_kernel(const uint8_t* src, uint8_t* dst,
-                                                              int64_t verbatim, ExpandDesc d) {
+                                                              int64_t verbatim, ExpandDesc d,
+                                                              uint32_t* done, uint32_t seq) {
   __shared__ DecodeRec rec[kMaxExpandSeqs];
   __shared__ int32_t tails[kMaxExpandSeqs];
   const int64_t stride = int64_t(gridDim.x) * kThreads;
@@ -59,7 +71,7 @@ __global__ __launch_bounds__(kThreads) void plan_expand_kernel(const uint8_t* sr
   const int32_t* ts = reinterpret_cast<const int32_t*>(src + d.tail_off);
   for (int32_t i = threadIdx.x; i < d.n_seqs; i += kThreads) rec[i] = rs[i];
   for (int32_t i = threadIdx.x; i < d.n_tails; i += kThreads) tails[i] = ts[i];
-  __syncthreads();
+  report_read(done, seq);  // the slot is read; the rest works from LDS
   WorkItem* items = reinterpret_cast<WorkItem*>(dst + d.items_off);
   CombineGroup* groups = reinterpret_cast<CombineGroup*>(dst + d.groups_off);
   for (int64_t i = first; i < d.n_items + d.n_groups; i += stride) {
@@ -71,13 +83,16 @@ __global__ __launch_bounds__(kThreads) void plan_expand_kernel(const uint8_t* sr
 }  // namespace
 
 hipError_t launch_plan_expand(const void* src, void* dst, size_t verbatim, const ExpandDesc& d,
-                              hipStream_t stream) {
+                              hipStream_t stream, uint32_t* done, uint32_t seq, int32_t* workgroups) {
   if (d.n_seqs < 1 || d.n_seqs > kMaxExpandSeqs || d.n_tails > d.n_seqs || verbatim % 16 != 0)
     return hipErrorInvalidValue;
   const int64_t work = std::max<int64_t>(int64_t(verbatim / 16), int64_t(d.n_items) + d.n_groups);
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((work + kThreads - 1) / kThreads, 1024));
+  const int64_t blocks =
+      std::max<int64_t>(1, std::min<int64_t>((work + kThreads - 1) / kThreads, kMaxUploadWorkgroups));
+  *workgroups = static_cast<int32_t>(blocks);
   hipLaunchKernelGGL(plan_expand_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream,
-                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), int64_t(verbatim), d);
+                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), int64_t(verbatim), d,
+                     done, seq);
   return hipGetLastError();
 }
 
@@ -97,12 +112,14 @@ hipError_t launch_arg_copy(const void* src, void* dst, size_t bytes, hipStream_t
   return hipSuccess;
 }
 
-hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
-  if (bytes == 0) return hipSuccess;
+hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t stream, uint32_t* done,
+                             uint32_t seq, int32_t* workgroups) {
   const int64_t n16 = int64_t(bytes / 16);
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n16 + kThreads - 1) / kThreads, 1024));
+  const int64_t blocks =
+      std::max<int64_t>(1, std::min<int64_t>((n16 + kThreads - 1) / kThreads, kMaxUploadWorkgroups));
+  if (workgroups) *workgroups = static_cast<int32_t>(blocks);
   hipLaunchKernelGGL(stage_copy_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream,
-                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), int64_t(bytes));
+                     static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), int64_t(bytes), done, seq);
   return hipGetLastError();
 }
 

@@ -106,7 +106,8 @@ __host__ __device__ inline CombineGroup expand_group(const DecodeRec* rec, const
 // Upload of a plan blob: its first `verbatim` bytes are copied as they are,
 // then the decode plan of `d` is rebuilt into dst (d.n_seqs <= kMaxExpandSeqs).
 constexpr int32_t kMaxExpandSeqs = 2048;
+// Its workgroups report their reads as launch_stage_copy's do.
 hipError_t launch_plan_expand(const void* src, void* dst, size_t verbatim, const ExpandDesc& d,
-                              hipStream_t stream);
+                              hipStream_t stream, uint32_t* done, uint32_t seq, int32_t* workgroups);
 
 }  // namespace cw
