@@ -107,3 +107,28 @@ def test_decode_full_size(name):
     tol = BF16_MAX_ABS if s.kv_dtype == "bf16" else FP8_MAX_ABS
     assert_close(as_f64(out), ref, tol, BF16_MEAN_ABS if s.kv_dtype == "bf16" else None, f"full {name}")
     assert_close(lse.cpu().double().numpy(), ref_lse, 1e-2, None, f"full {name} lse")
+
+
+@pytest.mark.parametrize("n_seqs", [2048, 2049])
+def test_decode_plan_upload_forms(n_seqs):
+    """Decode plans are uploaded in compact form (rebuilt on the device) up to
+    2048 sequences and as full work lists beyond: both against the oracle, and
+    the compact upload switched off (CW_TUNE_COMPACT_DECODE 0) bit-identical."""
+    rng = np.random.default_rng(n_seqs)
+    lp = [int(x) for x in rng.integers(0, 200, size=n_seqs)]
+    spec = cw.custom_spec(lp, [1] * n_seqs, num_kv_heads=2, gqa_group=4, head_dim=64, page_size=16,
+                          kv_dtype="bf16", seed=n_seqs)
+    print(f"\n[case] decode plan upload: {n_seqs} sequences", flush=True)
+    w = cw.materialize(spec)
+    dw = to_gpu(w)
+    out, lse = _run_decode(dw)
+    cwlib.set_tuning(6, 0)
+    try:
+        out_full, lse_full = _run_decode(dw)
+    finally:
+        cwlib.set_tuning(6, 1)
+    assert torch.equal(out.view(torch.int16), out_full.view(torch.int16))
+    assert torch.equal(lse, lse_full)
+    ref, ref_lse = oracle.extend_attention_rowwise(paged_inputs(w))
+    assert_close(as_f64(out), ref, BF16_MAX_ABS, BF16_MEAN_ABS, f"{n_seqs} sequences")
+    assert_close(lse.cpu().double().numpy(), ref_lse, 1e-2, None, f"{n_seqs} sequences lse")
