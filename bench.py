@@ -73,6 +73,9 @@ def parse():
     ap.add_argument("--compact-decode", type=int, default=1, choices=[0, 1],
                     help="1 (default): decode plans are uploaded in compact form and rebuilt on "
                          "the device; 0: their work items are uploaded as they are")
+    ap.add_argument("--arg-plans", type=int, default=1, choices=[0, 1],
+                    help="1 (default): extend plans of up to 16 KB travel in the kernel arguments; "
+                         "0: they are uploaded by a copy kernel")
     ap.add_argument("--suffix-weight", type=int, default=None,
                     help="split-K cost of a key tile past the cached prefix, percent of a prefix tile "
                          "(default: the library's)")
@@ -626,6 +629,7 @@ def main():
     cwlib.set_tuning(cwlib._lib.CW_TUNE_DEAL_ROUNDS, args.deal_rounds)
     cwlib.set_tuning(cwlib._lib.CW_TUNE_PLAN_DIRECT, args.plan_direct)
     cwlib.set_tuning(cwlib._lib.CW_TUNE_COMPACT_DECODE, args.compact_decode)
+    cwlib.set_tuning(cwlib._lib.CW_TUNE_ARG_PLANS, args.arg_plans)
     if args.suffix_weight is not None:
         cwlib.set_tuning(cwlib._lib.CW_TUNE_SUFFIX_WEIGHT, args.suffix_weight)
     res = run_workload(args.workload, args.steps, args.warmup, separate=args.separate_calls,

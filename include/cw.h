@@ -325,6 +325,11 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           the upload kernel (the default; up to 2048
  *                           sequences, beyond that as 0); 0 = its work items
  *                           are uploaded as they are.  Larger values act as 1.
+ *   CW_TUNE_ARG_PLANS       1 = an extend plan of up to 16 KB (of an extend
+ *                           call, or of a step without decodes) travels in the
+ *                           kernel arguments of the extend and merge kernels,
+ *                           with no upload kernel (the default); 0 = it is
+ *                           uploaded like larger plans.  Larger values act as 1.
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {
   CW_TUNE_KV_CHUNK_TILES = 0,
@@ -334,6 +339,7 @@ typedef enum {
   CW_TUNE_PLAN_DIRECT = 4,
   CW_TUNE_SUFFIX_WEIGHT = 5,
   CW_TUNE_COMPACT_DECODE = 6,
+  CW_TUNE_ARG_PLANS = 7,
   CW_TUNE_RANGE_MIN_ = -2147483647 - 1,
   CW_TUNE_RANGE_MAX_ = 2147483647
 } cw_tune_key_t;

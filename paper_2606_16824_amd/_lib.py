@@ -14,7 +14,7 @@ LIB_PATH = os.environ.get("CW_LIBRARY") or os.path.join(
  CW_ERR_ALIAS, CW_ERR_INIT) = range(9)
 CW_KV_BF16, CW_KV_FP8_E4M3FN = 0, 1
 CW_TUNE_KV_CHUNK_TILES, CW_TUNE_TARGET_WGS, CW_TUNE_EXTEND_KERNEL, CW_TUNE_DEAL_ROUNDS, CW_TUNE_PLAN_DIRECT, CW_TUNE_SUFFIX_WEIGHT = 0, 1, 2, 3, 4, 5
-CW_TUNE_COMPACT_DECODE = 6
+CW_TUNE_COMPACT_DECODE, CW_TUNE_ARG_PLANS = 6, 7
 CW_CEILING_LOW_ENTROPY, CW_CEILING_RANDOM = 0, 1
 
 _i32p = C.POINTER(C.c_int32)

@@ -63,9 +63,9 @@ Tuning current_tuning() {
 // one (64 rows per wave, bf16 pools only) is asked for.  Both own LDS_BLOCK_M
 // rows per work item, so they share the plan.
 hipError_t launch_extend(const ExtendParams& p, int head_dim, int page_size, bool fp8,
-                         hipStream_t stream) {
-  if (!fp8 && current_tuning().extend_kernel == 2) return launch_extend_w64(p, head_dim, page_size, stream);
-  return launch_extend_lds(p, head_dim, page_size, fp8, stream);
+                         hipStream_t stream, const ArgPlan* ap) {
+  if (!fp8 && current_tuning().extend_kernel == 2) return launch_extend_w64(p, head_dim, page_size, stream, ap);
+  return launch_extend_lds(p, head_dim, page_size, fp8, stream, ap);
 }
 
 // ---------------------------------------------------------------------------
@@ -274,8 +274,15 @@ cw_status_t wait_slot_reads(StagingSlot& s) {
 template <class Fill, class Launch, class FillHead>
 cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&& fill,
                              Launch&& launch, bool no_alloc, bool direct,
-                             const CompactUpload* compact, FillHead&& fill_head) {
-  if (bytes == 0) return launch(static_cast<const uint8_t*>(dst));
+                             const CompactUpload* compact, FillHead&& fill_head, bool arg_plan = false) {
+  if (bytes == 0) return launch(static_cast<const uint8_t*>(dst), nullptr);
+  if (arg_plan && !direct && bytes <= kArgPlanBytes) {
+    // the plan travels in the kernel arguments: no slot, no upload kernel (and
+    // a captured launch keeps it by value)
+    ArgPlan ap;
+    fill(ap.bytes);
+    return launch(nullptr, &ap);
+  }
   if (bytes > kPlanSlotBytes)
     return fail(CW_ERR_UNSUPPORTED,
                 "the call's plan takes %zu bytes, more than the %zu-byte staging slot "
@@ -298,7 +305,7 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
     fill(st.capture_buf);
     ce = launch_arg_copy(st.capture_buf, dst, bytes, stream);
     if (ce != hipSuccess) return hip_fail(ce, "plan upload kernel launch");
-    return launch(static_cast<const uint8_t*>(dst));
+    return launch(static_cast<const uint8_t*>(dst), nullptr);
   }
   if (!st.ready) {
     if (no_alloc) return fail(CW_ERR_INIT, "cw_init() has not been called on this device");
@@ -327,7 +334,7 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
     fill(h);
   }
   if (direct) {
-    const cw_status_t launched = launch(static_cast<const uint8_t*>(s.dev));
+    const cw_status_t launched = launch(static_cast<const uint8_t*>(s.dev), nullptr);
     // recorded even when a launch failed: whatever was enqueued may read the slot
     e = hipEventRecord(s.ev, stream);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -347,18 +354,21 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
   s.seq = st.upload_seq;
   s.workgroups = workgroups;
   s.reads_pending = true;
-  return launch(static_cast<const uint8_t*>(dst));
+  return launch(static_cast<const uint8_t*>(dst), nullptr);
 }
 
 template <class Fill>
 cw_status_t upload_fill(size_t bytes, void* dst, hipStream_t stream, Fill&& fill) {
-  return stage_and_launch(bytes, dst, stream, fill, [](const uint8_t*) { return CW_OK; }, false, false,
-                          nullptr, fill);
+  return stage_and_launch(bytes, dst, stream, fill, [](const uint8_t*, const ArgPlan*) { return CW_OK; },
+                          false, false, nullptr, fill);
 }
 
 cw_status_t upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
   return upload_fill(bytes, dst, stream, [&](uint8_t* h) { std::memcpy(h, src, bytes); });
 }
+
+// Whether a small extend plan travels in the kernel arguments (CW_TUNE_ARG_PLANS).
+bool arg_plans() { return current_tuning().arg_plans != 0; }
 
 // Whether a call's plan is read by its kernels straight from the staging slot
 // (CW_TUNE_PLAN_DIRECT).
@@ -550,9 +560,11 @@ StepPlan make_step_plan(const int32_t* lp, const int32_t* ls, int32_t num_seqs, 
 // sit at ws + part.
 ExtendParams plan_params(const ExtendPlan& plan, const uint8_t* meta, uint8_t* ws, size_t part) {
   ExtendParams p{};
-  p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
-  p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
-  p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
+  if (meta != nullptr) {
+    p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
+    p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
+    p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
+  }
   p.part_o = reinterpret_cast<uint16_t*>(ws + part + (plan.off_part_o - plan.meta_bytes));
   p.part_ml = reinterpret_cast<float*>(ws + part + (plan.off_part_ml - plan.meta_bytes));
   p.n_items = static_cast<int32_t>(plan.items.size());
@@ -645,21 +657,31 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     ev1 = g_ev_stop;
   }
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
-  auto launch = [&](const uint8_t* meta) -> cw_status_t {
-    p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
-    p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
-    p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
+  auto launch = [&](const uint8_t* meta, const ArgPlan* ap) -> cw_status_t {
+    if (ap != nullptr) {  // the plan is in the kernel arguments (extends only)
+      p.seqs = nullptr;
+      p.items = nullptr;
+      p.groups = nullptr;
+      p.ap_seqs = static_cast<int32_t>(plan.off_seqs);
+      p.ap_items = static_cast<int32_t>(plan.off_items);
+      p.ap_groups = static_cast<int32_t>(plan.off_groups);
+      p.ap_wseqs = static_cast<int32_t>(plan.off_seqs);
+    } else {
+      p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
+      p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
+      p.groups = reinterpret_cast<const CombineGroup*>(meta + plan.off_groups);
+    }
     if (write_pages) p.w.seqs = p.seqs;
     hipError_t e = hipSuccess;
     if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
-    else e = launch_extend(p, head_dim, page_size, fp8, stream);
+    else e = launch_extend(p, head_dim, page_size, fp8, stream, ap);
     if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
     if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     if (p.n_groups > 0) {
       int max_parts = 0;
       for (const CombineGroup& g : plan.groups) max_parts = std::max(max_parts, g.n_parts);
-      e = launch_combine(p, head_dim, max_parts, stream);
+      e = launch_combine(p, head_dim, max_parts, stream, ap);
       if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
     }
     return CW_OK;
@@ -668,7 +690,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
   const bool compact = decode && compact_upload(plan, 0, &cu);
   return stage_and_launch(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); },
                           launch, no_alloc, plan_direct(no_alloc), compact ? &cu : nullptr,
-                          [&](uint8_t* h) { pack_plan_head(plan, h); });
+                          [&](uint8_t* h) { pack_plan_head(plan, h); }, !decode && arg_plans());
 }
 
 // Shared by both swap directions: validates and enqueues block src_ids[i] of
@@ -818,8 +840,10 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     ev1 = g_ev_stop;
   }
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
-  auto launch = [&](const uint8_t* meta) -> cw_status_t {
-    w.seqs = reinterpret_cast<const SeqInfo*>(meta);
+  auto launch = [&](const uint8_t* meta, const ArgPlan* ap) -> cw_status_t {
+    // with an argument plan (steps without decodes) the step's sequences sit at
+    // its byte 0 and the extend meta at off_ext_meta
+    w.seqs = ap != nullptr ? nullptr : reinterpret_cast<const SeqInfo*>(meta);
     hipError_t e = hipSuccess;
     // the timing events bracket the extend kernel, or the decode kernel of a
     // step without extends
@@ -843,17 +867,27 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
       }
     }
     if (!sp.ext.empty()) {
-      ExtendParams pe = plan_params(sp.ext_plan, meta + sp.off_ext_meta, ws, sp.off_ext_part);
+      ExtendParams pe = plan_params(sp.ext_plan, ap != nullptr ? nullptr : meta + sp.off_ext_meta, ws,
+                                    sp.off_ext_part);
       common(pe);
       pe.w = w;  // every sequence's new K/V, written under the extend's first tiles
+      if (ap != nullptr) {
+        pe.seqs = nullptr;
+        pe.items = nullptr;
+        pe.groups = nullptr;
+        pe.ap_seqs = static_cast<int32_t>(sp.off_ext_meta + sp.ext_plan.off_seqs);
+        pe.ap_items = static_cast<int32_t>(sp.off_ext_meta + sp.ext_plan.off_items);
+        pe.ap_groups = static_cast<int32_t>(sp.off_ext_meta + sp.ext_plan.off_groups);
+        pe.ap_wseqs = 0;
+      }
       if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-      if ((e = launch_extend(pe, head_dim, page_size, fp8, stream)) != hipSuccess)
+      if ((e = launch_extend(pe, head_dim, page_size, fp8, stream, ap)) != hipSuccess)
         return hip_fail(e, "extend kernel launch");
       if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
       if (pe.n_groups > 0) {
         int max_parts = 0;
         for (const CombineGroup& g : sp.ext_plan.groups) max_parts = std::max(max_parts, g.n_parts);
-        if ((e = launch_combine(pe, head_dim, max_parts, stream)) != hipSuccess)
+        if ((e = launch_combine(pe, head_dim, max_parts, stream, ap)) != hipSuccess)
           return hip_fail(e, "combine kernel launch");
       }
     }
@@ -875,7 +909,7 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
   }, launch, false, plan_direct(false), compact ? &cu : nullptr, [&](uint8_t* h) {
     head(h);
     pack_plan_head(sp.dec_plan, h + sp.off_dec_meta);
-  });
+  }, sp.dec.empty() && arg_plans());
 }
 
 // Runs an entry point's body: a failed host allocation (or any other C++
@@ -1210,6 +1244,9 @@ cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
       return CW_OK;
     case CW_TUNE_COMPACT_DECODE:
       g_tuning.compact_decode = value;
+      return CW_OK;
+    case CW_TUNE_ARG_PLANS:
+      g_tuning.arg_plans = value;
       return CW_OK;
     default: break;
   }

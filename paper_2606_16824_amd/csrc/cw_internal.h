@@ -6,6 +6,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 namespace cw {
 
 // Tile shape of the extend kernel: a workgroup of LDS_WAVES wave64s owns
@@ -67,6 +69,25 @@ struct WriteParams {
   int32_t total_tokens;
 };
 
+// A work plan small enough to travel in the kernel arguments: the extend and
+// merge kernels then read it from there, and no upload kernel runs before them
+// (an upload kernel costs ~4 us of the stream's time however small the plan).
+constexpr size_t kArgPlanBytes = 16384;
+struct ArgPlan {
+  uint8_t bytes[kArgPlanBytes];
+};
+struct NoArgPlan {
+  uint8_t unused;
+};
+template <bool AP>
+using PlanArg = typename std::conditional<AP, ArgPlan, NoArgPlan>::type;
+// Pointer to a plan array: at byte `off` of the argument plan, or `dev`.
+template <bool AP, class T>
+__device__ __forceinline__ const T* plan_ptr(const PlanArg<AP>& ap, int32_t off, const T* dev) {
+  if constexpr (AP) return reinterpret_cast<const T*>(ap.bytes + off);
+  else return dev;
+}
+
 struct ExtendParams {
   const void* q;
   const void* k_new;
@@ -91,6 +112,9 @@ struct ExtendParams {
   int32_t n_items;
   int32_t n_groups;
   int32_t part_rows;  // rows per split-K partial slot (the row block for extend, G for decode)
+  // with an argument plan: byte offsets in it of seqs, items, groups and the
+  // page write's seqs (the device pointers above are then unused)
+  int32_t ap_seqs, ap_items, ap_groups, ap_wseqs;
   WriteParams w;      // extend: also scatter the new K/V into the pools when w.total_tokens > 0
 };
 
@@ -118,10 +142,13 @@ struct SwapParams {
 void set_last_error(const char* msg);
 
 // Kernel launchers (each defined in the translation unit of its kernel).
+// `ap`: the plan in the kernel arguments (nullptr: read through p's pointers).
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
-                             hipStream_t stream);
-hipError_t launch_extend_w64(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream);
-hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream);
+                             hipStream_t stream, const ArgPlan* ap = nullptr);
+hipError_t launch_extend_w64(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream,
+                             const ArgPlan* ap = nullptr);
+hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream,
+                          const ArgPlan* ap = nullptr);
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
                          hipStream_t stream);
 int decode_keys_per_tile(int head_dim, bool fp8);

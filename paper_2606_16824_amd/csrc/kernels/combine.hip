@@ -34,8 +34,8 @@ __device__ __forceinline__ void load_part(const uint16_t* base, size_t elem, flo
 // each row's SLICES slices of 32 lanes fold every SLICES-th partial with an
 // online merge, then the slices are merged through LDS (SLICES = 1 for a few
 // partials per row, 8 for many).  Fixed order, no atomics.
-template <int D, int SLICES>
-__global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
+template <int D, int SLICES, bool AP>
+__global__ __launch_bounds__(256) void combine_kernel(ExtendParams p, PlanArg<AP> ap) {
   constexpr int ROWS = 8 / SLICES;
   constexpr int PER = D / 32;  // dims per lane
   __shared__ float sh_o[ROWS][SLICES][D];
@@ -44,7 +44,7 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
   const int grp = blockIdx.x / wg_per_group;
   const int rsub = threadIdx.x / (32 * SLICES);
   const int lr = (blockIdx.x % wg_per_group) * ROWS + rsub;
-  const CombineGroup cg = p.groups[grp];
+  const CombineGroup cg = plan_ptr<AP>(ap, p.ap_groups, p.groups)[grp];
   const bool active = lr < cg.rows;
   const int slice = (threadIdx.x / 32) % SLICES, d0 = (threadIdx.x % 32) * PER;
 
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
       for (int e = 0; e < PER; ++e) out[e] += w * sh_o[rsub][s][d0 + e];
     }
   }
-  const SeqInfo sq = p.seqs[cg.seq];
+  const SeqInfo sq = plan_ptr<AP>(ap, p.ap_seqs, p.seqs)[cg.seq];
   const int G = p.gqa_group, hq = p.num_kv_heads * G;
   const int r = cg.q_row0 + lr;
   const int t = r / G, g = r - t * G;
@@ -162,20 +162,27 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p) {
 
 }  // namespace
 
-hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream) {
+hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream,
+                          const ArgPlan* ap) {
   if (p.n_groups <= 0) return hipSuccess;
   const bool many = max_parts > 4;
   const int rows_per_wg = many ? 1 : 8;
   const dim3 grid(p.n_groups * ((p.part_rows + rows_per_wg - 1) / rows_per_wg));
+#define CW_COMBINE(D_, S_)                                                                           \
+  do {                                                                                               \
+    if (ap) hipLaunchKernelGGL((combine_kernel<D_, S_, true>), grid, dim3(256), 0, stream, p, *ap); \
+    else hipLaunchKernelGGL((combine_kernel<D_, S_, false>), grid, dim3(256), 0, stream, p, NoArgPlan{}); \
+  } while (0)
   if (head_dim == 64) {
-    if (many) hipLaunchKernelGGL((combine_kernel<64, 8>), grid, dim3(256), 0, stream, p);
-    else hipLaunchKernelGGL((combine_kernel<64, 1>), grid, dim3(256), 0, stream, p);
+    if (many) CW_COMBINE(64, 8);
+    else CW_COMBINE(64, 1);
   } else if (head_dim == 128) {
-    if (many) hipLaunchKernelGGL((combine_kernel<128, 8>), grid, dim3(256), 0, stream, p);
-    else hipLaunchKernelGGL((combine_kernel<128, 1>), grid, dim3(256), 0, stream, p);
+    if (many) CW_COMBINE(128, 8);
+    else CW_COMBINE(128, 1);
   } else {
     return hipErrorInvalidValue;
   }
+#undef CW_COMBINE
   return hipGetLastError();
 }
 

@@ -182,9 +182,9 @@ struct LGeo {
   static_assert(NI * RPI == 8, "each wave stages 8 rows of a tile");
 };
 
-template <int D, int P, bool FP8>
+template <int D, int P, bool FP8, bool AP>
 __global__ __launch_bounds__(LDS_THREADS) __attribute__((amdgpu_waves_per_eu(2)))
-void extend_lds_kernel(ExtendParams p) {
+void extend_lds_kernel(ExtendParams p, PlanArg<AP> ap) {
   using T = LGeo<D, P, FP8>;
   // two-stage rings of K and V tiles, each stage its own array so the compiler
   // can tell that reads of one stage never alias the DMA in flight into another
@@ -197,19 +197,21 @@ void extend_lds_kernel(ExtendParams p) {
   // goes to the pools.  The extend never reads a slot at or past a sequence's
   // prefix end from the pool, so the writes and the attention are independent.
   auto fused_write = [&]() __attribute__((always_inline)) {
-    const int64_t total = int64_t(p.w.total_tokens) * p.w.num_kv_heads * (D / 8);
+    WriteParams w = p.w;
+    w.seqs = plan_ptr<AP>(ap, p.ap_wseqs, p.w.seqs);
+    const int64_t total = int64_t(w.total_tokens) * w.num_kv_heads * (D / 8);
     const int64_t per = (total + gridDim.x - 1) / gridDim.x;
     const int64_t end = min(total, int64_t(blockIdx.x + 1) * per);
     for (int64_t idx = int64_t(blockIdx.x) * per + threadIdx.x; idx < end; idx += LDS_THREADS)
-      pw::write_piece<D, P, FP8>(p.w, idx);
+      pw::write_piece<D, P, FP8>(w, idx);
   };
 
-  const WorkItem it = p.items[blockIdx.x];
+  const WorkItem it = plan_ptr<AP>(ap, p.ap_items, p.items)[blockIdx.x];
   if (it.seq < 0) {  // idle padding item (uniform across the workgroup)
     if (p.w.total_tokens > 0) fused_write();
     return;
   }
-  const SeqInfo sq = p.seqs[it.seq];
+  const SeqInfo sq = plan_ptr<AP>(ap, p.ap_seqs, p.seqs)[it.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -806,19 +808,23 @@ void extend_lds_kernel(ExtendParams p) {
 }
 
 template <int D, int P, bool FP8>
-hipError_t launch_t(const ExtendParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((extend_lds_kernel<D, P, FP8>), dim3(p.n_items), dim3(LDS_THREADS), 0, stream, p);
+hipError_t launch_t(const ExtendParams& p, hipStream_t stream, const ArgPlan* ap) {
+  if (ap != nullptr)
+    hipLaunchKernelGGL((extend_lds_kernel<D, P, FP8, true>), dim3(p.n_items), dim3(LDS_THREADS), 0, stream, p, *ap);
+  else
+    hipLaunchKernelGGL((extend_lds_kernel<D, P, FP8, false>), dim3(p.n_items), dim3(LDS_THREADS), 0, stream, p,
+                       NoArgPlan{});
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_extend_lds(const ExtendParams& p, int head_dim, int page_size, bool fp8,
-                             hipStream_t stream) {
+                             hipStream_t stream, const ArgPlan* ap) {
   if (p.n_items <= 0) return hipSuccess;
 #define CW_LDS_CASE(D_, P_)                                                        \
   if (head_dim == D_ && page_size == P_)                                           \
-    return fp8 ? launch_t<D_, P_, true>(p, stream) : launch_t<D_, P_, false>(p, stream);
+    return fp8 ? launch_t<D_, P_, true>(p, stream, ap) : launch_t<D_, P_, false>(p, stream, ap);
   CW_LDS_CASE(64, 16)
   CW_LDS_CASE(64, 64)
   CW_LDS_CASE(128, 16)

@@ -120,9 +120,9 @@ struct WGeo {
   static_assert(BLOCK_N % kTileN == 0, "work items start on a tile");
 };
 
-template <int D, int P>
+template <int D, int P, bool AP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void extend_w64_kernel(ExtendParams p) {
+void extend_w64_kernel(ExtendParams p, PlanArg<AP> ap) {
   using T = WGeo<D, P>;
   // each stage its own array, so the compiler can tell that fragment reads of
   // one stage never alias the DMA in flight into another
@@ -134,19 +134,21 @@ void extend_w64_kernel(ExtendParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds_v2[T::TILE];
 
   auto fused_write = [&]() __attribute__((always_inline)) {
-    const int64_t total = int64_t(p.w.total_tokens) * p.w.num_kv_heads * (D / 8);
+    WriteParams w = p.w;
+    w.seqs = plan_ptr<AP>(ap, p.ap_wseqs, p.w.seqs);
+    const int64_t total = int64_t(w.total_tokens) * w.num_kv_heads * (D / 8);
     const int64_t per = (total + gridDim.x - 1) / gridDim.x;
     const int64_t end = min(total, int64_t(blockIdx.x + 1) * per);
     for (int64_t idx = int64_t(blockIdx.x) * per + threadIdx.x; idx < end; idx += kThreads)
-      pw::write_piece<D, P, false>(p.w, idx);
+      pw::write_piece<D, P, false>(w, idx);
   };
 
-  const WorkItem it = p.items[blockIdx.x];
+  const WorkItem it = plan_ptr<AP>(ap, p.ap_items, p.items)[blockIdx.x];
   if (it.seq < 0) {
     if (p.w.total_tokens > 0) fused_write();
     return;
   }
-  const SeqInfo sq = p.seqs[it.seq];
+  const SeqInfo sq = plan_ptr<AP>(ap, p.ap_seqs, p.seqs)[it.seq];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -654,19 +656,24 @@ void extend_w64_kernel(ExtendParams p) {
 }
 
 template <int D, int P>
-hipError_t launch_t(const ExtendParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((extend_w64_kernel<D, P>), dim3(p.n_items), dim3(kThreads), 0, stream, p);
+hipError_t launch_t(const ExtendParams& p, hipStream_t stream, const ArgPlan* ap) {
+  if (ap != nullptr)
+    hipLaunchKernelGGL((extend_w64_kernel<D, P, true>), dim3(p.n_items), dim3(kThreads), 0, stream, p, *ap);
+  else
+    hipLaunchKernelGGL((extend_w64_kernel<D, P, false>), dim3(p.n_items), dim3(kThreads), 0, stream, p,
+                       NoArgPlan{});
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_extend_w64(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream) {
+hipError_t launch_extend_w64(const ExtendParams& p, int head_dim, int page_size, hipStream_t stream,
+                             const ArgPlan* ap) {
   if (p.n_items <= 0) return hipSuccess;
-  if (head_dim == 64 && page_size == 16) return launch_t<64, 16>(p, stream);
-  if (head_dim == 64 && page_size == 64) return launch_t<64, 64>(p, stream);
-  if (head_dim == 128 && page_size == 16) return launch_t<128, 16>(p, stream);
-  if (head_dim == 128 && page_size == 64) return launch_t<128, 64>(p, stream);
+  if (head_dim == 64 && page_size == 16) return launch_t<64, 16>(p, stream, ap);
+  if (head_dim == 64 && page_size == 64) return launch_t<64, 64>(p, stream, ap);
+  if (head_dim == 128 && page_size == 16) return launch_t<128, 16>(p, stream, ap);
+  if (head_dim == 128 && page_size == 64) return launch_t<128, 64>(p, stream, ap);
   return hipErrorInvalidValue;
 }
 

@@ -19,6 +19,7 @@ struct Tuning {
   int32_t plan_direct = 0;     // 1 = kernels read the plan from the pinned staging slot, 0 = copy it first
   int32_t suffix_weight = 125; // split-K cost of a key tile past the prefix, in percent of a prefix tile
   int32_t compact_decode = 1;  // 1 = decode plans are uploaded in compact form
+  int32_t arg_plans = 1;       // 1 = extend plans of up to 16 KB travel in the kernel arguments
 };
 
 struct ExtendPlan {
