@@ -326,9 +326,13 @@ cw_status_t cw_check_block_table(const int32_t* block_table, int32_t bt_stride, 
  *                           sequences, beyond that as 0); 0 = its work items
  *                           are uploaded as they are.  Larger values act as 1.
  *   CW_TUNE_ARG_PLANS       1 = an extend plan of up to 16 KB (of an extend
- *                           call, or of a step without decodes) travels in the
- *                           kernel arguments of the extend and merge kernels,
- *                           with no upload kernel (the default); 0 = it is
+ *                           call, or of a step without decodes), and a decode
+ *                           plan whose compact form fits in 16 KB (of a decode
+ *                           call, or of a step without extends; about 250
+ *                           sequences), travel in the kernel arguments of the
+ *                           attention and merge kernels, with no upload kernel
+ *                           (the default; the kernels rebuild a compact plan's
+ *                           items and merge groups themselves); 0 = they are
  *                           uploaded like larger plans.  Larger values act as 1.
  * Returns CW_ERR_UNSUPPORTED for an unknown key or a negative value. */
 typedef enum {

@@ -238,6 +238,19 @@ bool compact_upload(const ExtendPlan& plan, size_t at, CompactUpload* cu) {
   return true;
 }
 
+// Writes the compact blob: the meta's head, the records, the tail order.
+template <class FillHead>
+void fill_compact(const CompactUpload& cu, uint8_t* h, FillHead&& fill_head) {
+  const ExtendPlan& cp = *cu.plan;
+  fill_head(h);
+  std::memcpy(h + cu.desc.rec_off, cp.recs.data(), cp.recs.size() * sizeof(DecodeRec));
+  std::memcpy(h + cu.desc.tail_off, cp.tails.data(), cp.tails.size() * sizeof(int32_t));
+}
+
+// Whether the compact blob and its ExpandDesc (at byte cu.bytes) fit the
+// kernel arguments.
+bool compact_arg_fits(const CompactUpload& cu) { return cu.bytes + sizeof(ExpandDesc) <= kArgPlanBytes; }
+
 // Waits until every workgroup of the upload kernel that last read `s` has
 // reported its reads (the done words at the slot's end).  The host runs up to
 // kStagingSlots calls ahead of the device, so this waits for the device to
@@ -276,12 +289,22 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
                              Launch&& launch, bool no_alloc, bool direct,
                              const CompactUpload* compact, FillHead&& fill_head, bool arg_plan = false) {
   if (bytes == 0) return launch(static_cast<const uint8_t*>(dst), nullptr);
-  if (arg_plan && !direct && bytes <= kArgPlanBytes) {
+  if (arg_plan && !direct) {
     // the plan travels in the kernel arguments: no slot, no upload kernel (and
-    // a captured launch keeps it by value)
-    ArgPlan ap;
-    fill(ap.bytes);
-    return launch(nullptr, &ap);
+    // a captured launch keeps it by value); a decode plan in compact form, with
+    // its ExpandDesc behind the records, else as it is
+    if (compact != nullptr && compact->plan != nullptr) {
+      if (compact_arg_fits(*compact)) {
+        ArgPlan ap;
+        fill_compact(*compact, ap.bytes, fill_head);
+        std::memcpy(ap.bytes + compact->bytes, &compact->desc, sizeof(ExpandDesc));
+        return launch(nullptr, &ap);
+      }
+    } else if (bytes <= kArgPlanBytes) {
+      ArgPlan ap;
+      fill(ap.bytes);
+      return launch(nullptr, &ap);
+    }
   }
   if (bytes > kPlanSlotBytes)
     return fail(CW_ERR_UNSUPPORTED,
@@ -326,10 +349,7 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
                            compact->bytes <= kPlanSlotBytes && compact->bytes < bytes;
   uint8_t* h = static_cast<uint8_t*>(s.host);
   if (use_compact) {
-    const ExtendPlan& cp = *compact->plan;
-    fill_head(h);
-    std::memcpy(h + compact->desc.rec_off, cp.recs.data(), cp.recs.size() * sizeof(DecodeRec));
-    std::memcpy(h + compact->desc.tail_off, cp.tails.data(), cp.tails.size() * sizeof(int32_t));
+    fill_compact(*compact, h, fill_head);
   } else {
     fill(h);
   }
@@ -657,8 +677,10 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     ev1 = g_ev_stop;
   }
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  CompactUpload cu;
+  const bool compact = decode && compact_upload(plan, 0, &cu);
   auto launch = [&](const uint8_t* meta, const ArgPlan* ap) -> cw_status_t {
-    if (ap != nullptr) {  // the plan is in the kernel arguments (extends only)
+    if (ap != nullptr) {  // the plan is in the kernel arguments (decodes: in compact form)
       p.seqs = nullptr;
       p.items = nullptr;
       p.groups = nullptr;
@@ -666,6 +688,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
       p.ap_items = static_cast<int32_t>(plan.off_items);
       p.ap_groups = static_cast<int32_t>(plan.off_groups);
       p.ap_wseqs = static_cast<int32_t>(plan.off_seqs);
+      p.ap_desc = decode ? static_cast<int32_t>(cu.bytes) : 0;
     } else {
       p.seqs = reinterpret_cast<const SeqInfo*>(meta + plan.off_seqs);
       p.items = reinterpret_cast<const WorkItem*>(meta + plan.off_items);
@@ -674,7 +697,7 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     if (write_pages) p.w.seqs = p.seqs;
     hipError_t e = hipSuccess;
     if (ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream);
+    if (decode) e = launch_decode(p, head_dim, page_size, fp8, stream, ap);
     else e = launch_extend(p, head_dim, page_size, fp8, stream, ap);
     if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
     if (ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -686,11 +709,10 @@ cw_status_t extend_impl(const void* q, const void* k_new, const void* v_new, voi
     }
     return CW_OK;
   };
-  CompactUpload cu;
-  const bool compact = decode && compact_upload(plan, 0, &cu);
+  const bool arg_plan = arg_plans() && (decode ? compact && compact_arg_fits(cu) : true);
   return stage_and_launch(plan.meta_bytes, ws, stream, [&](uint8_t* h) { pack_plan_meta(plan, h); },
                           launch, no_alloc, plan_direct(no_alloc), compact ? &cu : nullptr,
-                          [&](uint8_t* h) { pack_plan_head(plan, h); }, !decode && arg_plans());
+                          [&](uint8_t* h) { pack_plan_head(plan, h); }, arg_plan);
 }
 
 // Shared by both swap directions: validates and enqueues block src_ids[i] of
@@ -840,9 +862,12 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     ev1 = g_ev_stop;
   }
   const bool fp8 = kv_dtype == CW_KV_FP8_E4M3FN;
+  CompactUpload cu;
+  const bool compact = !sp.dec.empty() && compact_upload(sp.dec_plan, sp.off_dec_meta, &cu);
   auto launch = [&](const uint8_t* meta, const ArgPlan* ap) -> cw_status_t {
-    // with an argument plan (steps without decodes) the step's sequences sit at
-    // its byte 0 and the extend meta at off_ext_meta
+    // with an argument plan (steps of extends only, or of decodes only with the
+    // decode plan in compact form) the step's sequences sit at its byte 0, the
+    // extend meta at off_ext_meta and the decode meta at off_dec_meta
     w.seqs = ap != nullptr ? nullptr : reinterpret_cast<const SeqInfo*>(meta);
     hipError_t e = hipSuccess;
     // the timing events bracket the extend kernel, or the decode kernel of a
@@ -850,19 +875,24 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
     if (sp.ext.empty() && ev0 && (e = hipEventRecord(ev0, stream)) != hipSuccess)
       return hip_fail(e, "hipEventRecord");
     if (!sp.dec.empty()) {
-      ExtendParams pd = plan_params(sp.dec_plan, meta + sp.off_dec_meta, ws, sp.off_dec_part);
+      ExtendParams pd = plan_params(sp.dec_plan, ap != nullptr ? nullptr : meta + sp.off_dec_meta, ws,
+                                    sp.off_dec_part);
       common(pd);
       // without extends, the decode launch performs the page write (each
       // sequence's one new token, stored by the work item holding its key)
       if (sp.ext.empty()) pd.w = w;
-      if ((e = launch_decode(pd, head_dim, page_size, fp8, stream)) != hipSuccess)
+      if (ap != nullptr) {
+        pd.ap_seqs = static_cast<int32_t>(sp.off_dec_meta + sp.dec_plan.off_seqs);
+        pd.ap_desc = static_cast<int32_t>(cu.bytes);
+      }
+      if ((e = launch_decode(pd, head_dim, page_size, fp8, stream, ap)) != hipSuccess)
         return hip_fail(e, "decode kernel launch");
       if (sp.ext.empty() && ev1 && (e = hipEventRecord(ev1, stream)) != hipSuccess)
         return hip_fail(e, "hipEventRecord");
       if (pd.n_groups > 0) {
         int max_parts = 0;
         for (const CombineGroup& g : sp.dec_plan.groups) max_parts = std::max(max_parts, g.n_parts);
-        if ((e = launch_combine(pd, head_dim, max_parts, stream)) != hipSuccess)
+        if ((e = launch_combine(pd, head_dim, max_parts, stream, ap)) != hipSuccess)
           return hip_fail(e, "combine kernel launch");
       }
     }
@@ -901,15 +931,15 @@ cw_status_t step_impl(const void* q, const void* k_new, const void* v_new, void*
               reinterpret_cast<const uint8_t*>(sp.seqs.data() + sp.seqs.size()), h);
     if (!sp.ext.empty()) pack_plan_meta(sp.ext_plan, h + sp.off_ext_meta);
   };
-  CompactUpload cu;
-  const bool compact = !sp.dec.empty() && compact_upload(sp.dec_plan, sp.off_dec_meta, &cu);
+  const bool arg_plan =
+      arg_plans() && (sp.dec.empty() || (sp.ext.empty() && compact && compact_arg_fits(cu)));
   return stage_and_launch(sp.meta_bytes, ws, stream, [&](uint8_t* h) {
     head(h);
     if (!sp.dec.empty()) pack_plan_meta(sp.dec_plan, h + sp.off_dec_meta);
   }, launch, false, plan_direct(false), compact ? &cu : nullptr, [&](uint8_t* h) {
     head(h);
     pack_plan_head(sp.dec_plan, h + sp.off_dec_meta);
-  }, sp.dec.empty() && arg_plans());
+  }, arg_plan);
 }
 
 // Runs an entry point's body: a failed host allocation (or any other C++

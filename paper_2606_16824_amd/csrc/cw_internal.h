@@ -113,8 +113,10 @@ struct ExtendParams {
   int32_t n_groups;
   int32_t part_rows;  // rows per split-K partial slot (the row block for extend, G for decode)
   // with an argument plan: byte offsets in it of seqs, items, groups and the
-  // page write's seqs (the device pointers above are then unused)
-  int32_t ap_seqs, ap_items, ap_groups, ap_wseqs;
+  // page write's seqs (the device pointers above are then unused); a decode
+  // plan in compact form (plan_expand.h) has its ExpandDesc at ap_desc (> 0),
+  // and its items and groups are rebuilt from the records where they are read
+  int32_t ap_seqs, ap_items, ap_groups, ap_wseqs, ap_desc;
   WriteParams w;      // extend: also scatter the new K/V into the pools when w.total_tokens > 0
 };
 
@@ -150,7 +152,7 @@ hipError_t launch_extend_w64(const ExtendParams& p, int head_dim, int page_size,
 hipError_t launch_combine(const ExtendParams& p, int head_dim, int max_parts, hipStream_t stream,
                           const ArgPlan* ap = nullptr);
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
-                         hipStream_t stream);
+                         hipStream_t stream, const ArgPlan* ap = nullptr);
 int decode_keys_per_tile(int head_dim, bool fp8);
 int decode_waves_per_cu(bool fp8);  // resident decode waves per CU (LDS-bound)
 hipError_t launch_write_pages(const WriteParams& p, int head_dim, int page_size, bool fp8,

@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include "../cw_internal.h"
+#include "../plan_expand.h"
 
 namespace cw {
 namespace {
@@ -44,7 +45,18 @@ __global__ __launch_bounds__(256) void combine_kernel(ExtendParams p, PlanArg<AP
   const int grp = blockIdx.x / wg_per_group;
   const int rsub = threadIdx.x / (32 * SLICES);
   const int lr = (blockIdx.x % wg_per_group) * ROWS + rsub;
-  const CombineGroup cg = plan_ptr<AP>(ap, p.ap_groups, p.groups)[grp];
+  const CombineGroup cg = [&]() {
+    if constexpr (AP) {
+      if (p.ap_desc > 0) {  // a decode plan in compact form: the group is rebuilt (each wave searches)
+        const ExpandDesc& d = *reinterpret_cast<const ExpandDesc*>(ap.bytes + p.ap_desc);
+        const DecodeRec* rec = reinterpret_cast<const DecodeRec*>(ap.bytes + d.rec_off);
+        const int b = wave_last_at_most(d.n_seqs, grp, static_cast<int>(threadIdx.x % 64),
+                                        [&](int k) { return rec[k].group_off; });
+        return expand_group_at(rec, grp, b, d.rows);
+      }
+    }
+    return plan_ptr<AP>(ap, p.ap_groups, p.groups)[grp];
+  }();
   const bool active = lr < cg.rows;
   const int slice = (threadIdx.x / 32) % SLICES, d0 = (threadIdx.x % 32) * PER;
 

@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include "../cw_internal.h"
+#include "../plan_expand.h"
 #include "page_write.h"
 
 namespace cw {
@@ -136,8 +137,8 @@ __device__ __forceinline__ int v_swz8(int row) {
   return RB == 128 ? 2 * ((row >> 1) & 3) : 2 * ((row >> 2) & 1);
 }
 
-template <int D, int P, bool FP8>
-__global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
+template <int D, int P, bool FP8, bool AP>
+__global__ __launch_bounds__(64) void decode_kernel(ExtendParams p, PlanArg<AP> ap) {
   using T = DGeo<D, P, FP8>;
   // one array per stage; the tile loop is unrolled by the stage count, so
   // every step addresses a fixed array
@@ -146,9 +147,22 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds_s1[T::TILE];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_s2[T::TILE];
 
-  const WorkItem it = p.items[blockIdx.x];
+  WorkItem it;
+  if constexpr (AP) {
+    // the plan in the kernel arguments, in compact form: this item is rebuilt
+    // from the sequence records (the whole wave searches them)
+    const ExpandDesc& d = *reinterpret_cast<const ExpandDesc*>(ap.bytes + p.ap_desc);
+    const DecodeRec* rec = reinterpret_cast<const DecodeRec*>(ap.bytes + d.rec_off);
+    const int i = blockIdx.x;
+    const int b_full = i < d.n_full ? wave_last_at_most(d.n_seqs, i, static_cast<int>(threadIdx.x),
+                                                        [&](int k) { return rec[k].full_off; })
+                                    : 0;
+    it = expand_item_at(rec, reinterpret_cast<const int32_t*>(ap.bytes + d.tail_off), d, i, b_full);
+  } else {
+    it = p.items[blockIdx.x];
+  }
   if (it.seq < 0) return;
-  const SeqInfo sq = p.seqs[it.seq];
+  const SeqInfo sq = plan_ptr<AP>(ap, p.ap_seqs, p.seqs)[it.seq];
   const int lane = threadIdx.x;
   const int h = lane >> 5, col = lane & 31;
   const int G = p.gqa_group, hkv = p.num_kv_heads, hq = hkv * G;
@@ -471,8 +485,9 @@ __global__ __launch_bounds__(64) void decode_kernel(ExtendParams p) {
 }
 
 template <int D, int P, bool FP8>
-hipError_t launch_t(const ExtendParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_kernel<D, P, FP8>), dim3(p.n_items), dim3(64), 0, stream, p);
+hipError_t launch_t(const ExtendParams& p, hipStream_t stream, const ArgPlan* ap) {
+  if (ap) hipLaunchKernelGGL((decode_kernel<D, P, FP8, true>), dim3(p.n_items), dim3(64), 0, stream, p, *ap);
+  else hipLaunchKernelGGL((decode_kernel<D, P, FP8, false>), dim3(p.n_items), dim3(64), 0, stream, p, NoArgPlan{});
   return hipGetLastError();
 }
 
@@ -485,11 +500,11 @@ int decode_keys_per_tile(int head_dim, bool fp8) { return tile_bytes(fp8) / (2 *
 int decode_waves_per_cu(bool fp8) { return (160 * 1024) / (kStages * tile_bytes(fp8)); }  // 160 KB of LDS per CU
 
 hipError_t launch_decode(const ExtendParams& p, int head_dim, int page_size, bool fp8,
-                         hipStream_t stream) {
+                         hipStream_t stream, const ArgPlan* ap) {
   if (p.n_items <= 0) return hipSuccess;
 #define CW_CASE(D_, P_)                                                                   \
   if (head_dim == D_ && page_size == P_)                                                  \
-    return fp8 ? launch_t<D_, P_, true>(p, stream) : launch_t<D_, P_, false>(p, stream);
+    return fp8 ? launch_t<D_, P_, true>(p, stream, ap) : launch_t<D_, P_, false>(p, stream, ap);
   CW_CASE(64, 16)
   CW_CASE(64, 64)
   CW_CASE(128, 16)

@@ -54,14 +54,29 @@ __host__ __device__ inline int32_t last_at_most(int32_t n, int32_t x, Key key) {
   return lo;
 }
 
+// The same search by one whole wave (every lane active, `lane` its index):
+// the keys are non-decreasing, so the b with key(b) <= x are a prefix, and
+// their count less one is the result; 64 keys per load and ballot instead of
+// a chain of dependent loads.
+template <class Key>
+__device__ inline int32_t wave_last_at_most(int32_t n, int32_t x, int32_t lane, Key key) {
+  int32_t count = 0;
+  for (int32_t k0 = 0; k0 < n; k0 += 64) {
+    const int32_t k = k0 + lane;
+    count += __popcll(__ballot(k < n && key(k < n ? k : 0) <= x));
+  }
+  return __builtin_amdgcn_readfirstlane(count) - 1;
+}
+
 // Item i of the plan.  Full-length chunks: the sequence whose range holds i
 // (sequences without full chunks have empty ranges, so the last sequence that
-// starts at or before i is it); last chunks: the i-th of the tail order.
-__host__ __device__ inline WorkItem expand_item(const DecodeRec* rec, const int32_t* tails,
-                                                const ExpandDesc& d, int32_t i) {
+// starts at or before i is it), found by the caller as `b_full`; last chunks:
+// the i-th of the tail order.
+__host__ __device__ inline WorkItem expand_item_at(const DecodeRec* rec, const int32_t* tails,
+                                                   const ExpandDesc& d, int32_t i, int32_t b_full) {
   int32_t b, h, c;
   if (i < d.n_full) {
-    b = last_at_most(d.n_seqs, i, [&](int32_t k) { return rec[k].full_off; });
+    b = b_full;
     const int32_t r = i - rec[b].full_off;
     h = r / rec[b].full;
     c = r - h * rec[b].full;
@@ -86,21 +101,35 @@ __host__ __device__ inline WorkItem expand_item(const DecodeRec* rec, const int3
   return w;
 }
 
-// Merge group g: kv head h of a sequence cut into several chunks.
-__host__ __device__ inline CombineGroup expand_group(const DecodeRec* rec, const ExpandDesc& d, int32_t g) {
-  const int32_t b = last_at_most(d.n_seqs, g, [&](int32_t k) { return rec[k].group_off; });
+// The sequence of full-length chunk item i (i < d.n_full).
+__host__ __device__ inline int32_t full_item_seq(const DecodeRec* rec, const ExpandDesc& d, int32_t i) {
+  return last_at_most(d.n_seqs, i, [&](int32_t k) { return rec[k].full_off; });
+}
+
+__host__ __device__ inline WorkItem expand_item(const DecodeRec* rec, const int32_t* tails,
+                                                const ExpandDesc& d, int32_t i) {
+  return expand_item_at(rec, tails, d, i, i < d.n_full ? full_item_seq(rec, d, i) : 0);
+}
+
+// Merge group g: kv head h of a sequence cut into several chunks, the b-th
+// (the last sequence whose groups start at or before g).
+__host__ __device__ inline CombineGroup expand_group_at(const DecodeRec* rec, int32_t g, int32_t b, int32_t rows) {
   const DecodeRec& s = rec[b];
   const int32_t h = g - s.group_off;
   CombineGroup cg;
   cg.seq = b;
   cg.kvh = h;
   cg.q_row0 = 0;
-  cg.rows = d.rows;
+  cg.rows = rows;
   cg.part0 = s.part_off + h * s.nc;
   cg.n_parts = s.nc;
   cg.pad0 = 0;
   cg.pad1 = 0;
   return cg;
+}
+
+__host__ __device__ inline CombineGroup expand_group(const DecodeRec* rec, const ExpandDesc& d, int32_t g) {
+  return expand_group_at(rec, g, last_at_most(d.n_seqs, g, [&](int32_t k) { return rec[k].group_off; }), d.rows);
 }
 
 // Upload of a plan blob: its first `verbatim` bytes are copied as they are,
