@@ -51,11 +51,13 @@
  *
  * Graph capture: every call that runs kernels may be captured into a HIP graph
  * (hipStreamBeginCapture on `stream`).  A captured call carries its plan in
- * the arguments of small copy kernels (2 KiB each) instead of the staging
- * ring, so each replay writes the plan it was captured with into its
- * workspace; the lengths are those of capture time.  cw_init() must have been
- * called on the device first (CW_ERR_INIT), and a captured call's plan may
- * take at most 256 KiB (CW_ERR_UNSUPPORTED beyond).  The buffers of a captured
+ * kernel arguments, never in the staging ring: in those of its attention and
+ * merge kernels when the plan fits there (CW_TUNE_ARG_PLANS), else in those
+ * of small copy kernels (2 KiB each) that write it into the workspace at every
+ * replay; either way a replay runs with the plan it was captured with, and
+ * the lengths are those of capture time.  cw_init() must have been called on
+ * the device first (CW_ERR_INIT), and a plan that goes through the copy
+ * kernels may take at most 256 KiB (CW_ERR_UNSUPPORTED beyond).  The buffers of a captured
  * call must stay valid while the graph may be replayed, and a replay shares
  * its workspace (or the no-alloc scratch) with every other call using it, as
  * any call on the graph's stream would.
@@ -164,7 +166,8 @@ cw_status_t cw_extend_attention(const void* q, const void* k_new, const void* v_
  * shares that GPU's array: calls that may overlap on one GPU (different
  * streams, or different host threads) race and give wrong results; calls
  * ordered on one stream are safe.  Nothing in the array needs to start at
- * zero (each call uploads its plan and writes every partial it reads).
+ * zero (each call writes its plan there, unless it travels in the kernel
+ * arguments, and writes every partial it reads).
  * Results are bit-identical to cw_extend_attention with the same arguments. */
 #define CW_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 cw_status_t cw_extend_attention_noalloc(const void* q, const void* k_new, const void* v_new,
