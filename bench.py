@@ -49,8 +49,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="turn", choices=list(WORKLOAD_DESC))
-    ap.add_argument("--decode-steps", type=int, default=50,
-                    help="steps of the decode measurement added to an extend run (0 disables)")
+    ap.add_argument("--decode-steps", type=int, default=100,
+                    help="steps of the decode measurement added to an extend run, after as many "
+                         "warm-up steps as the main run (0 disables)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables)")
     ap.add_argument("--no-policy", dest="policy", action="store_false",
@@ -706,7 +707,7 @@ def main():
         result["power"] = power
     if not decode and args.decode_steps > 0:
         # the decode side of the metric: the mixed step's 48 decodes, fp8 pool
-        d = run_workload("decode", args.decode_steps, 10, cold_steps=args.cold_steps,
+        d = run_workload("decode", args.decode_steps, args.warmup, cold_steps=args.cold_steps,
                          power_s=args.power_seconds)
         if args.power_seconds > 0:
             result["power"]["decode"] = d.get("power")
