@@ -7,8 +7,9 @@ a compact decode plan's items and merge groups where they read them.
 CW_TUNE_ARG_PLANS 0 uploads every plan instead.  Each case runs both ways,
 bit-identical, and against the oracle: decode calls and steps of decodes only
 (bf16 and fp8 pools, split and unsplit sequences, one and many chunks per
-sequence), a decode call too large for the arguments (400 sequences, uploaded
-either way), extend calls and steps of extends only."""
+sequence), a decode call whose compact plan just fits the arguments (360
+sequences) and one too large for them (400 sequences, uploaded either way),
+extend calls and steps of extends only."""
 import numpy as np
 import pytest
 import torch
@@ -30,7 +31,9 @@ CASES = {
     "decode_d64_p64": ("decode", [63, 64, 65, 5000, 20000], None, 2, 8, 64, 64, "fp8"),
     "decode_step_bf16": ("step", [5, 700, 2000, 33, 12000], [1, 1, 1, 1, 1], 2, 4, 128, 16, "bf16"),
     "decode_step_fp8": ("step", [5, 700, 2000, 33, 12000], [1, 1, 1, 1, 1], 2, 4, 128, 16, "fp8"),
-    "decode_400": ("decode", None, None, 1, 4, 64, 16, "bf16"),
+    # 360 sequences: a compact plan of about 16 KB, the largest that fits the arguments
+    "decode_360": ("decode", 360, None, 1, 4, 64, 16, "bf16"),
+    "decode_400": ("decode", 400, None, 1, 4, 64, 16, "bf16"),
     "extend_bf16": ("extend", [700, 90, 3000], [150, 64, 300], 2, 4, 128, 16, "bf16"),
     "extend_step_fp8": ("step", [700, 0, 3000], [150, 64, 300], 2, 4, 128, 16, "fp8"),
 }
@@ -55,8 +58,8 @@ def _run(kind, spec, dw):
 @pytest.mark.parametrize("name", list(CASES))
 def test_arg_plan_matches_uploaded_plan(name):
     kind, lp, ls, hkv, g, d, p, dt = CASES[name]
-    if lp is None:
-        lp = [int(x) for x in np.random.default_rng(400).integers(0, 300, size=400)]
+    if isinstance(lp, int):
+        lp = [int(x) for x in np.random.default_rng(lp).integers(0, 300, size=lp)]
     if ls is None:
         ls = [1] * len(lp)
     spec = cw.custom_spec(lp, ls, num_kv_heads=hkv, gqa_group=g, head_dim=d, page_size=p, kv_dtype=dt,
