@@ -5,8 +5,9 @@
 // groups themselves, the plan upload can carry one record per sequence and the
 // order of the sequences' last chunks, and the upload kernel rebuilds the items
 // and groups on the device (a few KB over the host link instead of 32 bytes per
-// item).  The same functions rebuild them on the host, where the planner's own
-// items check them.
+// item); a compact plan small enough for the kernel arguments goes there, and
+// the decode and merge kernels rebuild their own item or group.  The same
+// functions rebuild them on the host, where the planner's own items check them.
 #pragma once
 
 #include <hip/hip_runtime.h>
