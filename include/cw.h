@@ -399,6 +399,11 @@ cw_status_t cw_init(void);
  * (kStagingSlots per initialised device; for tests that no call allocates). */
 int64_t cw_pinned_allocations(void);
 
+/* Number of calls in this process whose plan travelled in the kernel
+ * arguments (CW_TUNE_ARG_PLANS) rather than through the staging ring or the
+ * copy kernels of a captured call; for tests that a call took that path. */
+int64_t cw_arg_plan_calls(void);
+
 const char* cw_status_string(cw_status_t status);
 const char* cw_last_error_message(void);
 /* Library version, major * 10000 + minor * 100 + patch. */

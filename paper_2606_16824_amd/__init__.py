@@ -33,7 +33,7 @@ import torch
 
 from . import _lib as L
 
-__all__ = ["CWError", "init", "pinned_allocations", "extend_attention", "extend_attention_noalloc", "write_extend_attention", "decode_attention", "kv_write_pages",
+__all__ = ["CWError", "init", "pinned_allocations", "arg_plan_calls", "extend_attention", "extend_attention_noalloc", "write_extend_attention", "decode_attention", "kv_write_pages",
            "extend_workspace_bytes", "decode_workspace_bytes", "write_pages_workspace_bytes",
            "set_tuning", "plan_items", "decode_plan", "library", "kv_swap_out", "kv_swap_in", "swap_workspace_bytes",
            "step_attention", "step_workspace_bytes", "check_block_table", "ceiling_mfma_bf16", "ceiling_stream_read",
@@ -150,6 +150,11 @@ def init():
 def pinned_allocations() -> int:
     """Pinned host allocations the library has made in this process."""
     return int(library().cw_pinned_allocations())
+
+
+def arg_plan_calls() -> int:
+    """Calls whose plan travelled in the kernel arguments, in this process."""
+    return int(library().cw_arg_plan_calls())
 
 
 def _stream():

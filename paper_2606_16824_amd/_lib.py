@@ -59,6 +59,7 @@ SIGNATURES = {
                                               _vp, _i32, _i32, _i32, _i32, _i32, C.c_float, C.c_int,
                                               _vp, _vp, _vp]),
     "cw_pinned_allocations": (C.c_int64, []),
+    "cw_arg_plan_calls": (C.c_int64, []),
     "cw_status_string": (C.c_char_p, [C.c_int]),
     "cw_last_error_message": (C.c_char_p, []),
     "cw_version": (_i32, []),

@@ -109,6 +109,7 @@ struct DeviceState {
 
 DeviceState g_devices[kMaxDevices];
 std::atomic<int64_t> g_pinned_allocs{0};
+std::atomic<int64_t> g_arg_plan_calls{0};
 
 // Current device, or -1 when no GPU runtime is usable (host-only queries).
 int current_device() {
@@ -298,11 +299,13 @@ cw_status_t stage_and_launch(size_t bytes, void* dst, hipStream_t stream, Fill&&
         ArgPlan ap;
         fill_compact(*compact, ap.bytes, fill_head);
         std::memcpy(ap.bytes + compact->bytes, &compact->desc, sizeof(ExpandDesc));
+        g_arg_plan_calls.fetch_add(1);
         return launch(nullptr, &ap);
       }
     } else if (bytes <= kArgPlanBytes) {
       ArgPlan ap;
       fill(ap.bytes);
+      g_arg_plan_calls.fetch_add(1);
       return launch(nullptr, &ap);
     }
   }
@@ -1255,6 +1258,8 @@ cw_status_t cw_extend_attention_noalloc(const void* q, const void* k_new, const 
 }
 
 int64_t cw_pinned_allocations(void) { return g_pinned_allocs.load(); }
+
+int64_t cw_arg_plan_calls(void) { return g_arg_plan_calls.load(); }
 
 cw_status_t cw_set_tuning(cw_tune_key_t key, int32_t value) {
   if (value < 0) return fail(CW_ERR_UNSUPPORTED, "tuning value %d is negative", value);

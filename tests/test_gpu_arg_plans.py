@@ -24,8 +24,9 @@ pytestmark = pytest.mark.gpu
 
 ARG_PLANS = 7  # CW_TUNE_ARG_PLANS
 
+# name: (entry point, prefix lens, suffix lens, Hkv, G, D, P, kv); every case's
+# plan travels in the kernel arguments except decode_400's
 CASES = {
-    # name: (entry point, prefix lens, suffix lens, Hkv, G, D, P, kv)
     "decode_bf16": ("decode", [0, 1, 15, 300, 1023, 1025, 4000, 9000], None, 2, 4, 128, 16, "bf16"),
     "decode_fp8": ("decode", [0, 1, 15, 300, 1023, 1025, 4000, 9000], None, 2, 4, 128, 16, "fp8"),
     "decode_d64_p64": ("decode", [63, 64, 65, 5000, 20000], None, 2, 8, 64, 64, "fp8"),
@@ -69,12 +70,16 @@ def test_arg_plan_matches_uploaded_plan(name):
     dw = to_gpu(w)
     # a step of decodes only writes each new token into its page: start both runs from the same pools
     k0, v0 = dw.k_pool.clone(), dw.v_pool.clone()
+    n0 = cwlib.arg_plan_calls()
     out_a, lse_a = _run(kind, spec, dw)
+    assert cwlib.arg_plan_calls() - n0 == (0 if name == "decode_400" else 1), name
     dw.k_pool.copy_(k0)
     dw.v_pool.copy_(v0)
     cwlib.set_tuning(ARG_PLANS, 0)
     try:
+        n0 = cwlib.arg_plan_calls()
         out_u, lse_u = _run(kind, spec, dw)
+        assert cwlib.arg_plan_calls() == n0, name
     finally:
         cwlib.set_tuning(ARG_PLANS, 1)
     assert torch.equal(out_a.view(torch.int16), out_u.view(torch.int16)), name
